@@ -1,0 +1,264 @@
+"""Benchmark of the LUQ 4-bit backward hot path on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload resnet|mlp|mlp_smp|small]
+
+A step is one pass of the whole hot path over one batch of synthetic input,
+inputs resident in HBM:
+  LUQ of the neural gradient (row-major codes for dX, transposed for dW),
+  INT4 of the activations (+ 3x3 im2col on codes for the conv workload),
+  INT4 of the weights (transposed codes), the dX GEMM and the dW GEMM.
+
+Prints one JSON line.  `value` is roofline-normalised throughput: the sum,
+over the step's kernels, of each kernel's roofline time (algorithmic HBM
+bytes / 8 TB/s, or int8 MACs / 5 POPS, whichever is larger) divided by the
+measured step time, in percent.  Per-kernel GB/s and TOPS are listed too.
+`roofline` describes the dominant kernel, timed with HIP events on the
+stream it runs on; `cpu_baseline` times the CPU oracle on a bounded sample
+of the same workload.
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK = 8.0e12      # bytes/s
+I8_PEAK = 5.0e15       # int8 dense ops/s
+METRIC = "LUQ quantize GB/s + 4-bit bwd GEMM TFLOP/s (as % of roofline), 1 MI355X"
+
+
+def parse():
+    p = argparse.ArgumentParser()
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=20)
+    p.add_argument("--warmup", type=int, default=5)
+    p.add_argument("--workload", default="resnet", choices=["resnet", "mlp", "mlp_smp", "small"])
+    p.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
+    return p.parse_args()
+
+
+class Stage:
+    def __init__(self, name, fn, bytes_, ops=0.0):
+        self.name, self.fn, self.bytes, self.ops = name, fn, float(bytes_), float(ops)
+
+    def roofline_s(self):
+        return max(self.bytes / HBM_PEAK, self.ops / I8_PEAK)
+
+    def bound(self):
+        return "hbm" if self.bytes / HBM_PEAK >= self.ops / I8_PEAK else "mfma"
+
+
+def build_resnet(L, torch, dev):
+    import synth
+    p = synth.RESNET
+    B, H, W, C, Co = p["B"], p["H"], p["W"], p["C"], p["Cout"]
+    T, Ki = B * H * W, 9 * C
+    d = synth.resnet()
+    g = torch.from_numpy(d["g"]).to(dev)                              # [T, Cout]
+    act = torch.from_numpy(d["act"].reshape(T, C)).to(dev)            # NHWC as [T, C]
+    w = torch.from_numpy(d["W"]).to(dev)                              # [Cout, 9C]
+    u8 = lambda n: torch.empty(int(n), dtype=torch.uint8, device=dev)
+    f32 = lambda *s: torch.empty(*s, dtype=torch.float32, device=dev)
+    gc, gct, alpha, gmax = u8(L.plane_bytes(T * Co)), u8(L.plane_bytes(T * Co)), f32(1), f32(1)
+    ac, sa = u8(T * C // 2), f32(1)
+    colt = u8(Ki * T // 2)
+    wct, sw = u8(Co * Ki // 2), f32(1)
+    dx, dw = f32(T, Ki), f32(Co, Ki)
+    wsq = u8(L.workspace_size(L.OP_QUANTIZE_GRAD, T * Co))
+    wsa = u8(L.workspace_size(L.OP_INT4_QUANTIZE, T * C))
+    wsw = u8(L.workspace_size(L.OP_INT4_QUANTIZE, Co * Ki))
+    wsd = u8(max(L.workspace_size(L.OP_GEMM_DGRAD, T, Ki, Co), 1))
+    wsg = u8(max(L.workspace_size(L.OP_GEMM_WGRAD, T, Co, Ki), 1))
+    n_g, n_a, n_w = T * Co, T * C, Co * Ki
+    stages = [
+        Stage("luq_quantize_grad", lambda: L.luq_quantize_grad(g, 4, 0, 0, 1, gc, gct, alpha, gmax, wsq),
+              2 * 4 * n_g + 2 * n_g / 2),
+        Stage("int4_quantize(act)", lambda: L.int4_quantize(act, False, 0.0, ac, False, sa, wsa),
+              2 * 4 * n_a + n_a / 2),
+        Stage("int4_im2col3x3_t", lambda: L.int4_im2col3x3_t(ac, B, H, W, C, colt), n_a / 2 + Ki * T / 2),
+        Stage("int4_quantize(W)", lambda: L.int4_quantize(w, True, 0.0, False, wct, sw, wsw),
+              2 * 4 * n_w + n_w / 2),
+        Stage("luq_gemm_dgrad", lambda: L.luq_gemm_dgrad(gc, alpha, wct, sw, True, T, Ki, Co, 1, dx, wsd),
+              T * Co / 2 + Ki * Co / 2 + 4 * T * Ki, 2.0 * T * Ki * Co),
+        Stage("luq_gemm_wgrad", lambda: L.luq_gemm_wgrad(gct, alpha, colt, sa, False, T, Co, Ki, 1, dw, wsg),
+              Co * T / 2 + Ki * T / 2 + 4 * Co * Ki, 2.0 * T * Ki * Co),
+    ]
+    cfg = {"workload": "resnet50_conv3x3_bwd", "batch": B, "hw": [H, W], "cin": C, "cout": Co,
+           "gemm_dgrad_MNK": [T, Ki, Co], "gemm_wgrad_MNK": [Co, Ki, T], "grad": "lognormal(-12,2.5) fp32, 50% zeros",
+           "R": 4, "n_samples": 1}
+    return stages, cfg, d
+
+
+def build_mlp(L, torch, dev, ns=1, T=None, D=None, F=None):
+    import synth
+    T = T or synth.MLP["T"]
+    D = D or synth.MLP["D"]
+    F = F or synth.MLP["F"]
+    d = synth.mlp(T=T, D=D, F=F)
+    bf = lambda a: torch.from_numpy(a.view("int16")).to(dev).view(torch.bfloat16)
+    g, x = bf(d["g"]), bf(d["x"])                                     # [T, F], [T, D]
+    w = torch.from_numpy(d["W"]).to(dev)                              # [F, D]
+    u8 = lambda n: torch.empty(int(n), dtype=torch.uint8, device=dev)
+    f32 = lambda *s: torch.empty(*s, dtype=torch.float32, device=dev)
+    pb = L.plane_bytes(T * F)
+    gc, gct, alpha, gmax = u8(ns * pb), u8(ns * pb), f32(1), f32(1)
+    xct, sx = u8(T * D // 2), f32(1)
+    wct, sw = u8(F * D // 2), f32(1)
+    dx, dw = f32(T, D), f32(F, D)
+    wsq = u8(L.workspace_size(L.OP_QUANTIZE_GRAD, T * F))
+    wsx = u8(L.workspace_size(L.OP_INT4_QUANTIZE, T * D))
+    wsw = u8(L.workspace_size(L.OP_INT4_QUANTIZE, F * D))
+    wsd = u8(max(L.workspace_size(L.OP_GEMM_DGRAD, T, D, F), 1))
+    wsg = u8(max(L.workspace_size(L.OP_GEMM_WGRAD, T, F, D), 1))
+    n_g, n_x, n_w = T * F, T * D, F * D
+    stages = [
+        Stage("luq_quantize_grad", lambda: L.luq_quantize_grad(g, 4, 0, 0, ns, gc, gct, alpha, gmax, wsq),
+              2 * 2 * n_g + 2 * ns * n_g / 2),
+        Stage("int4_quantize(x)", lambda: L.int4_quantize(x, True, 0.0, False, xct, sx, wsx), 2 * 2 * n_x + n_x / 2),
+        Stage("int4_quantize(W)", lambda: L.int4_quantize(w, True, 0.0, False, wct, sw, wsw), 2 * 4 * n_w + n_w / 2),
+        Stage("luq_gemm_dgrad", lambda: L.luq_gemm_dgrad(gc, alpha, wct, sw, True, T, D, F, ns, dx, wsd),
+              ns * T * F / 2 + D * F / 2 + 4 * T * D, 2.0 * T * D * F),
+        Stage("luq_gemm_wgrad", lambda: L.luq_gemm_wgrad(gct, alpha, xct, sx, True, T, F, D, ns, dw, wsg),
+              ns * F * T / 2 + D * T / 2 + 4 * F * D, 2.0 * T * D * F),
+    ]
+    cfg = {"workload": "transformer_mlp_bwd" + ("_smp2" if ns == 2 else ""), "tokens": T, "d_model": D,
+           "hidden": F, "grad": "lognormal(-14,3) bf16", "R": 4, "n_samples": ns}
+    return stages, cfg, d
+
+
+def time_stages(torch, stages, steps, warmup):
+    def step():
+        for s in stages:
+            s.fn()
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record()
+    for _ in range(steps):
+        step()
+    e1.record()
+    torch.cuda.synchronize()
+    step_s = e0.elapsed_time(e1) / 1e3 / steps
+    per = {}
+    reps = max(3, steps)
+    for s in stages:
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        for _ in range(reps):
+            s.fn()
+        b.record()
+        torch.cuda.synchronize()
+        per[s.name] = a.elapsed_time(b) / 1e3 / reps
+    return step_s, per
+
+
+def cpu_baseline(workload, d):
+    """The oracle on a bounded sample of the workload (10-30 s of CPU work)."""
+    import numpy as np
+    from threadpoolctl import threadpool_info
+    from oracle import luq as oluq, int4 as oint4, gemm as ogemm, im2col as oim2col
+    import synth
+    t_roof, t_cpu, parts = 0.0, 0.0, []
+
+    def timed(label, fn, bytes_, ops=0.0):
+        nonlocal t_roof, t_cpu
+        t0 = time.perf_counter()
+        fn()
+        dt = time.perf_counter() - t0
+        t_cpu += dt
+        t_roof += max(bytes_ / HBM_PEAK, ops / I8_PEAK)
+        parts.append(f"{label} {dt:.2f}s")
+
+    if workload == "resnet":
+        p = synth.RESNET
+        C, Co = p["C"], p["Cout"]
+        n = 1 << 20
+        g = d["g"].reshape(-1)[:n]
+        timed("luq 2^20", lambda: oluq.luq_quantize(g, R=4), 2 * 4 * n + n / 2)
+        act = d["act"].reshape(-1)[:n]
+        timed("int4 2^20", lambda: oint4.int4_quantize(act, is_signed=False), 2 * 4 * n + n / 2)
+        img = d["act"][:2]
+        codes, _ = oint4.int4_quantize(img, is_signed=False)
+        timed("im2col 2 images", lambda: oim2col.im2col3x3_codes(codes, 2, p["H"], p["W"], C),
+              img.size / 2 + 9 * img.size / 2)
+        gcodes, alpha, _ = oluq.luq_quantize(d["g"][:8192], R=4)
+        K, N = Co, 9 * C
+        wcn, wsn = oint4.int4_quantize(np.ascontiguousarray(d["W"]), is_signed=True)  # [Co, 9C] = [K, N]
+        timed("dgrad 8192 rows", lambda: ogemm.gemm_dgrad_ref(gcodes, alpha, wcn, wsn, True, 8192, N, K),
+              8192 * K / 2 + 4 * 8192 * N, 2.0 * 8192 * N * K)
+        colc = oim2col.im2col3x3_codes(codes, 2, p["H"], p["W"], C)
+        gc2, a2, _ = oluq.luq_quantize(d["g"][: 2 * p["H"] * p["W"]], R=4)
+        T2 = 2 * p["H"] * p["W"]
+        timed("wgrad 2 images", lambda: ogemm.gemm_wgrad_ref(gc2, a2, colc, 1.0, False, T2, Co, N),
+              T2 * (Co + N) / 2, 2.0 * T2 * Co * N)
+        sample = "LUQ and INT4 on 2^20 elements, im2col and dW on 2 images, dX on 8192 rows"
+    else:
+        n = 1 << 20
+        g = d["g"].reshape(-1)[:n]
+        timed("luq 2^20 bf16", lambda: oluq.luq_quantize(g, dtype="bf16", R=4), 2 * 2 * n + n / 2)
+        x = d["x"].reshape(-1)[:n]
+        timed("int4 2^20 bf16", lambda: oint4.int4_quantize(x, dtype="bf16"), 2 * 2 * n + n / 2)
+        F = d["g"].shape[1]
+        D = d["x"].shape[1]
+        rows = 64
+        gcodes, alpha, _ = oluq.luq_quantize(d["g"][:rows], dtype="bf16", R=4)
+        wc, ws = oint4.int4_quantize(d["W"], is_signed=True)             # [F, D] = [K, N]
+        timed(f"dgrad {rows} rows", lambda: ogemm.gemm_dgrad_ref(gcodes, alpha, wc, ws, True, rows, D, F),
+              rows * F / 2 + 4 * rows * D, 2.0 * rows * D * F)
+        sample = f"LUQ and INT4 on 2^20 elements, dX on {rows} token rows"
+    blas = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    return {"value": 100.0 * t_roof / t_cpu, "unit": "% of MI355X roofline", "cores": int(blas),
+            "kind": "oracle", "sample": sample + "; " + ", ".join(parts),
+            "cpu_seconds": round(t_cpu, 3)}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(json.dumps({"error": "this build measures one GPU only; --gpus must be 1"}))
+        sys.exit(2)
+    import torch
+    import paper_2112_10769_amd as L
+    dev = torch.device("cuda:0")
+    if args.workload == "resnet":
+        stages, cfg, d = build_resnet(L, torch, dev)
+    elif args.workload == "small":
+        stages, cfg, d = build_mlp(L, torch, dev, 1, T=256, D=512, F=512)
+        cfg["workload"] = "linear_256x512x512_bwd"
+    else:
+        stages, cfg, d = build_mlp(L, torch, dev, 2 if args.workload == "mlp_smp" else 1)
+    step_s, per = time_stages(torch, stages, args.steps, args.warmup)
+    roof_total = sum(s.roofline_s() for s in stages)
+    kernels = {}
+    for s in stages:
+        t = per[s.name]
+        kernels[s.name] = {"us": round(t * 1e6, 2), "GB/s": round(s.bytes / t / 1e9, 1),
+                           "TOPS": round(s.ops / t / 1e12, 1) if s.ops else None,
+                           "bound": s.bound(), "frac": round(s.roofline_s() / t, 4)}
+    dom = max(stages, key=lambda s: per[s.name])
+    t = per[dom.name]
+    if dom.bound() == "hbm":
+        roof = {"kernel": dom.name, "bound": "hbm", "achieved": round(dom.bytes / t / 1e9, 1), "peak": 8000.0,
+                "unit": "GB/s", "frac": round(dom.bytes / t / HBM_PEAK, 4), "traffic": None}
+    else:
+        roof = {"kernel": dom.name, "bound": "mfma", "achieved": round(dom.ops / t / 1e12, 1), "peak": 5000.0,
+                "unit": "TFLOP/s", "frac": round(dom.ops / t / I8_PEAK, 4), "traffic": None}
+    out = {
+        "metric": METRIC, "value": round(100.0 * roof_total / step_s, 2), "unit": "% of roofline",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(step_s * 1e3, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "int8-mfma/int32",
+        "data": "synthetic", "config": cfg, "roofline": roof, "kernels": kernels,
+        "roofline_step_us": round(roof_total * 1e6, 2),
+    }
+    if not args.no_cpu:
+        out["cpu_baseline"] = cpu_baseline("resnet" if args.workload == "resnet" else "mlp", d)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

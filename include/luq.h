@@ -1,0 +1,209 @@
+/*
+ * luq.h -- C ABI of libluq: 4-bit LUQ training GEMM hot path on AMD MI355X.
+ *
+ * Method: "Accurate Neural Training with 4-bit Matrix Multiplications at
+ * Standard Formats" (Chmiel, Banner, Hoffer, Ben Yaacov, Soudry; arXiv
+ * 2112.10769).  Neural gradients are quantized with logarithmic unbiased
+ * quantization (LUQ, Section 4) to a radix-2 FP4 [sign, 3-bit exponent, no
+ * mantissa] code; weights and activations with a uniform INT4
+ * round-to-nearest quantizer (Section 3.3, Appendix A.1); the backward and
+ * update GEMMs of Eqs. backward / update then run on the 4-bit codes with
+ * the per-tensor scales applied once to each sum (Appendix A.1).
+ *
+ * General conventions
+ *  - Every pointer argument is DEVICE memory owned by the caller, except
+ *    where noted.  The library never allocates or frees memory; it keeps no
+ *    state between calls.
+ *  - All work is enqueued asynchronously on `stream` (a hipStream_t; NULL is
+ *    the null stream).  No call synchronizes with the host.
+ *  - Scales (alpha, s) live in device memory: no host round trip.
+ *  - Argument errors are detected on the host, before anything is enqueued,
+ *    and returned as a luq_status; nothing is launched in that case.
+ *    luq_last_error() then holds a message (thread-local).
+ *  - Data errors (a non-finite input element) are reported through the
+ *    outputs: the scale becomes NaN and every code 0.
+ *  - Base pointers must be 16-byte aligned (LUQ_ERR_ALIGN otherwise).
+ *
+ * Code formats (two 4-bit codes per byte, element 2b in the low nibble)
+ *  - LUQ nibble: bit 3 = sign, bits 2..0 = exponent field e.  e = 0 is zero
+ *    (sign bit always 0); e >= 1 decodes to (-1)^sign * alpha * 2^(e-1).
+ *    Field 011 is the paper's FP4 value 4 (Appendix A.8.1 worked example).
+ *  - INT4 nibble: signed codes -7..7 in two's complement, or unsigned codes
+ *    0..15; the value is s * q.
+ *  - A matrix of codes is stored row-major, each row packed along its
+ *    columns.  "codes" is the [rows][cols] layout, "codes_t" the transposed
+ *    [cols][rows] layout of the same codes.
+ *  - LUQ SMP planes (Section 5.1: n independent samples with one alpha) are
+ *    stored one after another, each plane luq_plane_bytes(rows*cols) bytes
+ *    apart.
+ */
+#ifndef LUQ_H
+#define LUQ_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define LUQ_ABI_VERSION 1
+
+typedef int luq_status;
+enum {
+  LUQ_OK = 0,
+  LUQ_ERR_NULL = 1,      /* a required pointer is NULL                       */
+  LUQ_ERR_SHAPE = 2,     /* a size is negative or breaks a layout rule      */
+  LUQ_ERR_DTYPE = 3,     /* unknown luq_dtype                                */
+  LUQ_ERR_PARAM = 4,     /* R, n_samples or another parameter out of range   */
+  LUQ_ERR_WORKSPACE = 5, /* workspace missing or smaller than required       */
+  LUQ_ERR_ALIGN = 6,     /* a pointer is not 16-byte aligned                 */
+  LUQ_ERR_HIP = 7        /* the HIP runtime rejected a launch                */
+};
+
+typedef enum { LUQ_F32 = 0, LUQ_BF16 = 1 } luq_dtype;
+
+/* Operation ids for luq_workspace_size. */
+enum {
+  LUQ_OP_QUANTIZE_GRAD = 0, /* d0 = number of elements                     */
+  LUQ_OP_INT4_QUANTIZE = 1, /* d0 = number of elements                     */
+  LUQ_OP_GEMM_DGRAD = 2,    /* d0 = M, d1 = N, d2 = K                        */
+  LUQ_OP_GEMM_WGRAD = 3     /* d0 = T, d1 = Nout, d2 = Kin                   */
+};
+
+/* ABI version of the loaded library (LUQ_ABI_VERSION of its build). */
+int luq_abi_version(void);
+
+/* Static description of a status code. */
+const char* luq_status_string(luq_status status);
+
+/* Detail of the last error returned on the calling thread ("" if none). */
+const char* luq_last_error(void);
+
+/* Bytes between consecutive SMP planes of a code tensor of n elements:
+ * ceil(n/2) rounded up to a multiple of 256. */
+size_t luq_plane_bytes(int64_t n);
+
+/* Device workspace (bytes) an operation needs; 0 if none.  The workspace
+ * holds per-block partial maxima (quantizers) or split-K partial sums
+ * (GEMMs); its contents on entry do not matter. */
+size_t luq_workspace_size(int op, int64_t d0, int64_t d1, int64_t d2);
+
+/*
+ * luq_quantize_grad -- LUQ of a neural-gradient tensor (Section 4).
+ *
+ * Computes m = max|g|, alpha = fl32(m / 2^R) (Eq. alpha; R = 2^(b-1) = 4 for
+ * FP4 with b = 3 exponent bits), and for every element and SMP sample s the
+ * code of X_q = Q_alpha(T_alpha(g)): stochastic underflow below alpha
+ * (Eq. StochasticPruning) and logarithmic stochastic rounding between
+ * adjacent levels alpha*2^n (Eq. unbiasedFpQ).  One 16-bit uniform j per
+ * element and sample comes from Philox4x32-10 with key = (seed lo, seed hi)
+ * and counter = (blk lo, blk hi, s, counter), blk = i >> 3 for the row-major
+ * flat index i; word (i >> 1) & 3, half i & 1.  With w the bin width and d
+ * the distance of |g| above the bin's lower level, the value rounds up iff
+ * j * w < d * 2^16 (exactly), so 0 <= E[Q(g)] - g < w * 2^-16.
+ *
+ *  g        [rows][cols] row-major, dtype dt (LUQ_F32 or LUQ_BF16).
+ *  rows, cols  >= 0.  For rows > 1, cols must be even.  When codes_t is
+ *           requested, rows and cols must be multiples of 8.
+ *  R        4, 5 or 6: levels alpha * 2^n for n = 0..R.
+ *  seed, counter  Philox key and step counter; the codes are a pure
+ *           function of (g, R, seed, counter, sample).
+ *  n_samples  1 or 2 (SMP planes, Section 5.1).  2 requires R <= 5 so that
+ *           the sum of two decoded planes fits an int8 (|sum| <= 2^(R+1)).
+ *  codes    out: n_samples planes of [rows][cols] codes (row stride
+ *           ceil(cols/2) bytes), or NULL.
+ *  codes_t  out: n_samples planes of the transposed [cols][rows] codes (row
+ *           stride rows/2 bytes), or NULL.  At least one of codes, codes_t.
+ *  alpha    out: 1 float.  0 when max|g| = 0 (all codes 0); NaN when g has
+ *           a non-finite element (all codes 0).
+ *  maxabs   out: 1 float, max|g| (non-finite when g is), or NULL.
+ *  ws       workspace of luq_workspace_size(LUQ_OP_QUANTIZE_GRAD, rows*cols).
+ */
+luq_status luq_quantize_grad(const void* g, luq_dtype dt, int64_t rows, int64_t cols, int R,
+                             uint64_t seed, uint32_t counter, int n_samples, uint8_t* codes,
+                             uint8_t* codes_t, float* alpha, float* maxabs, void* ws,
+                             size_t ws_bytes, void* stream);
+
+/*
+ * int4_quantize -- uniform INT4 round-to-nearest quantizer (Section 3.3;
+ * scale alpha = Delta / (2^b - 1) of Appendix A.1; Delta = max-abs or clip,
+ * since the SAWB coefficients the paper used are not given).
+ *
+ *  m = clip if clip > 0, else max|x| (signed) or max(max x, 0) (unsigned).
+ *  Q = 7 (signed, codes -7..7) or 15 (unsigned, codes 0..15).
+ *  inv = fl32(Q / m), s = fl32(m / Q), q = clamp(rne(fl32(x * inv))), with a
+ *  NaN product (0 * inf for tiny m) giving q = 0.  m = 0: s = 0, codes 0.
+ *  Non-finite x (when clip <= 0): s = NaN, codes 0.
+ *
+ *  x        [rows][cols] row-major, dtype dt.  Shape rules as for
+ *           luq_quantize_grad.
+ *  codes, codes_t  out: [rows][cols] and/or [cols][rows] codes (one may be
+ *           NULL, not both).
+ *  scale    out: 1 float s.
+ *  ws       workspace of luq_workspace_size(LUQ_OP_INT4_QUANTIZE, rows*cols)
+ *           (may be NULL when clip > 0).
+ */
+luq_status int4_quantize(const void* x, luq_dtype dt, int64_t rows, int64_t cols, int is_signed,
+                         float clip, uint8_t* codes, uint8_t* codes_t, float* scale, void* ws,
+                         size_t ws_bytes, void* stream);
+
+/*
+ * luq_gemm_dgrad -- the backward GEMM of Eq. backward on codes:
+ *   dx[m][n] = (alpha / n_samples) * w_scale * sum_k (sum_s cg_s[m][k]) * cw[n][k]
+ * i.e. dX = Q(g) Q(W) with g [M tokens][K out-features] and the weight
+ * W [K out][N in] given TRANSPOSED as w_codes_t [N][K] (the codes_t output of
+ * int4_quantize on W).  SMP planes are summed exactly before the MACs
+ * (Section 5.1 average).  Integer MACs accumulate exactly in int32; the
+ * scales are applied once in fp32 (Appendix A.1).
+ *
+ *  g_codes    n_samples planes of [M][K] LUQ codes (plane stride
+ *             luq_plane_bytes(M*K)).
+ *  alpha      1 float (device), the LUQ alpha of g.
+ *  w_codes_t  [N][K] INT4 codes; w_scale 1 float (device); w_signed 0/1.
+ *  M, N >= 1; K >= 32 and a multiple of 32.  Reductions longer than the
+ *             int32-exact length are split internally and the partial sums
+ *             combined exactly, so any K is exact.  The codes must come from
+ *             this library: with n_samples = 2 every field must be <= 6
+ *             (R <= 5), which luq_quantize_grad enforces.
+ *  dx         out: [M][N] fp32, row-major.
+ *  ws         workspace of luq_workspace_size(LUQ_OP_GEMM_DGRAD, M, N, K).
+ */
+luq_status luq_gemm_dgrad(const uint8_t* g_codes, const float* alpha, int n_samples,
+                          const uint8_t* w_codes_t, const float* w_scale, int w_signed,
+                          int64_t M, int64_t N, int64_t K, float* dx, void* ws, size_t ws_bytes,
+                          void* stream);
+
+/*
+ * luq_gemm_wgrad -- the update GEMM of Eq. update on codes:
+ *   dw[o][i] = (alpha / n_samples) * a_scale * sum_t (sum_s cg_s[t][o]) * ca[t][i]
+ * i.e. dW = Q(g)^T Q(a) in the torch weight-gradient layout [Nout][Kin], with
+ * both operands given TRANSPOSED (tokens innermost): g_codes_t [Nout][T]
+ * (codes_t of luq_quantize_grad on g [T][Nout]) and a_codes_t [Kin][T].
+ * Long reductions are split over T with exact int32 partial sums combined
+ * in a fixed order, so the result does not depend on the split.
+ *
+ *  T >= 32 and a multiple of 32; Nout, Kin >= 1.
+ *  ws  workspace of luq_workspace_size(LUQ_OP_GEMM_WGRAD, T, Nout, Kin).
+ */
+luq_status luq_gemm_wgrad(const uint8_t* g_codes_t, const float* alpha, int n_samples,
+                          const uint8_t* a_codes_t, const float* a_scale, int a_signed, int64_t T,
+                          int64_t Nout, int64_t Kin, float* dw, void* ws, size_t ws_bytes,
+                          void* stream);
+
+/*
+ * int4_im2col3x3_t -- lowering of a 3x3 / stride 1 / zero-pad 1 convolution
+ * on INT4 codes, written transposed for luq_gemm_wgrad: for activation codes
+ * act [B][H][W][C] (NHWC, packed along C), writes
+ *   col_t[(kh*3 + kw)*C + c][t] = act[b][y+kh-1][x+kw-1][c]   (0 off-image)
+ * for t = (b*H + y)*W + x, packed along t (row stride T/2 bytes, T = B*H*W).
+ * C must be even and T a multiple of 8.
+ */
+luq_status int4_im2col3x3_t(const uint8_t* act_codes, int64_t B, int64_t H, int64_t W, int64_t C,
+                            uint8_t* col_t, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* LUQ_H */

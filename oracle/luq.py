@@ -136,13 +136,23 @@ def luq_quantize(x, dtype="f32", R=4, seed=0, counter=0, n_samples=1):
     alpha = luq_alpha(maxabs, R)
     if alpha == 0:
         return codes, alpha, maxabs
-    sign = np.signbit(xf)
     for s in range(n_samples):
-        j = luq_uniforms(N, seed, counter, s)
-        e = luq_fields(a, alpha, R, j)
-        nib = e | np.where((e != 0) & sign, 8, 0).astype(np.uint8)
-        codes[s] = pack_nibbles(nib)
+        codes[s] = pack_nibbles(luq_nibbles_range(xf, 0, alpha, R, seed, counter, s))
     return codes, alpha, maxabs
+
+
+def luq_nibbles_range(xf, start, alpha, R, seed, counter, sample):
+    """Unpacked codes of the elements start .. start+len(xf)-1 of a tensor
+    whose alpha is already known (xf: their float32 values).  The codes of a
+    slice equal the slice of the whole tensor's codes: the uniforms depend
+    only on the element's flat index."""
+    xf = np.asarray(xf, dtype=np.float32).ravel()
+    if not (float(alpha) > 0):  # zero or NaN alpha: all codes 0
+        return np.zeros(xf.size, dtype=np.uint8)
+    a = np.abs(xf.astype(np.float64))
+    j = luq_uniforms(xf.size, seed, counter, sample, start=start)
+    e = luq_fields(a, alpha, R, j)
+    return e | np.where((e != 0) & np.signbit(xf), 8, 0).astype(np.uint8)
 
 
 def luq_decode_int(codes, n):

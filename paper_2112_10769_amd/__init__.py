@@ -1,0 +1,192 @@
+"""Python binding of libluq (the LUQ 4-bit backward hot path on MI355X).
+
+Argument marshalling only: torch tensors supply device memory and the
+current HIP stream; every step runs in the HIP kernels of libluq.so.  The
+functions carry the names of the C ABI in include/luq.h.  Outputs that are
+not passed in are allocated with torch on the input's device.
+
+The library must have been built (``python -m paper_2112_10769_amd._build``
+or ``__graft_entry__.build()``); importing the binding without it raises.
+"""
+import ctypes
+import os
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libluq.so")
+
+LUQ_OK = 0
+LUQ_F32, LUQ_BF16 = 0, 1
+OP_QUANTIZE_GRAD, OP_INT4_QUANTIZE, OP_GEMM_DGRAD, OP_GEMM_WGRAD = 0, 1, 2, 3
+
+EXPORTS = (
+    "luq_abi_version", "luq_status_string", "luq_last_error", "luq_plane_bytes",
+    "luq_workspace_size", "luq_quantize_grad", "int4_quantize", "luq_gemm_dgrad",
+    "luq_gemm_wgrad", "int4_im2col3x3_t",
+)
+
+
+class LuqError(RuntimeError):
+    def __init__(self, status, where, detail):
+        super().__init__(f"{where}: status {status} ({detail})")
+        self.status = status
+
+
+def _load():
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"libluq.so not built at {LIB_PATH}; run __graft_entry__.build()")
+    lib = ctypes.CDLL(LIB_PATH)
+    vp, i64, u64, u32, i32, f32, sz = (ctypes.c_void_p, ctypes.c_int64, ctypes.c_uint64,
+                                       ctypes.c_uint32, ctypes.c_int, ctypes.c_float, ctypes.c_size_t)
+    lib.luq_abi_version.restype = i32
+    lib.luq_status_string.restype = ctypes.c_char_p
+    lib.luq_status_string.argtypes = [i32]
+    lib.luq_last_error.restype = ctypes.c_char_p
+    lib.luq_plane_bytes.restype = sz
+    lib.luq_plane_bytes.argtypes = [i64]
+    lib.luq_workspace_size.restype = sz
+    lib.luq_workspace_size.argtypes = [i32, i64, i64, i64]
+    lib.luq_quantize_grad.restype = i32
+    lib.luq_quantize_grad.argtypes = [vp, i32, i64, i64, i32, u64, u32, i32, vp, vp, vp, vp, vp, sz, vp]
+    lib.int4_quantize.restype = i32
+    lib.int4_quantize.argtypes = [vp, i32, i64, i64, i32, f32, vp, vp, vp, vp, sz, vp]
+    lib.luq_gemm_dgrad.restype = i32
+    lib.luq_gemm_dgrad.argtypes = [vp, vp, i32, vp, vp, i32, i64, i64, i64, vp, vp, sz, vp]
+    lib.luq_gemm_wgrad.restype = i32
+    lib.luq_gemm_wgrad.argtypes = [vp, vp, i32, vp, vp, i32, i64, i64, i64, vp, vp, sz, vp]
+    lib.int4_im2col3x3_t.restype = i32
+    lib.int4_im2col3x3_t.argtypes = [vp, i64, i64, i64, i64, vp, vp]
+    return lib
+
+
+LIB = _load()
+
+
+def _check(status, where):
+    if status != LUQ_OK:
+        detail = LIB.luq_last_error().decode() or LIB.luq_status_string(status).decode()
+        raise LuqError(status, where, detail)
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(dev):
+    return ctypes.c_void_p(torch.cuda.current_stream(dev).cuda_stream)
+
+
+def _dtype(t):
+    if t.dtype == torch.float32:
+        return LUQ_F32
+    if t.dtype == torch.bfloat16:
+        return LUQ_BF16
+    raise TypeError(f"unsupported dtype {t.dtype}")
+
+
+def abi_version():
+    return LIB.luq_abi_version()
+
+
+def plane_bytes(n):
+    return int(LIB.luq_plane_bytes(n))
+
+
+def workspace_size(op, d0, d1=0, d2=0):
+    return int(LIB.luq_workspace_size(op, d0, d1, d2))
+
+
+def _bytes(n, dev):
+    return torch.empty(max(int(n), 1), dtype=torch.uint8, device=dev)
+
+
+def _shape2d(x):
+    if x.dim() == 1:
+        return 1, x.shape[0]
+    return x.shape[0], x.numel() // max(x.shape[0], 1)
+
+
+def luq_quantize_grad(g, R=4, seed=0, counter=0, n_samples=1, codes=True, codes_t=False,
+                      alpha=None, maxabs=None, ws=None):
+    """LUQ codes of g (2-D [rows, cols] or 1-D).  codes / codes_t: True to
+    allocate, a uint8 tensor to write into, or False.  Returns
+    (codes, codes_t, alpha, maxabs) with codes of shape [n_samples, plane]."""
+    rows, cols = _shape2d(g)
+    n = rows * cols
+    dev = g.device
+    pb = plane_bytes(n)
+    if codes is True:
+        codes = _bytes(n_samples * pb, dev).view(n_samples, -1) if n else _bytes(1, dev)
+    if codes_t is True:
+        codes_t = _bytes(n_samples * pb, dev).view(n_samples, -1) if n else _bytes(1, dev)
+    codes = codes if codes is not False else None
+    codes_t = codes_t if codes_t is not False else None
+    alpha = torch.empty(1, dtype=torch.float32, device=dev) if alpha is None else alpha
+    maxabs = torch.empty(1, dtype=torch.float32, device=dev) if maxabs is None else maxabs
+    wsb = workspace_size(OP_QUANTIZE_GRAD, n)
+    ws = _bytes(wsb, dev) if ws is None else ws
+    g = g.contiguous()
+    st = LIB.luq_quantize_grad(_ptr(g) if n else None, _dtype(g), rows, cols, R,
+                               seed & (2**64 - 1), counter & 0xFFFFFFFF, n_samples,
+                               _ptr(codes), _ptr(codes_t), _ptr(alpha), _ptr(maxabs), _ptr(ws),
+                               ws.numel(), _stream(dev))
+    _check(st, "luq_quantize_grad")
+    return codes, codes_t, alpha, maxabs
+
+
+def int4_quantize(x, is_signed=True, clip=0.0, codes=True, codes_t=False, scale=None, ws=None):
+    """INT4 codes of x.  Returns (codes, codes_t, scale)."""
+    rows, cols = _shape2d(x)
+    n = rows * cols
+    dev = x.device
+    nb = (n + 1) // 2
+    if codes is True:
+        codes = _bytes(nb, dev)
+    if codes_t is True:
+        codes_t = _bytes(nb, dev)
+    codes = codes if codes is not False else None
+    codes_t = codes_t if codes_t is not False else None
+    scale = torch.empty(1, dtype=torch.float32, device=dev) if scale is None else scale
+    wsb = workspace_size(OP_INT4_QUANTIZE, n)
+    ws = _bytes(wsb, dev) if ws is None else ws
+    x = x.contiguous()
+    st = LIB.int4_quantize(_ptr(x) if n else None, _dtype(x), rows, cols,
+                           1 if is_signed else 0, float(clip), _ptr(codes), _ptr(codes_t),
+                           _ptr(scale), _ptr(ws), ws.numel(), _stream(dev))
+    _check(st, "int4_quantize")
+    return codes, codes_t, scale
+
+
+def luq_gemm_dgrad(g_codes, alpha, w_codes_t, w_scale, w_signed, M, N, K, n_samples=1, dx=None, ws=None):
+    """dX [M, N] = Q(g) Q(W) from g codes [M, K] and transposed W codes [N, K]."""
+    dev = g_codes.device
+    dx = torch.empty(M, N, dtype=torch.float32, device=dev) if dx is None else dx
+    wsb = workspace_size(OP_GEMM_DGRAD, M, N, K)
+    ws = _bytes(wsb, dev) if ws is None else ws
+    st = LIB.luq_gemm_dgrad(_ptr(g_codes), _ptr(alpha), n_samples, _ptr(w_codes_t), _ptr(w_scale),
+                            1 if w_signed else 0, M, N, K, _ptr(dx), _ptr(ws), ws.numel(), _stream(dev))
+    _check(st, "luq_gemm_dgrad")
+    return dx
+
+
+def luq_gemm_wgrad(g_codes_t, alpha, a_codes_t, a_scale, a_signed, T, Nout, Kin, n_samples=1, dw=None, ws=None):
+    """dW [Nout, Kin] = Q(g)^T Q(a) from transposed codes g^T [Nout, T] and a^T [Kin, T]."""
+    dev = g_codes_t.device
+    dw = torch.empty(Nout, Kin, dtype=torch.float32, device=dev) if dw is None else dw
+    wsb = workspace_size(OP_GEMM_WGRAD, T, Nout, Kin)
+    ws = _bytes(wsb, dev) if ws is None else ws
+    st = LIB.luq_gemm_wgrad(_ptr(g_codes_t), _ptr(alpha), n_samples, _ptr(a_codes_t), _ptr(a_scale),
+                            1 if a_signed else 0, T, Nout, Kin, _ptr(dw), _ptr(ws), ws.numel(), _stream(dev))
+    _check(st, "luq_gemm_wgrad")
+    return dw
+
+
+def int4_im2col3x3_t(act_codes, B, H, W, C, col_t=None):
+    """Transposed 3x3 im2col of NHWC INT4 codes: [9*C, B*H*W] packed along tokens."""
+    dev = act_codes.device
+    T = B * H * W
+    col_t = _bytes(9 * C * T // 2, dev) if col_t is None else col_t
+    st = LIB.int4_im2col3x3_t(_ptr(act_codes), B, H, W, C, _ptr(col_t), _stream(dev))
+    _check(st, "int4_im2col3x3_t")
+    return col_t

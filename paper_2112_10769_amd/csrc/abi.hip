@@ -1,0 +1,192 @@
+// extern "C" entry points of libluq: argument validation on the host, then
+// launches on the caller's stream.  Nothing is enqueued when validation
+// fails.  See include/luq.h for the contract of every function.
+#include <stdint.h>
+#include <stdio.h>
+#include <string.h>
+
+#include "../../include/luq.h"
+#include "luq_launch.hpp"
+
+namespace {
+
+thread_local char g_last_error[256] = "";
+
+luq_status fail(luq_status st, const char* fmt, const char* what) {
+  snprintf(g_last_error, sizeof(g_last_error), fmt, what);
+  return st;
+}
+
+bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+bool aligned4(const void* p) { return ((uintptr_t)p & 3u) == 0; }
+
+luq_status hip_status(hipError_t e) {
+  if (e == hipSuccess) return LUQ_OK;
+  return fail(LUQ_ERR_HIP, "HIP launch failed: %s", hipGetErrorString(e));
+}
+
+bool mul_overflows(int64_t a, int64_t b) { return a > 0 && b > INT64_MAX / a; }
+
+luq_status check_matrix(int64_t rows, int64_t cols, bool transposed, const char* name) {
+  if (rows < 0 || cols < 0) return fail(LUQ_ERR_SHAPE, "%s: negative size", name);
+  if (mul_overflows(rows, cols)) return fail(LUQ_ERR_SHAPE, "%s: size overflows", name);
+  if (rows > 1 && (cols & 1)) return fail(LUQ_ERR_SHAPE, "%s: cols must be even when rows > 1", name);
+  if (transposed && ((rows & 7) || (cols & 7)))
+    return fail(LUQ_ERR_SHAPE, "%s: the transposed layout needs rows and cols multiples of 8", name);
+  return LUQ_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int luq_abi_version(void) { return LUQ_ABI_VERSION; }
+
+const char* luq_status_string(luq_status s) {
+  switch (s) {
+    case LUQ_OK: return "ok";
+    case LUQ_ERR_NULL: return "required pointer is NULL";
+    case LUQ_ERR_SHAPE: return "invalid shape";
+    case LUQ_ERR_DTYPE: return "unknown dtype";
+    case LUQ_ERR_PARAM: return "parameter out of range";
+    case LUQ_ERR_WORKSPACE: return "workspace missing or too small";
+    case LUQ_ERR_ALIGN: return "pointer not 16-byte aligned";
+    case LUQ_ERR_HIP: return "HIP runtime error";
+    default: return "unknown status";
+  }
+}
+
+const char* luq_last_error(void) { return g_last_error; }
+
+size_t luq_plane_bytes(int64_t n) { return n <= 0 ? 0 : luq::plane_bytes(n); }
+
+size_t luq_workspace_size(int op, int64_t d0, int64_t d1, int64_t d2) {
+  switch (op) {
+    case LUQ_OP_QUANTIZE_GRAD:
+    case LUQ_OP_INT4_QUANTIZE:
+      return d0 > 0 ? luq::quant_workspace_bytes(d0) : 0;
+    case LUQ_OP_GEMM_DGRAD:
+      return (d0 > 0 && d1 > 0 && d2 > 0) ? luq::gemm_workspace_bytes(d0, d1, d2, 1) : 0;
+    case LUQ_OP_GEMM_WGRAD:
+      return (d0 > 0 && d1 > 0 && d2 > 0) ? luq::gemm_workspace_bytes(d1, d2, d0, 1) : 0;
+    default:
+      return 0;
+  }
+}
+
+luq_status luq_quantize_grad(const void* g, luq_dtype dt, int64_t rows, int64_t cols, int R,
+                             uint64_t seed, uint32_t counter, int n_samples, uint8_t* codes,
+                             uint8_t* codes_t, float* alpha, float* maxabs, void* ws,
+                             size_t ws_bytes, void* stream) {
+  g_last_error[0] = 0;
+  if (dt != LUQ_F32 && dt != LUQ_BF16) return fail(LUQ_ERR_DTYPE, "%s: dtype", "luq_quantize_grad");
+  luq_status st = check_matrix(rows, cols, codes_t != nullptr, "luq_quantize_grad");
+  if (st != LUQ_OK) return st;
+  if (R < 4 || R > 6) return fail(LUQ_ERR_PARAM, "%s: R must be 4, 5 or 6", "luq_quantize_grad");
+  if (n_samples != 1 && n_samples != 2)
+    return fail(LUQ_ERR_PARAM, "%s: n_samples must be 1 or 2", "luq_quantize_grad");
+  if (n_samples == 2 && R > 5)
+    return fail(LUQ_ERR_PARAM, "%s: n_samples = 2 needs R <= 5", "luq_quantize_grad");
+  if (!alpha) return fail(LUQ_ERR_NULL, "%s: alpha is NULL", "luq_quantize_grad");
+  const int64_t n = rows * cols;
+  if (n > 0) {
+    if (!g) return fail(LUQ_ERR_NULL, "%s: g is NULL", "luq_quantize_grad");
+    if (!codes && !codes_t) return fail(LUQ_ERR_NULL, "%s: no code output", "luq_quantize_grad");
+    if (!ws || ws_bytes < luq_workspace_size(LUQ_OP_QUANTIZE_GRAD, n, 0, 0))
+      return fail(LUQ_ERR_WORKSPACE, "%s: workspace too small", "luq_quantize_grad");
+    if (!aligned16(g) || !aligned16(codes) || !aligned16(codes_t) || !aligned16(ws))
+      return fail(LUQ_ERR_ALIGN, "%s: g, codes, codes_t and ws must be 16-byte aligned",
+                  "luq_quantize_grad");
+  }
+  if (!aligned4(alpha) || !aligned4(maxabs))
+    return fail(LUQ_ERR_ALIGN, "%s: alpha / maxabs misaligned", "luq_quantize_grad");
+  return hip_status(luq::launch_luq_quantize(g, dt == LUQ_BF16, rows, cols, R, seed, counter,
+                                             n_samples, codes, codes_t, alpha, maxabs, ws,
+                                             static_cast<hipStream_t>(stream)));
+}
+
+luq_status int4_quantize(const void* x, luq_dtype dt, int64_t rows, int64_t cols, int is_signed,
+                         float clip, uint8_t* codes, uint8_t* codes_t, float* scale, void* ws,
+                         size_t ws_bytes, void* stream) {
+  g_last_error[0] = 0;
+  if (dt != LUQ_F32 && dt != LUQ_BF16) return fail(LUQ_ERR_DTYPE, "%s: dtype", "int4_quantize");
+  luq_status st = check_matrix(rows, cols, codes_t != nullptr, "int4_quantize");
+  if (st != LUQ_OK) return st;
+  if (!(clip == clip) || clip == __builtin_inff())
+    return fail(LUQ_ERR_PARAM, "%s: clip must be finite", "int4_quantize");
+  if (!scale) return fail(LUQ_ERR_NULL, "%s: scale is NULL", "int4_quantize");
+  const int64_t n = rows * cols;
+  if (n > 0) {
+    if (!x) return fail(LUQ_ERR_NULL, "%s: x is NULL", "int4_quantize");
+    if (!codes && !codes_t) return fail(LUQ_ERR_NULL, "%s: no code output", "int4_quantize");
+    if (clip <= 0.0f && (!ws || ws_bytes < luq_workspace_size(LUQ_OP_INT4_QUANTIZE, n, 0, 0)))
+      return fail(LUQ_ERR_WORKSPACE, "%s: workspace too small", "int4_quantize");
+    if (!aligned16(x) || !aligned16(codes) || !aligned16(codes_t) || !aligned16(ws))
+      return fail(LUQ_ERR_ALIGN, "%s: x, codes, codes_t and ws must be 16-byte aligned",
+                  "int4_quantize");
+  }
+  if (!aligned4(scale)) return fail(LUQ_ERR_ALIGN, "%s: scale misaligned", "int4_quantize");
+  return hip_status(luq::launch_int4_quantize(x, dt == LUQ_BF16, rows, cols, is_signed ? 1 : 0,
+                                              clip, codes, codes_t, scale, ws,
+                                              static_cast<hipStream_t>(stream)));
+}
+
+static luq_status gemm_common(const char* name, const uint8_t* A, const float* alpha, int ns,
+                              const uint8_t* B, const float* bscale, int b_signed, int64_t M,
+                              int64_t N, int64_t K, float* C, void* ws, size_t ws_bytes,
+                              void* stream) {
+  if (!A || !alpha || !B || !bscale || !C) return fail(LUQ_ERR_NULL, "%s: NULL operand", name);
+  if (ns != 1 && ns != 2) return fail(LUQ_ERR_PARAM, "%s: n_samples must be 1 or 2", name);
+  if (M < 1 || N < 1 || K < 32 || (K & 31))
+    return fail(LUQ_ERR_SHAPE, "%s: need M, N >= 1 and K a positive multiple of 32", name);
+  if (mul_overflows(M, N) || mul_overflows(M, K) || mul_overflows(N, K))
+    return fail(LUQ_ERR_SHAPE, "%s: size overflows", name);
+  if (M > INT32_MAX / 2 || N > INT32_MAX / 2)
+    return fail(LUQ_ERR_SHAPE, "%s: M and N must be below 2^30", name);
+  const size_t need = luq::gemm_workspace_bytes(M, N, K, ns);
+  if (need && (!ws || ws_bytes < need)) return fail(LUQ_ERR_WORKSPACE, "%s: workspace too small", name);
+  if (!aligned16(A) || !aligned16(B) || !aligned16(ws) || !aligned4(C) || !aligned4(alpha) ||
+      !aligned4(bscale))
+    return fail(LUQ_ERR_ALIGN, "%s: code operands and ws must be 16-byte aligned", name);
+  return hip_status(luq::launch_gemm_luq_int4(A, (int64_t)luq::plane_bytes(M * K), ns, alpha, B,
+                                              bscale, b_signed ? 1 : 0, M, N, K, C, ws, ws_bytes,
+                                              static_cast<hipStream_t>(stream)));
+}
+
+luq_status luq_gemm_dgrad(const uint8_t* g_codes, const float* alpha, int n_samples,
+                          const uint8_t* w_codes_t, const float* w_scale, int w_signed,
+                          int64_t M, int64_t N, int64_t K, float* dx, void* ws, size_t ws_bytes,
+                          void* stream) {
+  g_last_error[0] = 0;
+  return gemm_common("luq_gemm_dgrad", g_codes, alpha, n_samples, w_codes_t, w_scale, w_signed, M,
+                     N, K, dx, ws, ws_bytes, stream);
+}
+
+luq_status luq_gemm_wgrad(const uint8_t* g_codes_t, const float* alpha, int n_samples,
+                          const uint8_t* a_codes_t, const float* a_scale, int a_signed, int64_t T,
+                          int64_t Nout, int64_t Kin, float* dw, void* ws, size_t ws_bytes,
+                          void* stream) {
+  g_last_error[0] = 0;
+  return gemm_common("luq_gemm_wgrad", g_codes_t, alpha, n_samples, a_codes_t, a_scale, a_signed,
+                     Nout, Kin, T, dw, ws, ws_bytes, stream);
+}
+
+luq_status int4_im2col3x3_t(const uint8_t* act_codes, int64_t B, int64_t H, int64_t W, int64_t C,
+                            uint8_t* col_t, void* stream) {
+  g_last_error[0] = 0;
+  if (B < 0 || H < 0 || W < 0 || C < 0) return fail(LUQ_ERR_SHAPE, "%s: negative size", "int4_im2col3x3_t");
+  if (mul_overflows(B, H) || mul_overflows(B * H, W) || mul_overflows(B * H * W, 9 * C))
+    return fail(LUQ_ERR_SHAPE, "%s: size overflows", "int4_im2col3x3_t");
+  const int64_t T = B * H * W;
+  if ((C & 1) || (T & 7)) return fail(LUQ_ERR_SHAPE, "%s: C must be even and B*H*W a multiple of 8", "int4_im2col3x3_t");
+  if (B > INT32_MAX || H > INT32_MAX || W > INT32_MAX || C > INT32_MAX / 9)
+    return fail(LUQ_ERR_SHAPE, "%s: dimension too large", "int4_im2col3x3_t");
+  if (T == 0 || C == 0) return LUQ_OK;
+  if (!act_codes || !col_t) return fail(LUQ_ERR_NULL, "%s: NULL pointer", "int4_im2col3x3_t");
+  if (!aligned16(act_codes) || !aligned16(col_t))
+    return fail(LUQ_ERR_ALIGN, "%s: pointers must be 16-byte aligned", "int4_im2col3x3_t");
+  return hip_status(luq::launch_im2col3x3_t(act_codes, B, H, W, C, col_t,
+                                            static_cast<hipStream_t>(stream)));
+}
+
+}  // extern "C"

@@ -1,0 +1,146 @@
+// Device helpers shared by the libluq kernels (gfx950 / CDNA4, wave64).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace luq {
+
+constexpr int kWave = 64;
+
+// ---------------------------------------------------------------------------
+// Philox4x32-10 (Salmon et al., SC'11).  Ten rounds; each round takes the
+// full 64-bit products of the two multipliers with words 0 and 2 (one
+// v_mad_u64_u32 each) and mixes in the key, which is bumped by the Weyl
+// constants after every round.  The key is wave-uniform, so its schedule
+// stays in scalar registers.
+// ---------------------------------------------------------------------------
+struct U4 {
+  uint32_t x, y, z, w;
+};
+
+__device__ __forceinline__ U4 philox4x32_10(U4 c, uint32_t k0, uint32_t k1) {
+#pragma unroll
+  for (int r = 0; r < 10; ++r) {
+    const uint64_t p0 = (uint64_t)0xD2511F53u * c.x;
+    const uint64_t p1 = (uint64_t)0xCD9E8D57u * c.z;
+    const uint32_t hi0 = (uint32_t)(p0 >> 32), lo0 = (uint32_t)p0;
+    const uint32_t hi1 = (uint32_t)(p1 >> 32), lo1 = (uint32_t)p1;
+    c = U4{hi1 ^ c.y ^ k0, lo1, hi0 ^ c.w ^ k1, lo0};
+    k0 += 0x9E3779B9u;
+    k1 += 0xBB67AE85u;
+  }
+  return c;
+}
+
+// ---------------------------------------------------------------------------
+// Loads of 8 consecutive elements as float32 bit patterns (exact for bf16:
+// a bfloat16 is the upper half of the float32 with the same value).
+// ---------------------------------------------------------------------------
+struct U8 {
+  uint32_t v[8];
+};
+
+template <bool BF16>
+__device__ __forceinline__ U8 load8(const void* base, int64_t elem) {
+  U8 r;
+  if constexpr (BF16) {
+    const uint4 q = *reinterpret_cast<const uint4*>(static_cast<const uint16_t*>(base) + elem);
+    const uint32_t w[4] = {q.x, q.y, q.z, q.w};
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      r.v[2 * i] = w[i] << 16;
+      r.v[2 * i + 1] = w[i] & 0xFFFF0000u;
+    }
+  } else {
+    const uint4* p = reinterpret_cast<const uint4*>(static_cast<const float*>(base) + elem);
+    const uint4 a = p[0], b = p[1];
+    r.v[0] = a.x; r.v[1] = a.y; r.v[2] = a.z; r.v[3] = a.w;
+    r.v[4] = b.x; r.v[5] = b.y; r.v[6] = b.z; r.v[7] = b.w;
+  }
+  return r;
+}
+
+// Bounded variant for a ragged tail: elements at or beyond n read as +0.
+template <bool BF16>
+__device__ __forceinline__ U8 load8_tail(const void* base, int64_t elem, int64_t n) {
+  U8 r;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    uint32_t b = 0;
+    if (elem + i < n) {
+      if constexpr (BF16)
+        b = (uint32_t)(static_cast<const uint16_t*>(base)[elem + i]) << 16;
+      else
+        b = static_cast<const uint32_t*>(base)[elem + i];
+    }
+    r.v[i] = b;
+  }
+  return r;
+}
+
+// ---------------------------------------------------------------------------
+// Reductions of unsigned keys (float32 bit patterns of non-negative values,
+// whose unsigned order is the float order; non-finite values sort above
+// every finite one).
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ uint32_t wave_max_u32(uint32_t v) {
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) v = max(v, (uint32_t)__shfl_xor((int)v, off, kWave));
+  return v;
+}
+
+// Max over a block of `threads` threads (a multiple of 64, at most 1024).
+// Every thread gets the result.  `scratch` holds at least threads/64 words.
+__device__ __forceinline__ uint32_t block_max_u32(uint32_t v, uint32_t* scratch) {
+  const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x / kWave;
+  const int nwaves = blockDim.x / kWave;
+  v = wave_max_u32(v);
+  __syncthreads();  // scratch may still be read by a previous call
+  if (lane == 0) scratch[wave] = v;
+  __syncthreads();
+  uint32_t m = 0;
+  for (int i = 0; i < nwaves; ++i) m = max(m, scratch[i]);
+  return m;
+}
+
+// Max of the per-block partial keys written by a max pass.
+__device__ __forceinline__ uint32_t reduce_partials(const uint32_t* partial, int nparts,
+                                                    uint32_t* scratch) {
+  uint32_t m = 0;
+  for (int i = threadIdx.x; i < nparts; i += blockDim.x) m = max(m, partial[i]);
+  return block_max_u32(m, scratch);
+}
+
+// ---------------------------------------------------------------------------
+// 8x8 transpose of 4-bit fields: on entry r[i] holds row i (nibble j at bits
+// 4j); on exit r[j] holds column j (nibble i at bits 4i).  Three rounds of
+// field swaps between row pairs at distance 1, 2 and 4 (4-, 8-, 16-bit).
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ void swap_fields(uint32_t& a, uint32_t& b, int s, uint32_t mask) {
+  const uint32_t t = ((a >> s) ^ b) & mask;
+  b ^= t;
+  a ^= t << s;
+}
+
+__device__ __forceinline__ void transpose8x8_nibbles(uint32_t (&r)[8]) {
+  swap_fields(r[0], r[1], 4, 0x0F0F0F0Fu);
+  swap_fields(r[2], r[3], 4, 0x0F0F0F0Fu);
+  swap_fields(r[4], r[5], 4, 0x0F0F0F0Fu);
+  swap_fields(r[6], r[7], 4, 0x0F0F0F0Fu);
+  swap_fields(r[0], r[2], 8, 0x00FF00FFu);
+  swap_fields(r[1], r[3], 8, 0x00FF00FFu);
+  swap_fields(r[4], r[6], 8, 0x00FF00FFu);
+  swap_fields(r[5], r[7], 8, 0x00FF00FFu);
+  swap_fields(r[0], r[4], 16, 0x0000FFFFu);
+  swap_fields(r[1], r[5], 16, 0x0000FFFFu);
+  swap_fields(r[2], r[6], 16, 0x0000FFFFu);
+  swap_fields(r[3], r[7], 16, 0x0000FFFFu);
+}
+
+// Stores the first `nbytes` (0..4) bytes of w at p (ragged tails).
+__device__ __forceinline__ void store_bytes(uint8_t* p, uint32_t w, int nbytes) {
+  for (int i = 0; i < nbytes; ++i) p[i] = (uint8_t)(w >> (8 * i));
+}
+
+}  // namespace luq

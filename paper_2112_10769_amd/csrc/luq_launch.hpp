@@ -1,0 +1,39 @@
+// Internal launchers behind the C ABI (host side).  Arguments are already
+// validated by the ABI layer.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace luq {
+
+// ceil(n/2) rounded up to 256 bytes: the distance between SMP planes.
+inline size_t plane_bytes(int64_t n) {
+  const size_t b = (size_t)((n + 1) / 2);
+  return (b + 255) & ~(size_t)255;
+}
+
+size_t quant_workspace_bytes(int64_t n);
+
+hipError_t launch_luq_quantize(const void* g, int bf16, int64_t rows, int64_t cols, int R,
+                               uint64_t seed, uint32_t counter, int ns, uint8_t* codes,
+                               uint8_t* codes_t, float* alpha, float* maxabs, void* ws,
+                               hipStream_t st);
+
+hipError_t launch_int4_quantize(const void* x, int bf16, int64_t rows, int64_t cols, int is_signed,
+                                float clip, uint8_t* codes, uint8_t* codes_t, float* scale,
+                                void* ws, hipStream_t st);
+
+// C[m][n] = (alpha / ns) * bscale * sum_k A[m][k] * B[n][k] with A LUQ codes
+// (ns planes, plane stride a_plane) and B INT4 codes, both K-major.
+size_t gemm_workspace_bytes(int64_t M, int64_t N, int64_t K, int ns);
+hipError_t launch_gemm_luq_int4(const uint8_t* A, int64_t a_plane, int ns, const float* alpha,
+                                const uint8_t* B, const float* bscale, int b_signed, int64_t M,
+                                int64_t N, int64_t K, float* C, void* ws, size_t ws_bytes,
+                                hipStream_t st);
+
+hipError_t launch_im2col3x3_t(const uint8_t* act, int64_t B, int64_t H, int64_t W, int64_t C,
+                              uint8_t* col_t, hipStream_t st);
+
+}  // namespace luq

@@ -1,0 +1,144 @@
+"""The C-ABI library loads without a GPU, exports every function include/luq.h
+declares, and rejects invalid arguments on the host before any launch.
+
+Every call below is built to fail validation, so nothing is enqueued; the
+pointers are never dereferenced.
+"""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "luq.h")
+
+luq = pytest.importorskip("paper_2112_10769_amd")
+LIB = luq.LIB
+
+P = ctypes.c_void_p(0x10000)      # 16-byte aligned, never dereferenced
+P2 = ctypes.c_void_p(0x20000)
+P3 = ctypes.c_void_p(0x30000)
+PMIS = ctypes.c_void_p(0x10004)   # misaligned
+NUL = None
+WS = 1 << 20
+
+
+def _declared():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"^[a-z_][\w \*]*?\b((?:luq|int4)_\w+)\s*\(", text, flags=re.M)))
+
+
+def test_every_declared_function_is_exported():
+    names = _declared()
+    assert len(names) == 10, names
+    for n in names:
+        assert hasattr(LIB, n), n
+    assert set(names) == set(luq.EXPORTS)
+
+
+def test_version_and_strings():
+    v = int(re.search(r"#define LUQ_ABI_VERSION (\d+)", open(HEADER).read()).group(1))
+    assert LIB.luq_abi_version() == v
+    for s in range(8):
+        assert LIB.luq_status_string(s)
+    assert LIB.luq_status_string(99) == b"unknown status"
+
+
+def test_plane_and_workspace_sizes():
+    assert luq.plane_bytes(0) == 0
+    assert luq.plane_bytes(1) == 256
+    assert luq.plane_bytes(512) == 256
+    assert luq.plane_bytes(514) == 512
+    assert luq.plane_bytes(256 * 512) == 65536
+    assert luq.workspace_size(luq.OP_QUANTIZE_GRAD, 1000) >= 4096
+    assert luq.workspace_size(luq.OP_INT4_QUANTIZE, 0) == 0
+    # a long, thin reduction is split along K and needs partial sums
+    assert luq.workspace_size(luq.OP_GEMM_WGRAD, 200704, 64, 576) > 0
+    assert luq.workspace_size(luq.OP_GEMM_DGRAD, 8192, 4096, 16384) == 0
+    assert luq.workspace_size(99, 1, 1, 1) == 0
+
+
+def _qg(**kw):
+    a = dict(g=P, dt=0, rows=4, cols=8, R=4, seed=0, counter=0, ns=1, codes=P2, codes_t=NUL,
+             alpha=P3, maxabs=NUL, ws=P, ws_bytes=WS)
+    a.update(kw)
+    return LIB.luq_quantize_grad(a["g"], a["dt"], a["rows"], a["cols"], a["R"], a["seed"], a["counter"],
+                                 a["ns"], a["codes"], a["codes_t"], a["alpha"], a["maxabs"], a["ws"],
+                                 a["ws_bytes"], None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(dt=2), 3),
+    (dict(rows=-1), 2),
+    (dict(rows=3, cols=7), 2),
+    (dict(rows=12, cols=8, codes_t=P2), 2),
+    (dict(rows=16, cols=12, codes_t=P2), 2),
+    (dict(rows=2**40, cols=2**40), 2),
+    (dict(R=3), 4), (dict(R=7), 4),
+    (dict(ns=3), 4), (dict(ns=0), 4),
+    (dict(ns=2, R=6), 4),
+    (dict(alpha=NUL), 1),
+    (dict(g=NUL), 1),
+    (dict(codes=NUL, codes_t=NUL), 1),
+    (dict(ws=NUL), 5),
+    (dict(ws_bytes=16), 5),
+    (dict(g=PMIS), 6),
+    (dict(codes=PMIS), 6),
+    (dict(alpha=ctypes.c_void_p(0x10001)), 6),
+])
+def test_quantize_grad_validation(kw, status):
+    assert _qg(**kw) == status
+    assert LIB.luq_last_error()
+
+
+def _i4(**kw):
+    a = dict(x=P, dt=0, rows=4, cols=8, signed=1, clip=0.0, codes=P2, codes_t=NUL, scale=P3, ws=P, ws_bytes=WS)
+    a.update(kw)
+    return LIB.int4_quantize(a["x"], a["dt"], a["rows"], a["cols"], a["signed"], a["clip"], a["codes"],
+                             a["codes_t"], a["scale"], a["ws"], a["ws_bytes"], None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(dt=5), 3), (dict(cols=-2), 2), (dict(rows=8, cols=4, codes_t=P2), 2),
+    (dict(clip=float("nan")), 4), (dict(clip=float("inf")), 4),
+    (dict(scale=NUL), 1), (dict(x=NUL), 1), (dict(codes=NUL), 1),
+    (dict(ws=NUL), 5), (dict(ws_bytes=8), 5), (dict(x=PMIS), 6),
+])
+def test_int4_validation(kw, status):
+    assert _i4(**kw) == status
+
+
+def _dg(**kw):
+    a = dict(g=P, alpha=P3, ns=1, w=P2, ws_=P3, wsig=1, M=64, N=64, K=64, dx=P, ws=P, wsb=WS)
+    a.update(kw)
+    return LIB.luq_gemm_dgrad(a["g"], a["alpha"], a["ns"], a["w"], a["ws_"], a["wsig"], a["M"], a["N"],
+                              a["K"], a["dx"], a["ws"], a["wsb"], None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(g=NUL), 1), (dict(alpha=NUL), 1), (dict(w=NUL), 1), (dict(ws_=NUL), 1), (dict(dx=NUL), 1),
+    (dict(ns=3), 4),
+    (dict(M=0), 2), (dict(N=-1), 2), (dict(K=48), 2), (dict(K=0), 2), (dict(M=2**31), 2),
+    (dict(g=PMIS), 6), (dict(w=PMIS), 6),
+    (dict(M=64, N=64, K=1 << 19, ws=NUL), 5),
+])
+def test_dgrad_validation(kw, status):
+    assert _dg(**kw) == status
+
+
+def test_wgrad_validation():
+    args = [P, P3, 1, P2, P3, 0]
+    assert LIB.luq_gemm_wgrad(*args, 40, 64, 64, P, P, WS, None) == 2          # T not a multiple of 32
+    assert LIB.luq_gemm_wgrad(*args, 200704, 64, 576, P, NUL, 0, None) == 5    # split-K needs ws
+    assert LIB.luq_gemm_wgrad(NUL, P3, 1, P2, P3, 0, 64, 8, 8, P, P, WS, None) == 1
+
+
+def test_im2col_validation():
+    assert LIB.int4_im2col3x3_t(P, 1, 3, 3, 3, P2, None) == 2       # odd C
+    assert LIB.int4_im2col3x3_t(P, 1, 3, 3, 2, P2, None) == 2       # T = 9 not a multiple of 8
+    assert LIB.int4_im2col3x3_t(NUL, 1, 2, 4, 2, P2, None) == 1
+    assert LIB.int4_im2col3x3_t(PMIS, 1, 2, 4, 2, P2, None) == 6
+    assert LIB.int4_im2col3x3_t(P, -1, 2, 4, 2, P2, None) == 2
+    assert LIB.int4_im2col3x3_t(P, 0, 2, 4, 2, P2, None) == 0       # empty: nothing to do
