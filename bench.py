@@ -129,31 +129,45 @@ def build_mlp(L, torch, dev, ns=1, T=None, D=None, F=None):
     return stages, cfg, d
 
 
+def capture(torch, fns):
+    """A HIP graph that replays the given launches (no host work per replay)."""
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        for f in fns:
+            f()
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        for f in fns:
+            f()
+    torch.cuda.synchronize()
+    return g
+
+
+def time_graph(torch, g, reps):
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    a.record()
+    for _ in range(reps):
+        g.replay()
+    b.record()
+    torch.cuda.synchronize()
+    return a.elapsed_time(b) / 1e3 / reps
+
+
 def time_stages(torch, stages, steps, warmup):
-    def step():
-        for s in stages:
-            s.fn()
+    """Step time (whole hot path, one graph) and per-stage times (one graph each)."""
+    step = capture(torch, [s.fn for s in stages])
     for _ in range(warmup):
-        step()
-    torch.cuda.synchronize()
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    e0.record()
-    for _ in range(steps):
-        step()
-    e1.record()
-    torch.cuda.synchronize()
-    step_s = e0.elapsed_time(e1) / 1e3 / steps
+        step.replay()
+    step_s = time_graph(torch, step, steps)
     per = {}
-    reps = max(3, steps)
     for s in stages:
-        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        a.record()
-        for _ in range(reps):
-            s.fn()
-        b.record()
-        torch.cuda.synchronize()
-        per[s.name] = a.elapsed_time(b) / 1e3 / reps
+        g = capture(torch, [s.fn])
+        g.replay()
+        per[s.name] = time_graph(torch, g, max(10, steps))
     return step_s, per
 
 

@@ -7,7 +7,7 @@
 // quantizers write whichever layout (row-major or transposed) a GEMM needs,
 // so the GEMM never transposes.
 //
-// Carrier: v_mfma_i32_16x16x64_i8 with exact int32 accumulation.  Codes are
+// Carrier: v_mfma_i32_32x32x32_i8 with exact int32 accumulation.  Codes are
 // expanded from nibbles to int8 once per workgroup tile, on the way from
 // global memory into LDS:
 //   LUQ  : a byte LUT (v_perm_b32) maps the exponent field e to 2^(e-1) (or
@@ -30,10 +30,16 @@
 namespace luq {
 
 typedef int v4i __attribute__((ext_vector_type(4)));
+typedef int v16i __attribute__((ext_vector_type(16)));
+typedef unsigned v4u __attribute__((ext_vector_type(4)));
+
+// Word 3 of a raw buffer descriptor on gfx9 (32-bit data, no swizzle).
+constexpr int kBufferFlags = 0x00020000;
+// A buffer offset beyond any operand's range: such loads return zeros.
+constexpr int kOutOfRange = 0x7FFFFFF0;
 
 constexpr int kGemmThreads = 256;
-constexpr int kBK = 128;                 // k per LDS stage (two MFMA k-steps)
-constexpr int kPitch = kBK + 16;         // LDS row pitch in bytes
+constexpr int kKAlign = 128;            // k-chunk granularity of a split
 constexpr int64_t kMaxExactK = 1 << 18;  // |A| <= 64, |B| <= 120: 2^18 * 7680 < 2^31
 
 // ---- nibble -> int8 expansion ------------------------------------------------
@@ -43,11 +49,15 @@ __device__ __forceinline__ void expand_luq(uint32_t x, uint32_t& lo, uint32_t& h
   const uint32_t t_lo = 0x04020100u, t_hi = 0x40201008u;
   const uint32_t m_lo = __builtin_amdgcn_perm(t_hi, t_lo, x & 0x07070707u);
   const uint32_t m_hi = __builtin_amdgcn_perm(t_hi, t_lo, (x >> 4) & 0x07070707u);
-  const uint32_t s_lo = (x >> 3) & 0x01010101u, s_hi = (x >> 7) & 0x01010101u;
-  // 0xFF in every byte whose sign bit is set; negation = (m ^ 0xFF) + 1, which
-  // never carries out of a byte because m >= 1 wherever the sign is set
-  lo = (m_lo ^ ((s_lo << 8) - s_lo)) + s_lo;
-  hi = (m_hi ^ ((s_hi << 8) - s_hi)) + s_hi;
+  // selector bytes 12 (sign clear) or 13 (sign set): v_perm_b32 turns them
+  // into 0x00 / 0xFF, a byte mask of the negative elements
+  const uint32_t q_lo = ((x >> 3) & 0x01010101u) | 0x0C0C0C0Cu;
+  const uint32_t q_hi = ((x >> 7) & 0x01010101u) | 0x0C0C0C0Cu;
+  const uint32_t k_lo = __builtin_amdgcn_perm(0u, 0u, q_lo), k_hi = __builtin_amdgcn_perm(0u, 0u, q_hi);
+  // negation = (m ^ 0xFF) + 1, which never carries out of a byte because
+  // m >= 1 wherever the sign is set
+  lo = (m_lo ^ k_lo) + (q_lo & 0x01010101u);
+  hi = (m_hi ^ k_hi) + (q_hi & 0x01010101u);
 }
 
 template <bool SIGNED>
@@ -76,62 +86,118 @@ struct GemmArgs {
   const float* bscale;
   float* C;
   int32_t* partial;   // split-K chunk sums [splits][M][N], or null
-  int64_t k_chunk;    // k per split (multiple of kBK)
-  int tiles_n;        // number of tiles along N
+  int64_t k_chunk;    // k per split (multiple of kKAlign)
+  int tiles_m, tiles_n;
+  int vec;            // rows of C (or partial) are 16-byte aligned: vector stores
 };
 
-// ---- the tile kernel ----------------------------------------------------------
+// Block -> output tile.  Blocks are dispatched round-robin over the 8 XCDs
+// (each with its own L2), so when the tile count allows, consecutive runs of
+// tiles are given to one XCD; within that run tiles are visited in groups of
+// 8 tile-rows so that the A rows and B rows in flight are shared.
+__device__ __forceinline__ void tile_coords(int bid, int ntm, int ntn, int& tm, int& tn) {
+  const int total = ntm * ntn;
+  int L = bid;
+  if ((total & 7) == 0) L = (bid & 7) * (total >> 3) + (bid >> 3);
+  constexpr int G = 8;
+  const int per_group = G * ntn;
+  const int first_m = (L / per_group) * G;
+  const int gsize = min(ntm - first_m, G);
+  const int in_group = L - (L / per_group) * per_group;
+  tm = first_m + in_group % gsize;
+  tn = in_group / gsize;
+}
 
-template <int BM, int BN, int NS, bool BSIGNED>
-__global__ __launch_bounds__(kGemmThreads) void gemm_luq_int4_kernel(GemmArgs a) {
-  static_assert(BM % 32 == 0 && BN % 32 == 0, "wave tiles are multiples of 16");
-  constexpr int TM = BM / 32, TN = BN / 32;            // MFMA tiles per wave
-  constexpr int ACH = BM * (kBK / 32) / kGemmThreads;  // 16-byte A chunks per thread
-  constexpr int BCH = BN * (kBK / 32) / kGemmThreads;
+// ---- the tile kernel ----------------------------------------------------------
+//
+// 256 threads = 2 x 2 waves; a wave owns a (BM/2) x (BN/2) block of C as
+// (BM/64) x (BN/64) tiles of the 32x32 MFMA.  Per k-stage of BK (64 or 128):
+//   - the packed tile for stage t+2 is loaded into registers,
+//   - stage t is multiplied out of LDS buffer t%2,
+//   - stage t+1 (loaded one iteration earlier) is expanded into LDS buffer
+//     (t+1)%2,
+// all in one block of straight-line code, so the expansion VALU work and the
+// global loads overlap the MFMAs.  The MFMA takes the B fragment as its first
+// operand, so each lane ends up with 4 consecutive columns of one C row.
+template <int BM, int BN, int BK, int NS, bool BSIGNED>
+__global__ __launch_bounds__(kGemmThreads, 1) void gemm_luq_int4_kernel(GemmArgs a) {
+  static_assert(BM % 64 == 0 && BN % 64 == 0, "wave tiles are multiples of 32");
+  static_assert(BK == 64 || BK == 128, "k per stage");
+  constexpr int kBK = BK;
+  constexpr int kPitch = BK + 16;                      // LDS row pitch in bytes
+  constexpr int KC = BK / 32;                          // 16-byte chunks per row and stage
+  constexpr int TM = BM / 64, TN = BN / 64;            // 32x32 MFMA tiles per wave
+  constexpr int ACH = BM * KC / kGemmThreads;          // 16-byte A chunks per thread and stage
+  constexpr int BCH = BN * KC / kGemmThreads;
   static_assert(ACH >= 1 && BCH >= 1, "tile too small for the block");
-  __shared__ __attribute__((aligned(16))) uint8_t As[2][BM * kPitch];
-  __shared__ __attribute__((aligned(16))) uint8_t Bs[2][BN * kPitch];
+  constexpr int STAGE = (BM + BN) * kPitch;            // bytes of one LDS stage
+  __shared__ __attribute__((aligned(16))) uint8_t lds[2 * STAGE];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave >> 1, wn = wave & 1;
-  const int64_t m0 = (int64_t)(blockIdx.x / a.tiles_n) * BM;
-  const int64_t n0 = (int64_t)(blockIdx.x % a.tiles_n) * BN;
+  int tm, tn;
+  tile_coords(blockIdx.x, a.tiles_m, a.tiles_n, tm, tn);
+  const int64_t m0 = (int64_t)tm * BM, n0 = (int64_t)tn * BN;
   const int64_t kbeg = (int64_t)blockIdx.y * a.k_chunk;
-  int64_t kend = kbeg + a.k_chunk;
-  if (kend > a.K) kend = a.K;
+  const int64_t kend = min(kbeg + a.k_chunk, a.K);
   const int nkt = (int)((kend - kbeg + kBK - 1) / kBK);
   const int64_t ld = a.K >> 1;  // bytes per operand row
 
-  uint4 ra[NS][ACH], rb[BCH];
-  auto load_tiles = [&](int64_t k0) {
+  // Operands are read through buffer descriptors whose range is the operand
+  // itself: rows past M (or N) fall outside the range, and a chunk past the
+  // end of this split's k range is given an offset outside it, so both read
+  // as zeros without a branch.
+  __amdgpu_buffer_rsrc_t rsa[NS];
+#pragma unroll
+  for (int s = 0; s < NS; ++s)
+    rsa[s] = __builtin_amdgcn_make_buffer_rsrc((void*)(a.A + s * a.a_plane), (short)0,
+                                               (int)(a.M * ld), kBufferFlags);
+  const __amdgpu_buffer_rsrc_t rsb =
+      __builtin_amdgcn_make_buffer_rsrc((void*)a.B, (short)0, (int)(a.N * ld), kBufferFlags);
+  int offa[ACH], kca[ACH], offb[BCH], kcb[BCH];
+#pragma unroll
+  for (int i = 0; i < ACH; ++i) {
+    const int c = tid + i * kGemmThreads, row = c / KC, kc = c % KC;
+    kca[i] = kc * 32;
+    offa[i] = (int)((m0 + row) * ld + (kbeg >> 1) + kc * 16);
+  }
+#pragma unroll
+  for (int i = 0; i < BCH; ++i) {
+    const int c = tid + i * kGemmThreads, row = c / KC, kc = c % KC;
+    kcb[i] = kc * 32;
+    offb[i] = (int)((n0 + row) * ld + (kbeg >> 1) + kc * 16);
+  }
+
+  struct Regs {
+    v4u a[NS][ACH];
+    v4u b[BCH];
+  };
+  auto load = [&](Regs& r, int t) {
+    const int64_t k0 = kbeg + (int64_t)t * kBK;
 #pragma unroll
     for (int i = 0; i < ACH; ++i) {
-      const int c = tid + i * kGemmThreads, row = c >> 2, kc = c & 3;
-      const int64_t m = m0 + row, k = k0 + kc * 32;
-      const bool ok = (m < a.M) && (k < kend);
+      const int off = (k0 + kca[i]) < kend ? offa[i] + t * (kBK / 2) : kOutOfRange;
 #pragma unroll
-      for (int s = 0; s < NS; ++s)
-        ra[s][i] = ok ? *reinterpret_cast<const uint4*>(a.A + s * a.a_plane + m * ld + (k >> 1))
-                      : make_uint4(0, 0, 0, 0);
+      for (int s = 0; s < NS; ++s) r.a[s][i] = __builtin_amdgcn_raw_buffer_load_b128(rsa[s], off, 0, 0);
     }
 #pragma unroll
     for (int i = 0; i < BCH; ++i) {
-      const int c = tid + i * kGemmThreads, row = c >> 2, kc = c & 3;
-      const int64_t n = n0 + row, k = k0 + kc * 32;
-      const bool ok = (n < a.N) && (k < kend);
-      rb[i] = ok ? *reinterpret_cast<const uint4*>(a.B + n * ld + (k >> 1)) : make_uint4(0, 0, 0, 0);
+      const int off = (k0 + kcb[i]) < kend ? offb[i] + t * (kBK / 2) : kOutOfRange;
+      r.b[i] = __builtin_amdgcn_raw_buffer_load_b128(rsb, off, 0, 0);
     }
   };
-  auto store_tiles = [&](int buf) {
+  auto expand_store = [&](const Regs& r, int buf) {
+    uint8_t* As = lds + buf * STAGE;
+    uint8_t* Bs = As + BM * kPitch;
 #pragma unroll
     for (int i = 0; i < ACH; ++i) {
-      const int c = tid + i * kGemmThreads, row = c >> 2, kc = c & 3;
+      const int c = tid + i * kGemmThreads, row = c / KC, kc = c % KC;
       uint32_t w[8];
-      const uint32_t x0[4] = {ra[0][i].x, ra[0][i].y, ra[0][i].z, ra[0][i].w};
+      const uint32_t x0[4] = {r.a[0][i][0], r.a[0][i][1], r.a[0][i][2], r.a[0][i][3]};
 #pragma unroll
       for (int d = 0; d < 4; ++d) expand_luq(x0[d], w[2 * d], w[2 * d + 1]);
       if constexpr (NS == 2) {
-        const uint32_t x1[4] = {ra[1][i].x, ra[1][i].y, ra[1][i].z, ra[1][i].w};
+        const uint32_t x1[4] = {r.a[1][i][0], r.a[1][i][1], r.a[1][i][2], r.a[1][i][3]};
 #pragma unroll
         for (int d = 0; d < 4; ++d) {
           uint32_t l, h;
@@ -140,92 +206,146 @@ __global__ __launch_bounds__(kGemmThreads) void gemm_luq_int4_kernel(GemmArgs a)
           w[2 * d + 1] = add_i8x4(w[2 * d + 1], h);
         }
       }
-      uint4* dst = reinterpret_cast<uint4*>(&As[buf][row * kPitch + kc * 32]);
+      uint4* dst = reinterpret_cast<uint4*>(As + row * kPitch + kc * 32);
       dst[0] = make_uint4(w[0], w[1], w[2], w[3]);
       dst[1] = make_uint4(w[4], w[5], w[6], w[7]);
     }
 #pragma unroll
     for (int i = 0; i < BCH; ++i) {
-      const int c = tid + i * kGemmThreads, row = c >> 2, kc = c & 3;
+      const int c = tid + i * kGemmThreads, row = c / KC, kc = c % KC;
       uint32_t w[8];
-      const uint32_t x0[4] = {rb[i].x, rb[i].y, rb[i].z, rb[i].w};
+      const uint32_t x0[4] = {r.b[i][0], r.b[i][1], r.b[i][2], r.b[i][3]};
 #pragma unroll
       for (int d = 0; d < 4; ++d) expand_int4<BSIGNED>(x0[d], w[2 * d], w[2 * d + 1]);
-      uint4* dst = reinterpret_cast<uint4*>(&Bs[buf][row * kPitch + kc * 32]);
+      uint4* dst = reinterpret_cast<uint4*>(Bs + row * kPitch + kc * 32);
       dst[0] = make_uint4(w[0], w[1], w[2], w[3]);
       dst[1] = make_uint4(w[4], w[5], w[6], w[7]);
     }
   };
 
-  v4i acc[TM][TN];
+  v16i acc[TM][TN];
 #pragma unroll
   for (int i = 0; i < TM; ++i)
 #pragma unroll
-    for (int j = 0; j < TN; ++j) acc[i][j] = v4i{0, 0, 0, 0};
+    for (int j = 0; j < TN; ++j) acc[i][j] = v16i{};
 
-  if (nkt > 0) load_tiles(kbeg);
-  for (int t = 0; t < nkt; ++t) {
-    const int buf = t & 1;
-    store_tiles(buf);
-    __syncthreads();
-    if (t + 1 < nkt) load_tiles(kbeg + (int64_t)(t + 1) * kBK);
-    const uint8_t* as = &As[buf][(wm * (BM / 2) + (lane & 15)) * kPitch + (lane >> 4) * 16];
-    const uint8_t* bs = &Bs[buf][(wn * (BN / 2) + (lane & 15)) * kPitch + (lane >> 4) * 16];
+  // 32x32x32 MFMA operands: lane l supplies row l%32 and 16 consecutive k
+  // (positions 16*(l/32) .. +15 of the 32-k step) of its fragment.
+  auto compute = [&](int buf) {
+    const uint8_t* As = lds + buf * STAGE;
+    const uint8_t* as = As + (wm * (BM / 2) + (lane & 31)) * kPitch + (lane >> 5) * 16;
+    const uint8_t* bs = As + BM * kPitch + (wn * (BN / 2) + (lane & 31)) * kPitch + (lane >> 5) * 16;
 #pragma unroll
-    for (int kk = 0; kk < kBK; kk += 64) {
+    for (int kk = 0; kk < kBK; kk += 32) {
       v4i fa[TM], fb[TN];
 #pragma unroll
-      for (int i = 0; i < TM; ++i) fa[i] = *reinterpret_cast<const v4i*>(as + i * 16 * kPitch + kk);
+      for (int i = 0; i < TM; ++i) fa[i] = *reinterpret_cast<const v4i*>(as + i * 32 * kPitch + kk);
 #pragma unroll
-      for (int j = 0; j < TN; ++j) fb[j] = *reinterpret_cast<const v4i*>(bs + j * 16 * kPitch + kk);
+      for (int j = 0; j < TN; ++j) fb[j] = *reinterpret_cast<const v4i*>(bs + j * 32 * kPitch + kk);
 #pragma unroll
       for (int i = 0; i < TM; ++i)
 #pragma unroll
         for (int j = 0; j < TN; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_i32_16x16x64_i8(fa[i], fb[j], acc[i][j], 0, 0, 0);
+          acc[i][j] = __builtin_amdgcn_mfma_i32_32x32x32_i8(fb[j], fa[i], acc[i][j], 0, 0, 0);
     }
+  };
+
+  // One pipeline step: multiply stage `cb` out of LDS while expanding the
+  // registers `r` (the next stage) into the other buffer, then reload `rl`
+  // with stage `tload`.  The MFMAs, the expansion and the loads sit in one
+  // straight-line block between barriers.
+  auto step = [&](int cb, const Regs& r, Regs& rl, int tload) {
+    compute(cb);
+    expand_store(r, cb ^ 1);
+    load(rl, tload);
+    __syncthreads();
+  };
+
+  Regs r0, r1;
+  load(r0, 0);
+  load(r1, 1);
+  expand_store(r0, 0);
+  __syncthreads();
+  load(r0, 2);
+  // Stages beyond nkt load as zeros (masked), so an odd stage count ends on
+  // a zero-filled buffer that adds nothing.
+  for (int t = 0; t < nkt; t += 2) {
+    step(0, r1, r1, t + 3);   // multiply t, expand t+1 (r1), then reuse r1 for t+3
+    step(1, r0, r0, t + 4);   // multiply t+1, expand t+2 (r0), then reuse r0 for t+4
   }
 
-  // D layout of the 16x16 MFMA: lane l, register r -> row 4*(l/16)+r, column l%16
-  const int64_t rbase = m0 + wm * (BM / 2) + 4 * (lane >> 4);
-  const int64_t cbase = n0 + wn * (BN / 2) + (lane & 15);
-  if (a.partial) {
-    int32_t* P = a.partial + (int64_t)blockIdx.y * a.M * a.N;
+  // C[m][n] from the swapped MFMA: in tile (i, j), lane l holds row l%32 and,
+  // in registers 4q..4q+3, the 4 consecutive columns 8q + 4*(l/32) + 0..3.
+  const int64_t row0 = m0 + wm * (BM / 2) + (lane & 31);
+  const int64_t col0 = n0 + wn * (BN / 2) + 4 * (lane >> 5);
+  const float sc = a.partial ? 0.0f
+                             : __fmul_rn(__fmul_rn(*a.alpha, 1.0f / NS), *a.bscale) * (BSIGNED ? 0x1p-4f : 0x1p-3f);
 #pragma unroll
-    for (int i = 0; i < TM; ++i)
+  for (int i = 0; i < TM; ++i) {
+    const int64_t row = row0 + i * 32;
+    if (row >= a.M) continue;
 #pragma unroll
-      for (int j = 0; j < TN; ++j)
+    for (int j = 0; j < TN; ++j)
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int64_t row = rbase + i * 16 + r, col = cbase + j * 16;
-          if (row < a.M && col < a.N) P[row * a.N + col] = acc[i][j][r];
+      for (int q = 0; q < 4; ++q) {
+        const int64_t col = col0 + j * 32 + 8 * q;
+        const v4i v = {acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]};
+        if (a.partial) {
+          int32_t* P = a.partial + (int64_t)blockIdx.y * a.M * a.N + row * a.N;
+          if (a.vec && col + 3 < a.N) {
+            *reinterpret_cast<v4i*>(P + col) = v;
+          } else {
+#pragma unroll
+            for (int r = 0; r < 4; ++r)
+              if (col + r < a.N) P[col + r] = v[r];
+          }
+        } else {
+          float4 f;
+          f.x = __fmul_rn((float)v[0], sc);
+          f.y = __fmul_rn((float)v[1], sc);
+          f.z = __fmul_rn((float)v[2], sc);
+          f.w = __fmul_rn((float)v[3], sc);
+          float* Cr = a.C + row * a.N;
+          if (a.vec && col + 3 < a.N) {
+            *reinterpret_cast<float4*>(Cr + col) = f;
+          } else {
+            const float ff[4] = {f.x, f.y, f.z, f.w};
+#pragma unroll
+            for (int r = 0; r < 4; ++r)
+              if (col + r < a.N) Cr[col + r] = ff[r];
+          }
         }
-  } else {
-    const float sc = __fmul_rn(__fmul_rn(*a.alpha, 1.0f / NS), *a.bscale) * (BSIGNED ? 0x1p-4f : 0x1p-3f);
-#pragma unroll
-    for (int i = 0; i < TM; ++i)
-#pragma unroll
-      for (int j = 0; j < TN; ++j)
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int64_t row = rbase + i * 16 + r, col = cbase + j * 16;
-          if (row < a.M && col < a.N) a.C[row * a.N + col] = __fmul_rn((float)acc[i][j][r], sc);
-        }
+      }
   }
 }
 
-// Sums the split-K chunk sums in int64 (fixed order) and applies the scales.
+// Sums the split-K chunk sums in int64 and applies the scales.  A block owns
+// 64 consecutive outputs; its four waves add every fourth chunk (coalesced
+// 256-byte reads), then combine through LDS in a fixed order.
 template <int NS, bool BSIGNED>
 __global__ __launch_bounds__(256) void splitk_reduce_kernel(const int32_t* __restrict__ partial,
                                                             int splits, int64_t MN,
                                                             const float* alpha, const float* bscale,
                                                             float* __restrict__ C) {
-  const float sc = __fmul_rn(__fmul_rn(*alpha, 1.0f / NS), *bscale) * (BSIGNED ? 0x1p-4f : 0x1p-3f);
-  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < MN;
-       i += (int64_t)gridDim.x * blockDim.x) {
-    int64_t s = 0;
-    for (int p = 0; p < splits; ++p) s += partial[p * MN + i];
-    C[i] = __fmul_rn((float)s, sc);
+  __shared__ int64_t part[4][64];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int64_t i = (int64_t)blockIdx.x * 64 + lane;
+  int64_t s = 0;
+  if (i < MN) {
+    int p = wave;
+    for (; p + 12 < splits; p += 16) {
+      const int32_t v0 = partial[(int64_t)p * MN + i], v1 = partial[(int64_t)(p + 4) * MN + i];
+      const int32_t v2 = partial[(int64_t)(p + 8) * MN + i], v3 = partial[(int64_t)(p + 12) * MN + i];
+      s += (int64_t)v0 + v1 + v2 + v3;
+    }
+    for (; p < splits; p += 4) s += partial[(int64_t)p * MN + i];
+  }
+  part[wave][lane] = s;
+  __syncthreads();
+  if (wave == 0 && i < MN) {
+    const int64_t tot = part[0][lane] + part[1][lane] + part[2][lane] + part[3][lane];
+    const float sc = __fmul_rn(__fmul_rn(*alpha, 1.0f / NS), *bscale) * (BSIGNED ? 0x1p-4f : 0x1p-3f);
+    C[i] = __fmul_rn((float)tot, sc);
   }
 }
 
@@ -240,16 +360,29 @@ struct GemmPlan {
 
 static GemmPlan plan_gemm(int64_t M, int64_t N, int64_t K) {
   GemmPlan p;
-  p.bm = 128;
-  p.bn = 128;
+  auto tiles = [&](int bm, int bn) { return ((M + bm - 1) / bm) * ((N + bn - 1) / bn); };
+  // 256x256 tiles halve the expansion and LDS work per MAC but run one wave
+  // per SIMD; they pay off only for long reductions.  Short reductions (the
+  // conv dX with K = 64) are bound by the fp32 output and prefer the 128x128
+  // tile, which keeps two workgroups per CU.
+  if (K >= 1024 && tiles(256, 256) >= 256) {
+    p.bm = 256;
+    p.bn = 256;
+  } else if (tiles(128, 128) >= 128) {
+    p.bm = 128;
+    p.bn = 128;
+  } else {
+    p.bm = 64;
+    p.bn = 64;
+  }
   p.tiles_m = (M + p.bm - 1) / p.bm;
   p.tiles_n = (N + p.bn - 1) / p.bn;
-  const int64_t tiles = p.tiles_m * p.tiles_n;
-  const int64_t ktiles = (K + kBK - 1) / kBK;
+  const int64_t nt = p.tiles_m * p.tiles_n;
+  const int64_t ktiles = (K + kKAlign - 1) / kKAlign;
   int64_t splits = 1;
-  // too few tiles to fill 256 CUs: split the reduction (>= 8 k-tiles each)
-  if (tiles < 512) {
-    splits = (512 + tiles - 1) / tiles;
+  // too few tiles to fill 256 CUs: split the reduction (>= 8 k-stages each)
+  if (nt < 256) {
+    splits = (512 + nt - 1) / nt;
     const int64_t max_by_len = ktiles / 8 > 0 ? ktiles / 8 : 1;
     if (splits > max_by_len) splits = max_by_len;
   }
@@ -257,8 +390,8 @@ static GemmPlan plan_gemm(int64_t M, int64_t N, int64_t K) {
   const int64_t min_splits = (K + kMaxExactK - 1) / kMaxExactK;
   if (splits < min_splits) splits = min_splits;
   if (splits < 1) splits = 1;
-  int64_t chunk_tiles = (ktiles + splits - 1) / splits;
-  p.k_chunk = chunk_tiles * kBK;
+  const int64_t chunk_tiles = (ktiles + splits - 1) / splits;
+  p.k_chunk = chunk_tiles * kKAlign;
   p.splits = (int)((ktiles + chunk_tiles - 1) / chunk_tiles);
   return p;
 }
@@ -269,18 +402,29 @@ size_t gemm_workspace_bytes(int64_t M, int64_t N, int64_t K, int /*ns*/) {
   return (size_t)p.splits * (size_t)M * (size_t)N * sizeof(int32_t);
 }
 
+template <int BM, int BN, int BK, int NS, bool BSIGNED>
+static void launch_tile(const GemmArgs& a, dim3 grid, hipStream_t st) {
+  hipLaunchKernelGGL((gemm_luq_int4_kernel<BM, BN, BK, NS, BSIGNED>), grid, dim3(kGemmThreads), 0, st, a);
+}
+
 template <int NS, bool BSIGNED>
 static hipError_t gemm_launch_t(const GemmArgs& a0, const GemmPlan& p, hipStream_t st) {
   GemmArgs a = a0;
+  a.tiles_m = (int)p.tiles_m;
   a.tiles_n = (int)p.tiles_n;
   a.k_chunk = p.k_chunk;
   const dim3 grid((unsigned)(p.tiles_m * p.tiles_n), (unsigned)p.splits);
-  hipLaunchKernelGGL((gemm_luq_int4_kernel<128, 128, NS, BSIGNED>), grid, dim3(kGemmThreads), 0, st, a);
+  // 16-byte stores need 16-byte aligned rows
+  a.vec = (a.N % 4) == 0 && (((uintptr_t)(a.partial ? (void*)a.partial : (void*)a.C)) & 15) == 0;
+  if (p.bm == 256)
+    launch_tile<256, 256, 128, NS, BSIGNED>(a, grid, st);
+  else if (p.bm == 128)
+    launch_tile<128, 128, 128, NS, BSIGNED>(a, grid, st);
+  else
+    launch_tile<64, 64, 128, NS, BSIGNED>(a, grid, st);
   if (p.splits > 1) {
     const int64_t MN = a.M * a.N;
-    int64_t nb = (MN + 255) / 256;
-    if (nb > 8192) nb = 8192;
-    hipLaunchKernelGGL((splitk_reduce_kernel<NS, BSIGNED>), dim3((unsigned)nb), dim3(256), 0, st,
+    hipLaunchKernelGGL((splitk_reduce_kernel<NS, BSIGNED>), dim3((unsigned)((MN + 63) / 64)), dim3(256), 0, st,
                        a.partial, p.splits, MN, a.alpha, a.bscale, a.C);
   }
   return hipGetLastError();

@@ -207,8 +207,11 @@ def _gemm_case(L, M, N, K, ns, signed, seed):
     assert np.array_equal(dx, epilogue_replica(acc, ra, ns, wsr)), "dgrad epilogue not bit-exact"
 
 
+# shapes chosen to select each tile configuration (64x64 with and without
+# split-K, 128x128, 256x256) with ragged edges in M, N and K
 @pytest.mark.parametrize("M,N,K", [(256, 512, 512), (300, 200, 160), (37, 8, 32), (129, 136, 1056),
-                                   (64, 64, 32768), (512, 384, 2048)])
+                                   (64, 64, 32768), (512, 384, 2048), (1500, 1400, 224),
+                                   (4192, 4128, 288)])
 @pytest.mark.parametrize("ns", [1, 2])
 def test_dgrad_parity(L, M, N, K, ns):
     _gemm_case(L, M, N, K, ns, True, seed=M + N + K)
@@ -237,7 +240,8 @@ def _wgrad_case(L, T, Nout, Kin, ns, signed, seed):
     assert np.array_equal(dw, epilogue_replica(acc, ra, ns, sar)), "wgrad epilogue not bit-exact"
 
 
-@pytest.mark.parametrize("T,Nout,Kin", [(256, 512, 512), (96, 40, 24), (4096, 64, 96), (8192, 8, 136)])
+@pytest.mark.parametrize("T,Nout,Kin", [(256, 512, 512), (96, 40, 24), (4096, 64, 96), (8192, 8, 136),
+                                         (160, 1544, 1416), (96, 4104, 4120)])
 @pytest.mark.parametrize("ns", [1, 2])
 def test_wgrad_parity(L, T, Nout, Kin, ns):
     _wgrad_case(L, T, Nout, Kin, ns, signed=False, seed=T + Nout)
@@ -254,7 +258,7 @@ def test_gemm_long_reduction_exact_split(L):
 
 # ------------------------------- im2col -------------------------------------
 
-@pytest.mark.parametrize("B,H,W,C", [(2, 6, 8, 16), (1, 5, 8, 6), (3, 7, 8, 64)])
+@pytest.mark.parametrize("B,H,W,C", [(2, 6, 8, 16), (1, 5, 8, 6), (3, 7, 8, 64), (2, 4, 12, 8), (1, 1, 8, 8)])
 def test_im2col_parity(L, B, H, W, C):
     act = synth.half_normal((B, H, W, C), [400, C])
     announce("im2col", B, H, W, C)
@@ -263,3 +267,54 @@ def test_im2col_parity(L, B, H, W, C):
     rac, _ = oint4.int4_quantize(act, is_signed=False)
     col = oim2col.im2col3x3_codes(rac, B, H, W, C)
     assert_codes_equal(col_t, transpose_codes(col, B * H * W, 9 * C), "im2col_t")
+
+
+# ------------------------------- HIP graphs ---------------------------------
+
+def test_graph_replays_match_eager(L):
+    """The whole step captured in a HIP graph gives the eager results on every
+    replay, with eager work and synchronisations between replays."""
+    T, D, F = 256, 192, 320
+    d = synth.mlp(seed=5, T=T, D=D, F=F)
+    g, x, w = to_dev(d["g"]), to_dev(d["x"]), to_dev(d["W"])
+    u8 = lambda n: torch.empty(int(n), dtype=torch.uint8, device="cuda:0")
+    f1 = lambda: torch.empty(1, dtype=torch.float32, device="cuda:0")
+    gc, gct, al, mx = u8(2 * L.plane_bytes(T * F)), u8(2 * L.plane_bytes(T * F)), f1(), f1()
+    xct, sx, wct, sw = u8(T * D // 2), f1(), u8(F * D // 2), f1()
+    dx = torch.empty(T, D, device="cuda:0")
+    dw = torch.empty(F, D, device="cuda:0")
+    wq = u8(L.workspace_size(L.OP_QUANTIZE_GRAD, T * F))
+    wx = u8(L.workspace_size(L.OP_INT4_QUANTIZE, T * D))
+    ww = u8(L.workspace_size(L.OP_INT4_QUANTIZE, F * D))
+    wd = u8(max(L.workspace_size(L.OP_GEMM_DGRAD, T, D, F), 1))
+    wg = u8(max(L.workspace_size(L.OP_GEMM_WGRAD, T, F, D), 1))
+
+    def step():
+        L.luq_quantize_grad(g, 4, 17, 5, 2, gc, gct, al, mx, wq)
+        L.int4_quantize(x, True, 0.0, False, xct, sx, wx)
+        L.int4_quantize(w, True, 0.0, False, wct, sw, ww)
+        L.luq_gemm_dgrad(gc, al, wct, sw, True, T, D, F, 2, dx, wd)
+        L.luq_gemm_wgrad(gct, al, xct, sx, True, T, F, D, 2, dw, wg)
+
+    announce("graph eager reference")
+    step()
+    ref = [host(t).copy() for t in (gc, gct, al, xct, wct, dx, dw)]
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        step()
+    torch.cuda.current_stream().wait_stream(side)
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        step()
+    for rep in range(4):
+        for t in (gc, gct, xct, wct, dx, dw):
+            t.zero_()
+        torch.cuda.synchronize()
+        announce("graph replay", rep)
+        graph.replay()
+        torch.cuda.synchronize()
+        got = [host(t) for t in (gc, gct, al, xct, wct, dx, dw)]
+        for a, b in zip(ref, got):
+            assert np.array_equal(a, b), f"replay {rep} differs from eager"
+        _ = (torch.ones(1024, device="cuda:0") * 2).sum().item()   # eager work between replays
