@@ -20,9 +20,8 @@
 // multiplied by 2^100 (exact: scaling up by a power of two) so that this
 // holds for any finite input.
 //
-// The "tile" encoders also write the transposed code matrix: each lane owns
-// an 8x8 element block, packs its 8 row words and transposes them with a
-// 4-bit field-swap network in registers.
+// The "tile" encoders also write the transposed code matrix (see
+// encode_tiles below).
 #include "luq_device.hpp"
 #include "luq_launch.hpp"
 
@@ -73,6 +72,69 @@ __global__ __launch_bounds__(kThreads) void max_partial_kernel(const void* __res
   if (threadIdx.x == 0) partial[blockIdx.x] = m;
 }
 
+// ---------------------------- transposing tiles ----------------------------
+//
+// When the transposed code layout is requested, work goes by tiles of
+// TG column groups (8 columns each) by TR = 8192 / TG rows; TG is 32, or the
+// next power of two above the number of column groups for narrow matrices.
+//   Phase A: consecutive lanes take consecutive column groups of a row, so
+//            the loads and the row-major code stores of a row are contiguous;
+//            every 8-element code word also goes to LDS at [group][row].
+//   Phase B: consecutive lanes take consecutive 8-row blocks of one column
+//            group, read the block's 8 words (two 16-byte LDS reads),
+//            transpose them in registers and store one word per column, so
+//            consecutive lanes write consecutive words of a transposed row.
+constexpr int kTileWords = 8192;
+constexpr int kTilePad = 4;  // LDS words between column groups (keeps 16-byte alignment)
+
+template <int NS, typename Enc>
+__device__ __forceinline__ void encode_tiles(const Enc& enc, int64_t rows, int64_t cols, int lg,
+                                             uint8_t* codes, uint8_t* codes_t, int64_t plane,
+                                             uint32_t* lds) {
+  const int tg = 1 << lg, tr = kTileWords >> lg, pitch = tr + kTilePad;
+  const int64_t cgs = cols >> 3;
+  const int64_t ntr = (rows + tr - 1) / tr, ntc = (cgs + tg - 1) / tg;
+  for (int64_t t = blockIdx.x; t < ntr * ntc; t += gridDim.x) {
+    const int64_t r0 = (t / ntc) * tr, g0 = (t % ntc) * tg;
+    for (int q = threadIdx.x; q < kTileWords; q += kThreads) {
+      const int g = q & (tg - 1), r = q >> lg;
+      const int64_t row = r0 + r, cg = g0 + g;
+      uint32_t w[NS];
+#pragma unroll
+      for (int s = 0; s < NS; ++s) w[s] = 0;
+      if (row < rows && cg < cgs) {
+        const int64_t e0 = row * cols + cg * 8;
+        const U8 v = enc.load(e0);
+#pragma unroll
+        for (int s = 0; s < NS; ++s) {
+          w[s] = enc.word(v, (uint64_t)(e0 >> 3), s);
+          if (codes) *reinterpret_cast<uint32_t*>(codes + s * plane + (e0 >> 1)) = w[s];
+        }
+      }
+#pragma unroll
+      for (int s = 0; s < NS; ++s) lds[(s * tg + g) * pitch + r] = w[s];
+    }
+    __syncthreads();
+    const int rbs = tr >> 3;  // 8-row blocks per tile
+    for (int q = threadIdx.x; q < kTileWords / 8; q += kThreads) {
+      const int rb = q & (rbs - 1), g = q / rbs;
+      const int64_t row0 = r0 + rb * 8, cg = g0 + g;
+      if (row0 >= rows || cg >= cgs) continue;
+#pragma unroll
+      for (int s = 0; s < NS; ++s) {
+        const uint4* src = reinterpret_cast<const uint4*>(lds + (s * tg + g) * pitch + rb * 8);
+        const uint4 lo = src[0], hi = src[1];
+        uint32_t w8[8] = {lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
+        transpose8x8_nibbles(w8);
+        uint8_t* dst = codes_t + s * plane + (cg * 8) * (rows >> 1) + (row0 >> 1);
+#pragma unroll
+        for (int c = 0; c < 8; ++c) *reinterpret_cast<uint32_t*>(dst + c * (rows >> 1)) = w8[c];
+      }
+    }
+    __syncthreads();
+  }
+}
+
 // ------------------------------- LUQ ---------------------------------------
 
 struct LuqParams {
@@ -114,36 +176,47 @@ __device__ __forceinline__ LuqParams luq_params(uint32_t mbits, int R, float* al
 }
 
 // One element's 4-bit LUQ code from its float32 bits and 16-bit uniform.
-__device__ __forceinline__ uint32_t luq_nibble(uint32_t b, uint32_t j, const LuqParams& p) {
-  const float as = __uint_as_float(b & 0x7FFFFFFFu) * p.S;
-  const uint32_t ab = __float_as_uint(as);
-  const bool under = as < p.alpha_s;  // stochastic underflow bin [0, alpha)
-  const bool top = as >= p.ltop_s;    // the largest level
-  // bin index n: the largest n with alpha * 2^n <= |x| (meaningful when
-  // neither under nor top, where |x| and alpha are normal floats)
-  const uint32_t n = (ab >> 23) - p.e_alpha - ((ab & 0x7FFFFFu) < p.m_alpha ? 1u : 0u);
-  const float lo = under ? 0.0f : __uint_as_float(p.a_bits + (n << 23));
-  const float w16 = under ? p.alpha16_s : __uint_as_float(p.a16_bits + (n << 23));
-  const float d = as - lo;  // exact
-  const bool up = fmaf((float)j, w16, -d) < 0.0f;
-  const uint32_t field = top ? p.top_field : (under ? (uint32_t)up : n + 1u + (uint32_t)up);
-  const uint32_t sgn = (field != 0u) ? ((b >> 31) << 3) : 0u;
-  return field | sgn;
+//
+// On scaled magnitudes (both normal once |x| >= alpha), the difference of the
+// float bit patterns D = bits(|x|) - bits(alpha) has D >> 23 equal to
+// floor(log2(|x| / alpha)): the exponent difference, less one when the
+// mantissa of |x| is below that of alpha (the borrow).  So n = D >> 23 is the
+// bin index, n < 0 is the underflow bin [0, alpha) and n >= R the top level.
+// The bin width is alpha * 2^max(n, 0), built by adding max(n,0) to the
+// exponent field; the lower level is that width, or 0 in the underflow bin.
+// The field is clamp(n, -1, R) + 1 + up, capped at R + 1 (where `up` is
+// irrelevant).
+template <bool SCALED>
+__device__ __forceinline__ uint32_t luq_field(uint32_t b, uint32_t j, const LuqParams& p) {
+  const float mag = __uint_as_float(b & 0x7FFFFFFFu);
+  const float as = SCALED ? mag * p.S : mag;
+  const int32_t D = (int32_t)__float_as_uint(as) - (int32_t)p.a_bits;
+  const int32_t n = D >> 23;
+  const uint32_t wb = p.a_bits + ((uint32_t)max(n, 0) << 23);
+  const float lo = __uint_as_float(n < 0 ? 0u : wb);
+  const float w16 = __uint_as_float(wb - (16u << 23));  // exponent of alpha is >= 78
+  const bool up = fmaf((float)j, w16, lo - as) < 0.0f;   // lo - as = -d, exact
+  return (uint32_t)min(max(n, -1) + 1 + (int32_t)up, (int32_t)p.top_field);
 }
 
-// Codes of 8 consecutive elements (bits in v) for Philox block `blk`.
+// Codes of 8 consecutive elements (bits in v) for Philox block `blk`: the
+// exponent fields are packed first, then each sign bit is set where its field
+// is non-zero (zero is always +0).
+template <bool SCALED>
 __device__ __forceinline__ uint32_t luq_word(const U8& v, uint64_t blk, uint32_t sample,
                                              uint32_t counter, uint32_t k0, uint32_t k1,
                                              const LuqParams& p) {
   const U4 y = philox4x32_10(U4{(uint32_t)blk, (uint32_t)(blk >> 32), sample, counter}, k0, k1);
   const uint32_t w[4] = {y.x, y.y, y.z, y.w};
-  uint32_t out = 0;
+  uint32_t fields = 0, signs = 0;
 #pragma unroll
   for (int e = 0; e < 8; ++e) {
     const uint32_t j = (e & 1) ? (w[e >> 1] >> 16) : (w[e >> 1] & 0xFFFFu);
-    out |= luq_nibble(v.v[e], j, p) << (4 * e);
+    fields |= luq_field<SCALED>(v.v[e], j, p) << (4 * e);
+    signs |= (v.v[e] >> 31) << (4 * e + 3);
   }
-  return out;
+  const uint32_t nz = (fields | (fields >> 1) | (fields >> 2)) & 0x11111111u;
+  return fields | (signs & (nz << 3));
 }
 
 struct LuqArgs {
@@ -173,60 +246,60 @@ __device__ __forceinline__ LuqParams luq_block_params(const LuqArgs& a) {
 }
 
 // Flat row-major codes; groups of 8 elements along the flattened tensor.
-template <bool BF16, int NS>
-__global__ __launch_bounds__(kThreads) void luq_encode_flat_kernel(LuqArgs a) {
-  const LuqParams p = luq_block_params(a);
-  const int64_t ngroups = (a.n + 7) >> 3;
-  for (int64_t g = (int64_t)blockIdx.x * kThreads + threadIdx.x; g < ngroups;
+template <bool BF16, int NS, bool SCALED>
+__device__ __forceinline__ void luq_flat_body(const LuqArgs& a, const LuqParams& p) {
+  const int64_t nfull = a.n >> 3;
+  for (int64_t g = (int64_t)blockIdx.x * kThreads + threadIdx.x; g < nfull;
        g += (int64_t)gridDim.x * kThreads) {
-    const bool full = (g * 8 + 8) <= a.n;
-    const U8 v = full ? load8<BF16>(a.g, g * 8) : load8_tail<BF16>(a.g, g * 8, a.n);
+    const U8 v = load8<BF16>(a.g, g * 8);
 #pragma unroll
-    for (int s = 0; s < NS; ++s) {
-      const uint32_t word = p.zero ? 0u : luq_word(v, (uint64_t)g, s, a.counter, a.k0, a.k1, p);
-      uint8_t* dst = a.codes + s * a.plane + g * 4;
-      if (full)
-        *reinterpret_cast<uint32_t*>(dst) = word;
-      else
-        store_bytes(dst, word, (int)((a.n - g * 8 + 1) >> 1));
-    }
+    for (int s = 0; s < NS; ++s)
+      *reinterpret_cast<uint32_t*>(a.codes + s * a.plane + g * 4) =
+          luq_word<SCALED>(v, (uint64_t)g, s, a.counter, a.k0, a.k1, p);
+  }
+  if ((a.n & 7) && blockIdx.x == 0 && threadIdx.x == 0) {
+    const U8 v = load8_tail<BF16>(a.g, nfull * 8, a.n);
+#pragma unroll
+    for (int s = 0; s < NS; ++s)
+      store_bytes(a.codes + s * a.plane + nfull * 4,
+                  luq_word<SCALED>(v, (uint64_t)nfull, s, a.counter, a.k0, a.k1, p),
+                  (int)(((a.n & 7) + 1) >> 1));
   }
 }
 
-// Tile encoder: rows % 8 == 0 and cols % 8 == 0.  A block covers 128 x 128
-// elements as 2 x 2 wave tiles of 8 x 8 lanes, each lane an 8 x 8 block.
 template <bool BF16, int NS>
-__global__ __launch_bounds__(kThreads) void luq_encode_tile_kernel(LuqArgs a) {
+__global__ __launch_bounds__(kThreads) void luq_encode_flat_kernel(LuqArgs a) {
   const LuqParams p = luq_block_params(a);
-  const int64_t RB = a.rows >> 3, CB = a.cols >> 3;
-  const int64_t ntr = (RB + 15) >> 4, ntc = (CB + 15) >> 4;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int lr = (wave >> 1) * 8 + (lane >> 3), lc = (wave & 1) * 8 + (lane & 7);
-  for (int64_t t = blockIdx.x; t < ntr * ntc; t += gridDim.x) {
-    const int64_t R = (t / ntc) * 16 + lr, C = (t % ntc) * 16 + lc;
-    if (R >= RB || C >= CB) continue;
-    uint32_t rw[NS][8];
-#pragma unroll
-    for (int r = 0; r < 8; ++r) {
-      const int64_t e0 = (R * 8 + r) * a.cols + C * 8;
-      const U8 v = load8<BF16>(a.g, e0);
-#pragma unroll
-      for (int s = 0; s < NS; ++s) {
-        rw[s][r] = p.zero ? 0u : luq_word(v, (uint64_t)(e0 >> 3), s, a.counter, a.k0, a.k1, p);
-        if (a.codes) *reinterpret_cast<uint32_t*>(a.codes + s * a.plane + (e0 >> 1)) = rw[s][r];
-      }
-    }
-    if (a.codes_t) {
-#pragma unroll
-      for (int s = 0; s < NS; ++s) {
-        transpose8x8_nibbles(rw[s]);
-#pragma unroll
-        for (int c = 0; c < 8; ++c)
-          *reinterpret_cast<uint32_t*>(a.codes_t + s * a.plane + (C * 8 + c) * (a.rows >> 1) + R * 4) =
-              rw[s][c];
-      }
-    }
+  if (p.zero) {  // alpha is 0 or NaN: every code is 0
+    const int64_t nbytes = (a.n + 1) >> 1;
+    for (int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x; i < nbytes; i += (int64_t)gridDim.x * kThreads)
+      for (int s = 0; s < NS; ++s) a.codes[s * a.plane + i] = 0;
+    return;
   }
+  if (p.S != 1.0f)
+    luq_flat_body<BF16, NS, true>(a, p);
+  else
+    luq_flat_body<BF16, NS, false>(a, p);
+}
+
+template <bool BF16, bool SCALED>
+struct LuqEnc {
+  const LuqArgs* a;
+  const LuqParams* p;
+  __device__ U8 load(int64_t e0) const { return load8<BF16>(a->g, e0); }
+  __device__ uint32_t word(const U8& v, uint64_t blk, int s) const {
+    return p->zero ? 0u : luq_word<SCALED>(v, blk, s, a->counter, a->k0, a->k1, *p);
+  }
+};
+
+template <bool BF16, int NS>
+__global__ __launch_bounds__(kThreads) void luq_encode_tile_kernel(LuqArgs a, int lg) {
+  __shared__ __attribute__((aligned(16))) uint32_t lds[NS * (kTileWords + 32 * kTilePad)];
+  const LuqParams p = luq_block_params(a);
+  if (p.S != 1.0f)
+    encode_tiles<NS>(LuqEnc<BF16, true>{&a, &p}, a.rows, a.cols, lg, a.codes, a.codes_t, a.plane, lds);
+  else
+    encode_tiles<NS>(LuqEnc<BF16, false>{&a, &p}, a.rows, a.cols, lg, a.codes, a.codes_t, a.plane, lds);
 }
 
 __global__ void write_two_floats_kernel(float* a, float va, float* b, float vb) {
@@ -318,30 +391,18 @@ __global__ __launch_bounds__(kThreads) void int4_encode_flat_kernel(Int4Args a) 
 }
 
 template <bool BF16>
-__global__ __launch_bounds__(kThreads) void int4_encode_tile_kernel(Int4Args a) {
+struct Int4Enc {
+  const Int4Args* a;
+  const Int4Params* p;
+  __device__ U8 load(int64_t e0) const { return load8<BF16>(a->x, e0); }
+  __device__ uint32_t word(const U8& v, uint64_t, int) const { return p->zero ? 0u : int4_word(v, *p); }
+};
+
+template <bool BF16>
+__global__ __launch_bounds__(kThreads) void int4_encode_tile_kernel(Int4Args a, int lg) {
+  __shared__ __attribute__((aligned(16))) uint32_t lds[kTileWords + 32 * kTilePad];
   const Int4Params p = int4_block_params(a);
-  const int64_t RB = a.rows >> 3, CB = a.cols >> 3;
-  const int64_t ntr = (RB + 15) >> 4, ntc = (CB + 15) >> 4;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int lr = (wave >> 1) * 8 + (lane >> 3), lc = (wave & 1) * 8 + (lane & 7);
-  for (int64_t t = blockIdx.x; t < ntr * ntc; t += gridDim.x) {
-    const int64_t R = (t / ntc) * 16 + lr, C = (t % ntc) * 16 + lc;
-    if (R >= RB || C >= CB) continue;
-    uint32_t rw[8];
-#pragma unroll
-    for (int r = 0; r < 8; ++r) {
-      const int64_t e0 = (R * 8 + r) * a.cols + C * 8;
-      const U8 v = load8<BF16>(a.x, e0);
-      rw[r] = p.zero ? 0u : int4_word(v, p);
-      if (a.codes) *reinterpret_cast<uint32_t*>(a.codes + (e0 >> 1)) = rw[r];
-    }
-    if (a.codes_t) {
-      transpose8x8_nibbles(rw);
-#pragma unroll
-      for (int c = 0; c < 8; ++c)
-        *reinterpret_cast<uint32_t*>(a.codes_t + (C * 8 + c) * (a.rows >> 1) + R * 4) = rw[c];
-    }
-  }
+  encode_tiles<1>(Int4Enc<BF16>{&a, &p}, a.rows, a.cols, lg, a.codes, a.codes_t, 0, lds);
 }
 
 // ------------------------------- launchers ---------------------------------
@@ -364,8 +425,18 @@ static int encode_blocks_flat(int64_t n) {
   return (int)b;
 }
 
+// log2 of the column groups per transposing tile
+static int tile_lg(int64_t cols) {
+  const int64_t cgs = cols >> 3;
+  int lg = 0;
+  while (lg < 5 && (1LL << lg) < cgs) ++lg;
+  return lg;
+}
+
 static int encode_blocks_tile(int64_t rows, int64_t cols) {
-  const int64_t tiles = (((rows >> 3) + 15) >> 4) * (((cols >> 3) + 15) >> 4);
+  const int lg = tile_lg(cols);
+  const int64_t tr = kTileWords >> lg, tg = 1LL << lg;
+  const int64_t tiles = ((rows + tr - 1) / tr) * (((cols >> 3) + tg - 1) / tg);
   int64_t b = tiles < 1 ? 1 : tiles;
   if (b > kMaxEncodeBlocks) b = kMaxEncodeBlocks;
   return (int)b;
@@ -378,9 +449,9 @@ static hipError_t luq_launch_t(const LuqArgs& a, int ns, int nmax, hipStream_t s
   if (a.codes_t) {
     const int nb = encode_blocks_tile(a.rows, a.cols);
     if (ns == 1)
-      hipLaunchKernelGGL((luq_encode_tile_kernel<BF16, 1>), dim3(nb), dim3(kThreads), 0, st, a);
+      hipLaunchKernelGGL((luq_encode_tile_kernel<BF16, 1>), dim3(nb), dim3(kThreads), 0, st, a, tile_lg(a.cols));
     else
-      hipLaunchKernelGGL((luq_encode_tile_kernel<BF16, 2>), dim3(nb), dim3(kThreads), 0, st, a);
+      hipLaunchKernelGGL((luq_encode_tile_kernel<BF16, 2>), dim3(nb), dim3(kThreads), 0, st, a, tile_lg(a.cols));
   } else {
     const int nb = encode_blocks_flat(a.n);
     if (ns == 1)
@@ -431,7 +502,7 @@ static hipError_t int4_launch_t(const Int4Args& a, hipStream_t st) {
   }
   if (a.codes_t)
     hipLaunchKernelGGL((int4_encode_tile_kernel<BF16>), dim3(encode_blocks_tile(a.rows, a.cols)),
-                       dim3(kThreads), 0, st, a);
+                       dim3(kThreads), 0, st, a, tile_lg(a.cols));
   else
     hipLaunchKernelGGL((int4_encode_flat_kernel<BF16>), dim3(encode_blocks_flat(a.n)),
                        dim3(kThreads), 0, st, a);
