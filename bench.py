@@ -37,6 +37,8 @@ def parse():
     p.add_argument("--warmup", type=int, default=5)
     p.add_argument("--workload", default="resnet", choices=["resnet", "mlp", "mlp_smp", "small"])
     p.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
+    p.add_argument("--calibrate-copy", action="store_true",
+                   help="only run a plain 512 MiB device-to-device copy (HBM counter calibration)")
     return p.parse_args()
 
 
@@ -165,9 +167,10 @@ def time_stages(torch, stages, steps, warmup):
     step_s = time_graph(torch, step, steps)
     per = {}
     for s in stages:
-        g = capture(torch, [s.fn])
+        # ten launches per graph, so one replay's submission cost is shared
+        g = capture(torch, [s.fn] * 10)
         g.replay()
-        per[s.name] = time_graph(torch, g, max(10, steps))
+        per[s.name] = time_graph(torch, g, max(4, steps // 2)) / 10
     return step_s, per
 
 
@@ -189,28 +192,35 @@ def cpu_baseline(workload, d):
         parts.append(f"{label} {dt:.2f}s")
 
     if workload == "resnet":
+        # the whole step (about 20 s of CPU work)
         p = synth.RESNET
-        C, Co = p["C"], p["Cout"]
-        n = 1 << 20
-        g = d["g"].reshape(-1)[:n]
-        timed("luq 2^20", lambda: oluq.luq_quantize(g, R=4), 2 * 4 * n + n / 2)
-        act = d["act"].reshape(-1)[:n]
-        timed("int4 2^20", lambda: oint4.int4_quantize(act, is_signed=False), 2 * 4 * n + n / 2)
-        img = d["act"][:2]
-        codes, _ = oint4.int4_quantize(img, is_signed=False)
-        timed("im2col 2 images", lambda: oim2col.im2col3x3_codes(codes, 2, p["H"], p["W"], C),
-              img.size / 2 + 9 * img.size / 2)
-        gcodes, alpha, _ = oluq.luq_quantize(d["g"][:8192], R=4)
-        K, N = Co, 9 * C
-        wcn, wsn = oint4.int4_quantize(np.ascontiguousarray(d["W"]), is_signed=True)  # [Co, 9C] = [K, N]
-        timed("dgrad 8192 rows", lambda: ogemm.gemm_dgrad_ref(gcodes, alpha, wcn, wsn, True, 8192, N, K),
-              8192 * K / 2 + 4 * 8192 * N, 2.0 * 8192 * N * K)
-        colc = oim2col.im2col3x3_codes(codes, 2, p["H"], p["W"], C)
-        gc2, a2, _ = oluq.luq_quantize(d["g"][: 2 * p["H"] * p["W"]], R=4)
-        T2 = 2 * p["H"] * p["W"]
-        timed("wgrad 2 images", lambda: ogemm.gemm_wgrad_ref(gc2, a2, colc, 1.0, False, T2, Co, N),
-              T2 * (Co + N) / 2, 2.0 * T2 * Co * N)
-        sample = "LUQ and INT4 on 2^20 elements, im2col and dW on 2 images, dX on 8192 rows"
+        B, H, W, C, Co = p["B"], p["H"], p["W"], p["C"], p["Cout"]
+        T, K9 = B * H * W, 9 * C
+        n_g, n_a, n_w = T * Co, T * C, Co * K9
+        out = {}
+
+        def luq():
+            out["g"] = oluq.luq_quantize(d["g"], R=4)
+
+        def act():
+            out["a"] = oint4.int4_quantize(d["act"], is_signed=False)
+
+        def col():
+            out["col"] = oim2col.im2col3x3_codes(out["a"][0], B, H, W, C)
+
+        def wq():
+            out["w"] = oint4.int4_quantize(d["W"], is_signed=True)
+
+        timed("luq", luq, 2 * 4 * n_g + 2 * n_g / 2)
+        timed("int4(act)", act, 2 * 4 * n_a + n_a / 2)
+        timed("im2col", col, n_a / 2 + K9 * T / 2)
+        timed("int4(W)", wq, 2 * 4 * n_w + n_w / 2)
+        gc, ga, _ = out["g"]
+        timed("dX", lambda: ogemm.gemm_dgrad_ref(gc, ga, out["w"][0], out["w"][1], True, T, K9, Co),
+              T * Co / 2 + K9 * Co / 2 + 4 * T * K9, 2.0 * T * K9 * Co)
+        timed("dW", lambda: ogemm.gemm_wgrad_ref(gc, ga, out["col"], out["a"][1], False, T, Co, K9),
+              Co * T / 2 + K9 * T / 2 + 4 * Co * K9, 2.0 * T * K9 * Co)
+        sample = "the whole step"
     else:
         n = 1 << 20
         g = d["g"].reshape(-1)[:n]
@@ -231,12 +241,49 @@ def cpu_baseline(workload, d):
             "cpu_seconds": round(t_cpu, 3)}
 
 
+PROFILES = os.path.join(ROOT, "profiles")
+KERNEL_SOURCES = {"luq_gemm_dgrad": "gemm.hip", "luq_gemm_wgrad": "gemm.hip",
+                  "luq_quantize_grad": "quant.hip", "int4_im2col3x3_t": "im2col.hip"}
+
+
+def measured_traffic(kernel, workload):
+    """HBM bytes per launch from the committed counter summary, if it was taken
+    on the current kernel source (else None)."""
+    import hashlib
+    path = os.path.join(PROFILES, f"{kernel}_{workload}_traffic.md")
+    src = KERNEL_SOURCES.get(kernel)
+    if not src or not os.path.exists(path):
+        return None
+    fields = {}
+    for line in open(path):
+        if ":" in line and line.strip().startswith("- "):
+            k, v = line.strip()[2:].split(":", 1)
+            fields[k.strip()] = v.strip().strip("`")
+    h = hashlib.sha256(open(os.path.join(ROOT, "paper_2112_10769_amd", "csrc", src), "rb").read()).hexdigest()
+    if fields.get("source_sha256") != h or "hbm_bytes_per_launch" not in fields:
+        return None
+    return float(fields["hbm_bytes_per_launch"])
+
+
+def calibrate_copy(torch):
+    n = 512 << 20
+    src = torch.empty(n // 4, dtype=torch.float32, device="cuda:0").fill_(1.0)
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"calibration": "device copy", "bytes_read": n, "bytes_written": n, "launches": 3}), flush=True)
+
+
 def main():
     args = parse()
     if args.gpus != 1:
         print(json.dumps({"error": "this build measures one GPU only; --gpus must be 1"}))
         sys.exit(2)
     import torch
+    if args.calibrate_copy:
+        calibrate_copy(torch)
+        return
     import paper_2112_10769_amd as L
     dev = torch.device("cuda:0")
     if args.workload == "resnet":
@@ -256,12 +303,15 @@ def main():
                            "bound": s.bound(), "frac": round(s.roofline_s() / t, 4)}
     dom = max(stages, key=lambda s: per[s.name])
     t = per[dom.name]
+    traffic = measured_traffic(dom.name, cfg["workload"])
     if dom.bound() == "hbm":
         roof = {"kernel": dom.name, "bound": "hbm", "achieved": round(dom.bytes / t / 1e9, 1), "peak": 8000.0,
-                "unit": "GB/s", "frac": round(dom.bytes / t / HBM_PEAK, 4), "traffic": None}
+                "unit": "GB/s", "frac": round(dom.bytes / t / HBM_PEAK, 4), "traffic": traffic}
     else:
         roof = {"kernel": dom.name, "bound": "mfma", "achieved": round(dom.ops / t / 1e12, 1), "peak": 5000.0,
-                "unit": "TFLOP/s", "frac": round(dom.ops / t / I8_PEAK, 4), "traffic": None}
+                "unit": "TFLOP/s", "frac": round(dom.ops / t / I8_PEAK, 4), "traffic": traffic}
+    roof["algorithmic_bytes"] = dom.bytes
+    roof["launch_us"] = round(t * 1e6, 2)
     out = {
         "metric": METRIC, "value": round(100.0 * roof_total / step_s, 2), "unit": "% of roofline",
         "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(step_s * 1e3, 4),
