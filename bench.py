@@ -1,6 +1,7 @@
 """Benchmark of the LUQ 4-bit backward hot path on one MI355X.
 
-    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload resnet|mlp|mlp_smp|small]
+    python bench.py [--gpus 1] [--steps K] [--warmup W]
+                    [--workload resnet|mlp|mlp_smp|small|luq_sweep]
 
 A step is one pass of the whole hot path over one batch of synthetic input,
 inputs resident in HBM:
@@ -15,6 +16,12 @@ measured step time, in percent.  Per-kernel GB/s and TOPS are listed too.
 `roofline` describes the dominant kernel, timed with HIP events on the
 stream it runs on; `cpu_baseline` times the CPU oracle on a bounded sample
 of the same workload.
+
+`--workload luq_sweep` measures the LUQ quantizer alone on 1-D gradients of
+2^20..2^30 elements (fp32 and bf16, lognormal magnitudes exp(N(-10, 3)),
+random sign, 25% zeros; 0% and 50% zeros at 2^28): `value` is then the
+quantizer's mean fraction of the HBM roofline over the sizes >= 2^27, and
+`sweep` lists every size.
 """
 import argparse
 import json
@@ -35,8 +42,10 @@ def parse():
     p.add_argument("--gpus", type=int, default=1)
     p.add_argument("--steps", type=int, default=20)
     p.add_argument("--warmup", type=int, default=5)
-    p.add_argument("--workload", default="resnet", choices=["resnet", "mlp", "mlp_smp", "small"])
+    p.add_argument("--workload", default="resnet", choices=["resnet", "mlp", "mlp_smp", "small", "luq_sweep"])
     p.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
+    p.add_argument("--sweep-log2", default=None,
+                   help="comma-separated log2 sizes for luq_sweep (default: 20,22,24,26..30)")
     p.add_argument("--calibrate-copy", action="store_true",
                    help="only run a plain 512 MiB device-to-device copy (HBM counter calibration)")
     return p.parse_args()
@@ -88,18 +97,20 @@ def build_resnet(L, torch, dev):
         Stage("luq_gemm_wgrad", lambda: L.luq_gemm_wgrad(gct, alpha, colt, sa, False, T, Co, Ki, 1, dw, wsg),
               Co * T / 2 + Ki * T / 2 + 4 * Co * Ki, 2.0 * T * Ki * Co),
     ]
+    d["dev"] = dict(g=g, act=act, w=w, gc=gc, gct=gct, alpha=alpha, gmax=gmax, ac=ac, sa=sa, colt=colt,
+                    wct=wct, sw=sw, dx=dx, dw=dw)
     cfg = {"workload": "resnet50_conv3x3_bwd", "batch": B, "hw": [H, W], "cin": C, "cout": Co,
            "gemm_dgrad_MNK": [T, Ki, Co], "gemm_wgrad_MNK": [Co, Ki, T], "grad": "lognormal(-12,2.5) fp32, 50% zeros",
            "R": 4, "n_samples": 1}
     return stages, cfg, d
 
 
-def build_mlp(L, torch, dev, ns=1, T=None, D=None, F=None):
+def build_mlp(L, torch, dev, ns=1, T=None, D=None, F=None, d=None):
     import synth
     T = T or synth.MLP["T"]
     D = D or synth.MLP["D"]
     F = F or synth.MLP["F"]
-    d = synth.mlp(T=T, D=D, F=F)
+    d = dict(d) if d is not None else synth.mlp(T=T, D=D, F=F)
     bf = lambda a: torch.from_numpy(a.view("int16")).to(dev).view(torch.bfloat16)
     g, x = bf(d["g"]), bf(d["x"])                                     # [T, F], [T, D]
     w = torch.from_numpy(d["W"]).to(dev)                              # [F, D]
@@ -126,9 +137,84 @@ def build_mlp(L, torch, dev, ns=1, T=None, D=None, F=None):
         Stage("luq_gemm_wgrad", lambda: L.luq_gemm_wgrad(gct, alpha, xct, sx, True, T, F, D, ns, dw, wsg),
               ns * F * T / 2 + D * T / 2 + 4 * F * D, 2.0 * T * D * F),
     ]
+    d["dev"] = dict(g=g, x=x, w=w, gc=gc, gct=gct, alpha=alpha, gmax=gmax, xct=xct, sx=sx, wct=wct, sw=sw,
+                    dx=dx, dw=dw)
     cfg = {"workload": "transformer_mlp_bwd" + ("_smp2" if ns == 2 else ""), "tokens": T, "d_model": D,
            "hidden": F, "grad": "lognormal(-14,3) bf16", "R": 4, "n_samples": ns}
     return stages, cfg, d
+
+
+SWEEP_LOG2 = (20, 22, 24, 26, 27, 28, 29, 30)
+
+
+def device_lognormal(torch, n, mu, sigma, zero_frac, seed, dtype):
+    """Gradient-like tensor drawn on the device: |g| = exp(N(mu, sigma)),
+    random sign, a fraction of exact zeros (inputs only; no method arithmetic)."""
+    gen = torch.Generator(device="cuda:0")
+    gen.manual_seed(seed)
+    g = torch.randn(n, generator=gen, device="cuda:0")
+    g.mul_(sigma).add_(mu).exp_()
+    sign = torch.rand(n, generator=gen, device="cuda:0") < 0.5
+    g[sign] = -g[sign]
+    del sign
+    if zero_frac > 0:
+        g[torch.rand(n, generator=gen, device="cuda:0") < zero_frac] = 0.0
+    return g if dtype == "f32" else g.to(torch.bfloat16)
+
+
+def run_sweep(L, torch, steps, sizes=None):
+    dev = torch.device("cuda:0")
+    sizes = sizes or SWEEP_LOG2
+    cases = [(k, dt, 0.25) for dt in ("f32", "bf16") for k in sizes]
+    if sizes == SWEEP_LOG2:
+        cases += [(28, dt, z) for dt in ("f32", "bf16") for z in (0.0, 0.5)]
+    rows = []
+    for k, dt, z in cases:
+        n = 1 << k
+        g = device_lognormal(torch, n, -10.0, 3.0, z, 4000 + 10 * k + (dt == "bf16"), dt)
+        s_in = 4 if dt == "f32" else 2
+        codes = torch.empty(L.plane_bytes(n), dtype=torch.uint8, device=dev)
+        alpha = torch.empty(1, dtype=torch.float32, device=dev)
+        gmax = torch.empty(1, dtype=torch.float32, device=dev)
+        ws = torch.empty(L.workspace_size(L.OP_QUANTIZE_GRAD, n), dtype=torch.uint8, device=dev)
+        fn = lambda: L.luq_quantize_grad(g, 4, 0, 0, 1, codes, False, alpha, gmax, ws)
+        per_graph = 10 if k >= 26 else 50
+        gr = capture(torch, [fn] * per_graph)
+        gr.replay()
+        t = time_graph(torch, gr, max(3, steps // 4)) / per_graph
+        alg = 2 * n * s_in + n / 2
+        rows.append({"log2_n": k, "dtype": dt, "zeros": z, "us": round(t * 1e6, 2),
+                     "GB/s": round(alg / t / 1e9, 1), "frac": round(alg / t / HBM_PEAK, 4),
+                     "single_read_GB/s": round((n * s_in + n / 2) / t / 1e9, 1)})
+        del g, codes, ws, gr
+        torch.cuda.empty_cache()
+    big = [r["frac"] for r in rows if r["log2_n"] >= min(27, max(sizes)) and r["zeros"] == 0.25]
+    top = max((r for r in rows if r["zeros"] == 0.25 and r["dtype"] == "f32"), key=lambda r: r["log2_n"])
+    n = 1 << top["log2_n"]
+    roof = {"kernel": "luq_quantize_grad (max pass + encode)", "bound": "hbm",
+            "achieved": top["GB/s"], "peak": 8000.0, "unit": "GB/s", "frac": top["frac"],
+            "traffic": None, "algorithmic_bytes": 2 * n * 4 + n / 2, "launch_us": top["us"]}
+    cfg = {"workload": "luq_quantizer_sweep", "sizes": [f"2^{k}" for k in sizes],
+           "dtypes": ["f32", "bf16"], "grad": "lognormal(-10,3), random sign, 25% zeros", "R": 4,
+           "n_samples": 1}
+    return rows, 100.0 * sum(big) / len(big), roof, cfg
+
+
+def cpu_sweep_baseline():
+    """The oracle's LUQ on 2^25 fp32 elements."""
+    import numpy as np
+    from threadpoolctl import threadpool_info
+    from oracle import luq as oluq
+    import synth
+    n = 1 << 25
+    g = synth.grad_1d(n, "f32", 0.25, seed=4)
+    t0 = time.perf_counter()
+    oluq.luq_quantize(g, R=4)
+    dt = time.perf_counter() - t0
+    alg = 2 * n * 4 + n / 2
+    return {"value": round(100.0 * alg / dt / HBM_PEAK, 6), "unit": "% of MI355X HBM roofline",
+            "cores": 1, "kind": "oracle", "GB/s": round(alg / dt / 1e9, 4),
+            "sample": f"LUQ of 2^25 fp32 elements ({dt:.2f}s, NumPy, one core)"}
 
 
 def capture(torch, fns):
@@ -286,6 +372,17 @@ def main():
         return
     import paper_2112_10769_amd as L
     dev = torch.device("cuda:0")
+    if args.workload == "luq_sweep":
+        sizes = tuple(int(k) for k in args.sweep_log2.split(",")) if args.sweep_log2 else None
+        rows, value, roof, cfg = run_sweep(L, torch, args.steps, sizes)
+        out = {"metric": METRIC, "value": round(value, 2), "unit": "% of roofline", "n_gpus": 1,
+               "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(roof["launch_us"] / 1e3, 4), "higher_is_better": True,
+               "scaling": "weak", "vs_baseline": None, "dtype": "f32/bf16 in, u4 codes out",
+               "data": "synthetic", "config": cfg, "roofline": roof, "sweep": rows}
+        if not args.no_cpu:
+            out["cpu_baseline"] = cpu_sweep_baseline()
+        print(json.dumps(out), flush=True)
+        return
     if args.workload == "resnet":
         stages, cfg, d = build_resnet(L, torch, dev)
     elif args.workload == "small":

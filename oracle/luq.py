@@ -46,7 +46,7 @@ from fractions import Fraction
 
 import numpy as np
 
-from .philox import luq_uniforms
+from .philox import luq_uniforms, luq_uniforms_at
 
 TWO16 = 65536
 
@@ -152,6 +152,17 @@ def luq_nibbles_range(xf, start, alpha, R, seed, counter, sample):
     a = np.abs(xf.astype(np.float64))
     j = luq_uniforms(xf.size, seed, counter, sample, start=start)
     e = luq_fields(a, alpha, R, j)
+    return e | np.where((e != 0) & np.signbit(xf), 8, 0).astype(np.uint8)
+
+
+def luq_nibbles_at(xf, idx, alpha, R, seed, counter, sample):
+    """Unpacked codes of the elements at flat indices idx of a tensor whose
+    alpha is already known (xf: their float32 values, in the order of idx)."""
+    xf = np.asarray(xf, dtype=np.float32).ravel()
+    if not (float(alpha) > 0):
+        return np.zeros(xf.size, dtype=np.uint8)
+    a = np.abs(xf.astype(np.float64))
+    e = luq_fields(a, alpha, R, luq_uniforms_at(idx, seed, counter, sample))
     return e | np.where((e != 0) & np.signbit(xf), 8, 0).astype(np.uint8)
 
 

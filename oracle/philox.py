@@ -97,3 +97,24 @@ def luq_uniforms(n, seed, counter, sample, start=0):
     half = idx & np.uint64(1)
     yw = y[b.astype(np.int64), word.astype(np.int64)].astype(np.uint32)
     return (yw >> (np.uint32(16) * half.astype(np.uint32))) & np.uint32(0xFFFF)
+
+
+def luq_uniforms_at(idx, seed, counter, sample):
+    """16-bit uniforms j_i for arbitrary flat element indices idx (uint32 array).
+
+    The same mapping as ``luq_uniforms``: element i reads half (i & 1) of word
+    ((i >> 1) & 3) of the Philox block for counter (i >> 3, sample, counter)."""
+    idx = np.asarray(idx, dtype=np.uint64).ravel()
+    if idx.size == 0:
+        return np.zeros(0, dtype=np.uint32)
+    blks, inv = np.unique(idx >> np.uint64(3), return_inverse=True)
+    ctr = np.empty((blks.size, 4), dtype=np.uint32)
+    ctr[:, 0] = (blks & np.uint64(MASK32)).astype(np.uint32)
+    ctr[:, 1] = (blks >> np.uint64(32)).astype(np.uint32)
+    ctr[:, 2] = np.uint32(sample & MASK32)
+    ctr[:, 3] = np.uint32(counter & MASK32)
+    y = philox4x32_10(ctr, (seed & MASK32, (seed >> 32) & MASK32))
+    word = ((idx >> np.uint64(1)) & np.uint64(3)).astype(np.int64)
+    half = (idx & np.uint64(1)).astype(np.uint32)
+    yw = y[inv.ravel(), word].astype(np.uint32)
+    return (yw >> (np.uint32(16) * half)) & np.uint32(0xFFFF)

@@ -43,40 +43,47 @@ __device__ __forceinline__ uint32_t max_key(uint32_t b) {
 template <bool BF16, int MODE>
 __global__ __launch_bounds__(kThreads) void max_partial_kernel(const void* __restrict__ x, int64_t n,
                                                               uint32_t* __restrict__ partial) {
+  // groups of 8 elements per trip: eight 16-byte loads in flight per thread
+  constexpr int G = BF16 ? 8 : 4;
   __shared__ uint32_t scratch[kThreads / kWave];
   const int64_t ngroups = n >> 3;
   const int64_t stride = (int64_t)gridDim.x * kThreads;
-  uint32_t m0 = 0, m1 = 0;
+  uint32_t m[G];
+#pragma unroll
+  for (int i = 0; i < G; ++i) m[i] = 0;
   int64_t g = (int64_t)blockIdx.x * kThreads + threadIdx.x;
-  // two groups per trip keep four 16-byte loads in flight for float32
-  for (; g + stride < ngroups; g += 2 * stride) {
-    const U8 a = load8<BF16>(x, g * 8);
-    const U8 b = load8<BF16>(x, (g + stride) * 8);
+  for (; g + (G - 1) * stride < ngroups; g += G * stride) {
+    U8 v[G];
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      m0 = max(m0, max_key<MODE>(a.v[i]));
-      m1 = max(m1, max_key<MODE>(b.v[i]));
-    }
+    for (int i = 0; i < G; ++i) v[i] = load8<BF16>(x, (g + i * stride) * 8);
+#pragma unroll
+    for (int i = 0; i < G; ++i)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) m[i] = max(m[i], max_key<MODE>(v[i].v[e]));
   }
-  if (g < ngroups) {
+  for (; g < ngroups; g += stride) {
     const U8 a = load8<BF16>(x, g * 8);
 #pragma unroll
-    for (int i = 0; i < 8; ++i) m0 = max(m0, max_key<MODE>(a.v[i]));
+    for (int e = 0; e < 8; ++e) m[0] = max(m[0], max_key<MODE>(a.v[e]));
   }
   if (blockIdx.x == 0 && threadIdx.x == 0 && (n & 7)) {
     const U8 a = load8_tail<BF16>(x, ngroups * 8, n);  // missing elements read +0 (key 0)
 #pragma unroll
-    for (int i = 0; i < 8; ++i) m0 = max(m0, max_key<MODE>(a.v[i]));
+    for (int e = 0; e < 8; ++e) m[0] = max(m[0], max_key<MODE>(a.v[e]));
   }
-  const uint32_t m = block_max_u32(max(m0, m1), scratch);
-  if (threadIdx.x == 0) partial[blockIdx.x] = m;
+#pragma unroll
+  for (int i = 1; i < G; ++i) m[0] = max(m[0], m[i]);
+  const uint32_t r = block_max_u32(m[0], scratch);
+  if (threadIdx.x == 0) partial[blockIdx.x] = r;
 }
 
 // ---------------------------- transposing tiles ----------------------------
 //
 // When the transposed code layout is requested, work goes by tiles of
-// TG column groups (8 columns each) by TR = 8192 / TG rows; TG is 32, or the
-// next power of two above the number of column groups for narrow matrices.
+// TW = 2^lt code words: TG = 2^lg column groups (8 columns each) by
+// TR = TW / TG rows.  TG is 32, or the next power of two above the number of
+// column groups for narrow matrices; TW is 8192, or smaller (down to 1024)
+// when that leaves too few tiles to fill the chip.
 //   Phase A: consecutive lanes take consecutive column groups of a row, so
 //            the loads and the row-major code stores of a row are contiguous;
 //            every 8-element code word also goes to LDS at [group][row].
@@ -89,14 +96,14 @@ constexpr int kTilePad = 4;  // LDS words between column groups (keeps 16-byte a
 
 template <int NS, typename Enc>
 __device__ __forceinline__ void encode_tiles(const Enc& enc, int64_t rows, int64_t cols, int lg,
-                                             uint8_t* codes, uint8_t* codes_t, int64_t plane,
-                                             uint32_t* lds) {
-  const int tg = 1 << lg, tr = kTileWords >> lg, pitch = tr + kTilePad;
+                                             int lt, uint8_t* codes, uint8_t* codes_t,
+                                             int64_t plane, uint32_t* lds) {
+  const int tw = 1 << lt, tg = 1 << lg, tr = tw >> lg, pitch = tr + kTilePad;
   const int64_t cgs = cols >> 3;
   const int64_t ntr = (rows + tr - 1) / tr, ntc = (cgs + tg - 1) / tg;
   for (int64_t t = blockIdx.x; t < ntr * ntc; t += gridDim.x) {
     const int64_t r0 = (t / ntc) * tr, g0 = (t % ntc) * tg;
-    for (int q = threadIdx.x; q < kTileWords; q += kThreads) {
+    for (int q = threadIdx.x; q < tw; q += kThreads) {
       const int g = q & (tg - 1), r = q >> lg;
       const int64_t row = r0 + r, cg = g0 + g;
       uint32_t w[NS];
@@ -116,7 +123,7 @@ __device__ __forceinline__ void encode_tiles(const Enc& enc, int64_t rows, int64
     }
     __syncthreads();
     const int rbs = tr >> 3;  // 8-row blocks per tile
-    for (int q = threadIdx.x; q < kTileWords / 8; q += kThreads) {
+    for (int q = threadIdx.x; q < (tw >> 3); q += kThreads) {
       const int rb = q & (rbs - 1), g = q / rbs;
       const int64_t row0 = r0 + rb * 8, cg = g0 + g;
       if (row0 >= rows || cg >= cgs) continue;
@@ -175,28 +182,44 @@ __device__ __forceinline__ LuqParams luq_params(uint32_t mbits, int R, float* al
   return p;
 }
 
-// One element's 4-bit LUQ code from its float32 bits and 16-bit uniform.
+// One element's 3-bit LUQ exponent field from its float32 bits and 16-bit
+// uniform.
 //
 // On scaled magnitudes (both normal once |x| >= alpha), the difference of the
 // float bit patterns D = bits(|x|) - bits(alpha) has D >> 23 equal to
 // floor(log2(|x| / alpha)): the exponent difference, less one when the
 // mantissa of |x| is below that of alpha (the borrow).  So n = D >> 23 is the
-// bin index, n < 0 is the underflow bin [0, alpha) and n >= R the top level.
-// The bin width is alpha * 2^max(n, 0), built by adding max(n,0) to the
-// exponent field; the lower level is that width, or 0 in the underflow bin.
-// The field is clamp(n, -1, R) + 1 + up, capped at R + 1 (where `up` is
-// irrelevant).
+// bin index, n < 0 is the underflow bin [0, alpha) and n = R the top level.
+// The bin width is w = alpha * 2^max(n, 0), built (times 2^-16) by adding
+// max(n, 0) to the exponent field of alpha * 2^-16; the lower level is w, or
+// 0 in the underflow bin, so lo - |x| = fma(w * 2^-16, 2^16 or 0, -|x|), which
+// is exact.  The field is max(n, -1) + 1 + up.  Unscaled, |x| <= max =
+// alpha * 2^R exactly, so n <= R and at n = R the offset d is 0 and `up` is
+// false: the field never exceeds R + 1.  Scaled, alpha may have been rounded
+// (subnormal alpha), so the field is capped at R + 1.
 template <bool SCALED>
 __device__ __forceinline__ uint32_t luq_field(uint32_t b, uint32_t j, const LuqParams& p) {
-  const float mag = __uint_as_float(b & 0x7FFFFFFFu);
+  const float mag = fabsf(__uint_as_float(b));
   const float as = SCALED ? mag * p.S : mag;
-  const int32_t D = (int32_t)__float_as_uint(as) - (int32_t)p.a_bits;
-  const int32_t n = D >> 23;
-  const uint32_t wb = p.a_bits + ((uint32_t)max(n, 0) << 23);
-  const float lo = __uint_as_float(n < 0 ? 0u : wb);
-  const float w16 = __uint_as_float(wb - (16u << 23));  // exponent of alpha is >= 78
-  const bool up = fmaf((float)j, w16, lo - as) < 0.0f;   // lo - as = -d, exact
-  return (uint32_t)min(max(n, -1) + 1 + (int32_t)up, (int32_t)p.top_field);
+  const int32_t n = ((int32_t)__float_as_uint(as) - (int32_t)p.a_bits) >> 23;
+  const bool su = n < 0;
+  const float w16 = __uint_as_float(p.a16_bits + ((uint32_t)max(n, 0) << 23));
+  const float c = fmaf(w16, su ? 0.0f : 0x1p16f, -as);  // lo - |x|, exact
+  const bool up = fmaf((float)j, w16, c) < 0.0f;
+  const int32_t f = max(n, -1) + 1 + (int32_t)up;
+  return (uint32_t)(SCALED ? min(f, (int32_t)p.top_field) : f);
+}
+
+// Sign bits of 8 elements at the sign position of their nibbles (bit 4e+3):
+// the top bytes of the odd elements are gathered as they are (bit 7 of byte k
+// is element 2k+1's sign), those of the even elements are gathered and
+// rotated right by 4 bits.  Other bits are garbage and masked by the caller.
+__device__ __forceinline__ uint32_t gather_signs(const U8& v) {
+  const uint32_t odd = __builtin_amdgcn_perm(v.v[3], v.v[1], 0x0C0C0703u) |
+                       __builtin_amdgcn_perm(v.v[7], v.v[5], 0x07030C0Cu);
+  const uint32_t even = __builtin_amdgcn_perm(v.v[2], v.v[0], 0x0C0C0703u) |
+                        __builtin_amdgcn_perm(v.v[6], v.v[4], 0x07030C0Cu);
+  return (odd & 0x80808080u) | (__builtin_amdgcn_alignbit(even, even, 4) & 0x08080808u);
 }
 
 // Codes of 8 consecutive elements (bits in v) for Philox block `blk`: the
@@ -208,15 +231,14 @@ __device__ __forceinline__ uint32_t luq_word(const U8& v, uint64_t blk, uint32_t
                                              const LuqParams& p) {
   const U4 y = philox4x32_10(U4{(uint32_t)blk, (uint32_t)(blk >> 32), sample, counter}, k0, k1);
   const uint32_t w[4] = {y.x, y.y, y.z, y.w};
-  uint32_t fields = 0, signs = 0;
+  uint32_t fields = 0;
 #pragma unroll
   for (int e = 0; e < 8; ++e) {
     const uint32_t j = (e & 1) ? (w[e >> 1] >> 16) : (w[e >> 1] & 0xFFFFu);
     fields |= luq_field<SCALED>(v.v[e], j, p) << (4 * e);
-    signs |= (v.v[e] >> 31) << (4 * e + 3);
   }
   const uint32_t nz = (fields | (fields >> 1) | (fields >> 2)) & 0x11111111u;
-  return fields | (signs & (nz << 3));
+  return fields | (gather_signs(v) & (nz << 3));
 }
 
 struct LuqArgs {
@@ -293,13 +315,13 @@ struct LuqEnc {
 };
 
 template <bool BF16, int NS>
-__global__ __launch_bounds__(kThreads) void luq_encode_tile_kernel(LuqArgs a, int lg) {
+__global__ __launch_bounds__(kThreads) void luq_encode_tile_kernel(LuqArgs a, int lg, int lt) {
   __shared__ __attribute__((aligned(16))) uint32_t lds[NS * (kTileWords + 32 * kTilePad)];
   const LuqParams p = luq_block_params(a);
   if (p.S != 1.0f)
-    encode_tiles<NS>(LuqEnc<BF16, true>{&a, &p}, a.rows, a.cols, lg, a.codes, a.codes_t, a.plane, lds);
+    encode_tiles<NS>(LuqEnc<BF16, true>{&a, &p}, a.rows, a.cols, lg, lt, a.codes, a.codes_t, a.plane, lds);
   else
-    encode_tiles<NS>(LuqEnc<BF16, false>{&a, &p}, a.rows, a.cols, lg, a.codes, a.codes_t, a.plane, lds);
+    encode_tiles<NS>(LuqEnc<BF16, false>{&a, &p}, a.rows, a.cols, lg, lt, a.codes, a.codes_t, a.plane, lds);
 }
 
 __global__ void write_two_floats_kernel(float* a, float va, float* b, float vb) {
@@ -399,10 +421,10 @@ struct Int4Enc {
 };
 
 template <bool BF16>
-__global__ __launch_bounds__(kThreads) void int4_encode_tile_kernel(Int4Args a, int lg) {
+__global__ __launch_bounds__(kThreads) void int4_encode_tile_kernel(Int4Args a, int lg, int lt) {
   __shared__ __attribute__((aligned(16))) uint32_t lds[kTileWords + 32 * kTilePad];
   const Int4Params p = int4_block_params(a);
-  encode_tiles<1>(Int4Enc<BF16>{&a, &p}, a.rows, a.cols, lg, a.codes, a.codes_t, 0, lds);
+  encode_tiles<1>(Int4Enc<BF16>{&a, &p}, a.rows, a.cols, lg, lt, a.codes, a.codes_t, 0, lds);
 }
 
 // ------------------------------- launchers ---------------------------------
@@ -425,21 +447,31 @@ static int encode_blocks_flat(int64_t n) {
   return (int)b;
 }
 
-// log2 of the column groups per transposing tile
-static int tile_lg(int64_t cols) {
-  const int64_t cgs = cols >> 3;
-  int lg = 0;
-  while (lg < 5 && (1LL << lg) < cgs) ++lg;
-  return lg;
+// Transposing tile shape: log2 of the column groups per tile (lg) and of the
+// code words per tile (lt).  Tiles shrink from 8192 words until there are at
+// least four per compute unit or a tile is 1024 words (or 8 rows) small.
+struct TileShape {
+  int lg, lt, blocks;
+};
+
+static int64_t tile_count(int64_t rows, int64_t cols, int lg, int lt) {
+  const int64_t tr = 1LL << (lt - lg), tg = 1LL << lg;
+  return ((rows + tr - 1) / tr) * (((cols >> 3) + tg - 1) / tg);
 }
 
-static int encode_blocks_tile(int64_t rows, int64_t cols) {
-  const int lg = tile_lg(cols);
-  const int64_t tr = kTileWords >> lg, tg = 1LL << lg;
-  const int64_t tiles = ((rows + tr - 1) / tr) * (((cols >> 3) + tg - 1) / tg);
-  int64_t b = tiles < 1 ? 1 : tiles;
+static TileShape tile_shape(int64_t rows, int64_t cols) {
+  constexpr int64_t kWantTiles = 1024;
+  const int64_t cgs = cols >> 3;
+  TileShape t;
+  t.lg = 0;
+  while (t.lg < 5 && (1LL << t.lg) < cgs) ++t.lg;
+  t.lt = 13;
+  while (t.lt > 10 && t.lt - 1 - t.lg >= 3 && tile_count(rows, cols, t.lg, t.lt) < kWantTiles) --t.lt;
+  int64_t b = tile_count(rows, cols, t.lg, t.lt);
+  if (b < 1) b = 1;
   if (b > kMaxEncodeBlocks) b = kMaxEncodeBlocks;
-  return (int)b;
+  t.blocks = (int)b;
+  return t;
 }
 
 template <bool BF16>
@@ -447,11 +479,11 @@ static hipError_t luq_launch_t(const LuqArgs& a, int ns, int nmax, hipStream_t s
   hipLaunchKernelGGL((max_partial_kernel<BF16, 0>), dim3(nmax), dim3(kThreads), 0, st, a.g, a.n,
                      const_cast<uint32_t*>(a.partial));
   if (a.codes_t) {
-    const int nb = encode_blocks_tile(a.rows, a.cols);
+    const TileShape t = tile_shape(a.rows, a.cols);
     if (ns == 1)
-      hipLaunchKernelGGL((luq_encode_tile_kernel<BF16, 1>), dim3(nb), dim3(kThreads), 0, st, a, tile_lg(a.cols));
+      hipLaunchKernelGGL((luq_encode_tile_kernel<BF16, 1>), dim3(t.blocks), dim3(kThreads), 0, st, a, t.lg, t.lt);
     else
-      hipLaunchKernelGGL((luq_encode_tile_kernel<BF16, 2>), dim3(nb), dim3(kThreads), 0, st, a, tile_lg(a.cols));
+      hipLaunchKernelGGL((luq_encode_tile_kernel<BF16, 2>), dim3(t.blocks), dim3(kThreads), 0, st, a, t.lg, t.lt);
   } else {
     const int nb = encode_blocks_flat(a.n);
     if (ns == 1)
@@ -500,9 +532,11 @@ static hipError_t int4_launch_t(const Int4Args& a, hipStream_t st) {
       hipLaunchKernelGGL((max_partial_kernel<BF16, 1>), dim3(a.nparts), dim3(kThreads), 0, st, a.x,
                          a.n, const_cast<uint32_t*>(a.partial));
   }
-  if (a.codes_t)
-    hipLaunchKernelGGL((int4_encode_tile_kernel<BF16>), dim3(encode_blocks_tile(a.rows, a.cols)),
-                       dim3(kThreads), 0, st, a, tile_lg(a.cols));
+  if (a.codes_t) {
+    const TileShape t = tile_shape(a.rows, a.cols);
+    hipLaunchKernelGGL((int4_encode_tile_kernel<BF16>), dim3(t.blocks), dim3(kThreads), 0, st, a,
+                       t.lg, t.lt);
+  }
   else
     hipLaunchKernelGGL((int4_encode_flat_kernel<BF16>), dim3(encode_blocks_flat(a.n)),
                        dim3(kThreads), 0, st, a);

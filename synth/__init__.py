@@ -23,6 +23,9 @@ Workloads (shapes of the paper's ResNet-50 and Transformer layers):
              fraction 0..0.5, fp32 or bf16.
 """
 
+import os
+from concurrent.futures import ThreadPoolExecutor
+
 import numpy as np
 
 CHUNK = 1 << 24
@@ -32,32 +35,47 @@ def _rng(seed):
     return np.random.default_rng(seed)
 
 
+def _chunked(n, seed, fill):
+    """float32 array of n entries drawn chunk by chunk; chunk c uses its own
+    generator seeded with seed + [c], so the result does not depend on how
+    many threads fill the chunks."""
+    out = np.empty(n, dtype=np.float32)
+    base = [int(s) for s in np.atleast_1d(seed)]
+
+    def one(c0):
+        c1 = min(n, c0 + CHUNK)
+        out[c0:c1] = fill(_rng(base + [c0 // CHUNK]), c1 - c0)
+
+    starts = range(0, n, CHUNK)
+    if n > CHUNK:
+        with ThreadPoolExecutor(max_workers=min(16, os.cpu_count() or 1)) as ex:
+            list(ex.map(one, starts))
+    else:
+        for c0 in starts:
+            one(c0)
+    return out
+
+
 def lognormal_grad(shape, mu, sigma, zero_frac, seed):
     """float32 tensor with ln|g| ~ N(mu, sigma^2), random sign, exact zeros."""
-    n = int(np.prod(shape))
-    out = np.empty(n, dtype=np.float32)
-    for c0 in range(0, n, CHUNK):
-        c1 = min(n, c0 + CHUNK)
-        r = _rng([int(s) for s in np.atleast_1d(seed)] + [c0 // CHUNK])
-        z = r.standard_normal(c1 - c0, dtype=np.float32)
+    def fill(r, m):
+        z = r.standard_normal(m, dtype=np.float32)
         mag = np.exp(np.float32(mu) + np.float32(sigma) * z)
-        u = r.random(c1 - c0, dtype=np.float32)
-        sgn = np.where(r.random(c1 - c0, dtype=np.float32) < 0.5, -1.0, 1.0).astype(np.float32)
+        u = r.random(m, dtype=np.float32)
+        sgn = np.where(r.random(m, dtype=np.float32) < 0.5, -1.0, 1.0).astype(np.float32)
         v = mag * sgn
         if zero_frac > 0:
             v = np.where(u < zero_frac, np.float32(0.0), v)
-        out[c0:c1] = v
-    return out.reshape(shape)
+        return v
+
+    return _chunked(int(np.prod(shape)), seed, fill).reshape(shape)
 
 
 def normal(shape, std, seed):
-    n = int(np.prod(shape))
-    out = np.empty(n, dtype=np.float32)
-    for c0 in range(0, n, CHUNK):
-        c1 = min(n, c0 + CHUNK)
-        r = _rng([int(s) for s in np.atleast_1d(seed)] + [c0 // CHUNK])
-        out[c0:c1] = r.standard_normal(c1 - c0, dtype=np.float32) * np.float32(std)
-    return out.reshape(shape)
+    def fill(r, m):
+        return r.standard_normal(m, dtype=np.float32) * np.float32(std)
+
+    return _chunked(int(np.prod(shape)), seed, fill).reshape(shape)
 
 
 def half_normal(shape, seed):

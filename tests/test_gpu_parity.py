@@ -73,7 +73,9 @@ def test_luq_flat_ragged(L, n, dtype):
     _check_luq(L, x, 1, n, seed=0xDEADBEEFCAFE0000 + n, counter=n, what="flat")
 
 
-@pytest.mark.parametrize("shape", [(8, 8), (264, 200), (136, 1032), (1024, 392), (40, 4096)])
+# includes narrow matrices whose transposing tiles shrink below 8192 words
+@pytest.mark.parametrize("shape", [(8, 8), (264, 200), (136, 1032), (1024, 392), (40, 4096), (4104, 64),
+                                   (2056, 16), (1000, 8)])
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 def test_luq_tile_both_layouts(L, shape, dtype):
     r, c = shape
@@ -159,7 +161,7 @@ def _check_int4(L, x, rows, cols, signed, clip=0.0, want_t=False, what=""):
 
 @pytest.mark.parametrize("signed", [True, False])
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
-@pytest.mark.parametrize("shape", [(1, 1), (1, 13), (1, 100001), (264, 200), (136, 1032)])
+@pytest.mark.parametrize("shape", [(1, 1), (1, 13), (1, 100001), (264, 200), (136, 1032), (4104, 64)])
 def test_int4_parity(L, signed, dtype, shape):
     r, c = shape
     x = synth.normal((r * c,), 1.3, [300, r, c])

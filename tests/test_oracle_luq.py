@@ -13,7 +13,8 @@ import pytest
 
 import synth
 from oracle import luq
-from oracle.luq import luq_quantize, luq_decode, luq_decode_int, luq_fields, luq_field_scalar, unpack_nibbles
+from oracle.luq import (luq_quantize, luq_decode, luq_decode_int, luq_fields, luq_field_scalar, unpack_nibbles,
+                        luq_nibbles_at)
 from oracle.int4 import int4_quantize, int4_decode
 from oracle.gemm import gemm_wgrad_ref
 
@@ -228,3 +229,15 @@ def test_unbiased_weight_gradient():
     _, alpha, _ = luq_quantize(g, R=4)
     bias_bound = (np.abs(aq).sum(0)[None, :] * float(alpha) * 2 ** 3 * 2.0 ** -16)
     assert np.all(np.abs(mean - exact) <= 5 * se + bias_bound + 1e-18)
+
+
+def test_index_addressed_codes_equal_whole_tensor_codes():
+    """Codes computed one by one from flat indices equal those of the whole
+    tensor (unsorted, repeated and tail indices; both SMP samples)."""
+    x = synth.lognormal_grad((5001,), -10.0, 2.0, 0.3, [77, 1])
+    codes, alpha, _ = luq_quantize(x, R=4, seed=99, counter=4, n_samples=2)
+    idx = np.array([5000, 0, 7, 8, 4999, 7, 1234, 2500, 3], dtype=np.int64)
+    for s in range(2):
+        whole = unpack_nibbles(codes[s], x.size)
+        got = luq_nibbles_at(x[idx], idx, alpha, 4, 99, 4, s)
+        assert np.array_equal(got, whole[idx])

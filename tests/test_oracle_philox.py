@@ -12,7 +12,7 @@ import subprocess
 import numpy as np
 import pytest
 
-from oracle.philox import philox4x32_10, philox4x32_10_scalar, luq_uniforms
+from oracle.philox import philox4x32_10, philox4x32_10_scalar, luq_uniforms, luq_uniforms_at
 
 GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
 
@@ -83,6 +83,19 @@ def test_uniform_layout_eight_elements_per_block():
         assert int(j[i]) == (w >> (16 * (i & 1))) & 0xFFFF
     # an offset start sees the same stream
     assert np.array_equal(luq_uniforms(17, seed, c, s, start=13), j[13:30])
+
+
+def test_index_addressed_uniforms_match_scalar_and_ranges():
+    """Arbitrary indices (unsorted, repeated, above 2^32) against the scalar
+    formulation, and against the contiguous-range generator."""
+    seed, c, s = 0x0123456789ABCDEF, 3, 1
+    idx = np.array([5, 0, 1 << 33, (1 << 33) + 7, 5, 64, 63, 12345678901], dtype=np.uint64)
+    j = luq_uniforms_at(idx, seed, c, s)
+    for i, v in zip(idx.tolist(), j.tolist()):
+        y = philox4x32_10_scalar([(i >> 3) & 0xFFFFFFFF, i >> 35, s, c], (seed & 0xFFFFFFFF, seed >> 32))
+        assert v == (y[(i >> 1) & 3] >> (16 * (i & 1))) & 0xFFFF
+    r = luq_uniforms(1000, seed, c, s, start=777)
+    assert np.array_equal(luq_uniforms_at(np.arange(777, 1777), seed, c, s), r)
 
 
 def test_samples_and_counters_are_distinct_streams():
