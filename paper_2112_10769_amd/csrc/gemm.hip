@@ -116,9 +116,10 @@ __device__ __forceinline__ void tile_coords(int bid, int ntm, int ntn, int& tm, 
 //   - stage t is multiplied out of LDS buffer t%2,
 //   - stage t+1 (loaded one iteration earlier) is expanded into LDS buffer
 //     (t+1)%2,
-// all in one block of straight-line code, so the expansion VALU work and the
-// global loads overlap the MFMAs.  The MFMA takes the B fragment as its first
-// operand, so each lane ends up with 4 consecutive columns of one C row.
+// all in one block of straight-line code, with the expansion and loads cut
+// into one piece per 32-deep k-step and placed after that k-step's MFMAs, so
+// the VALU work issues between MFMAs.  The MFMA takes the B fragment as its
+// first operand, so each lane ends up with 4 consecutive columns of one C row.
 template <int BM, int BN, int BK, int NS, bool BSIGNED>
 __global__ __launch_bounds__(kGemmThreads, 1) void gemm_luq_int4_kernel(GemmArgs a) {
   static_assert(BM % 64 == 0 && BN % 64 == 0, "wave tiles are multiples of 32");
@@ -172,25 +173,31 @@ __global__ __launch_bounds__(kGemmThreads, 1) void gemm_luq_int4_kernel(GemmArgs
     v4u a[NS][ACH];
     v4u b[BCH];
   };
-  auto load = [&](Regs& r, int t) {
+  // Work of one stage is split into KS pieces, one per 32-deep k-step: piece
+  // kk covers the A and B chunks i with i % KS == kk.
+  constexpr int KS = kBK / 32;
+  auto load_piece = [&](Regs& r, int t, int kk) {
     const int64_t k0 = kbeg + (int64_t)t * kBK;
 #pragma unroll
     for (int i = 0; i < ACH; ++i) {
+      if (i % KS != kk) continue;
       const int off = (k0 + kca[i]) < kend ? offa[i] + t * (kBK / 2) : kOutOfRange;
 #pragma unroll
       for (int s = 0; s < NS; ++s) r.a[s][i] = __builtin_amdgcn_raw_buffer_load_b128(rsa[s], off, 0, 0);
     }
 #pragma unroll
     for (int i = 0; i < BCH; ++i) {
+      if (i % KS != kk) continue;
       const int off = (k0 + kcb[i]) < kend ? offb[i] + t * (kBK / 2) : kOutOfRange;
       r.b[i] = __builtin_amdgcn_raw_buffer_load_b128(rsb, off, 0, 0);
     }
   };
-  auto expand_store = [&](const Regs& r, int buf) {
+  auto expand_piece = [&](const Regs& r, int buf, int kk) {
     uint8_t* As = lds + buf * STAGE;
     uint8_t* Bs = As + BM * kPitch;
 #pragma unroll
     for (int i = 0; i < ACH; ++i) {
+      if (i % KS != kk) continue;
       const int c = tid + i * kGemmThreads, row = c / KC, kc = c % KC;
       uint32_t w[8];
       const uint32_t x0[4] = {r.a[0][i][0], r.a[0][i][1], r.a[0][i][2], r.a[0][i][3]};
@@ -212,6 +219,7 @@ __global__ __launch_bounds__(kGemmThreads, 1) void gemm_luq_int4_kernel(GemmArgs
     }
 #pragma unroll
     for (int i = 0; i < BCH; ++i) {
+      if (i % KS != kk) continue;
       const int c = tid + i * kGemmThreads, row = c / KC, kc = c % KC;
       uint32_t w[8];
       const uint32_t x0[4] = {r.b[i][0], r.b[i][1], r.b[i][2], r.b[i][3]};
@@ -231,42 +239,55 @@ __global__ __launch_bounds__(kGemmThreads, 1) void gemm_luq_int4_kernel(GemmArgs
 
   // 32x32x32 MFMA operands: lane l supplies row l%32 and 16 consecutive k
   // (positions 16*(l/32) .. +15 of the 32-k step) of its fragment.
-  auto compute = [&](int buf) {
+  struct Frags {
+    v4i a[TM], b[TN];
+  };
+  auto read_frags = [&](int buf, int kk, Frags& f) {
     const uint8_t* As = lds + buf * STAGE;
-    const uint8_t* as = As + (wm * (BM / 2) + (lane & 31)) * kPitch + (lane >> 5) * 16;
-    const uint8_t* bs = As + BM * kPitch + (wn * (BN / 2) + (lane & 31)) * kPitch + (lane >> 5) * 16;
+    const uint8_t* as = As + (wm * (BM / 2) + (lane & 31)) * kPitch + (lane >> 5) * 16 + kk * 32;
+    const uint8_t* bs = As + BM * kPitch + (wn * (BN / 2) + (lane & 31)) * kPitch + (lane >> 5) * 16 + kk * 32;
 #pragma unroll
-    for (int kk = 0; kk < kBK; kk += 32) {
-      v4i fa[TM], fb[TN];
+    for (int i = 0; i < TM; ++i) f.a[i] = *reinterpret_cast<const v4i*>(as + i * 32 * kPitch);
 #pragma unroll
-      for (int i = 0; i < TM; ++i) fa[i] = *reinterpret_cast<const v4i*>(as + i * 32 * kPitch + kk);
+    for (int j = 0; j < TN; ++j) f.b[j] = *reinterpret_cast<const v4i*>(bs + j * 32 * kPitch);
+  };
+  auto mfmas = [&](const Frags& f) {
 #pragma unroll
-      for (int j = 0; j < TN; ++j) fb[j] = *reinterpret_cast<const v4i*>(bs + j * 32 * kPitch + kk);
+    for (int i = 0; i < TM; ++i)
 #pragma unroll
-      for (int i = 0; i < TM; ++i)
-#pragma unroll
-        for (int j = 0; j < TN; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_i32_32x32x32_i8(fb[j], fa[i], acc[i][j], 0, 0, 0);
-    }
+      for (int j = 0; j < TN; ++j)
+        acc[i][j] = __builtin_amdgcn_mfma_i32_32x32x32_i8(f.b[j], f.a[i], acc[i][j], 0, 0, 0);
   };
 
-  // One pipeline step: multiply stage `cb` out of LDS while expanding the
-  // registers `r` (the next stage) into the other buffer, then reload `rl`
-  // with stage `tload`.  The MFMAs, the expansion and the loads sit in one
-  // straight-line block between barriers.
+  // One pipeline step, straight-line code between barriers: for each k-step
+  // of stage `cb` (in LDS), the fragments of the next k-step are read ahead,
+  // the MFMAs of this k-step issue, and one piece of the next stage (the
+  // registers `r`) is expanded into the other buffer, after which that
+  // piece's registers are reloaded from stage `tload` into `rl`.  Source
+  // order interleaves the expansion work with the MFMAs.
   auto step = [&](int cb, const Regs& r, Regs& rl, int tload) {
-    compute(cb);
-    expand_store(r, cb ^ 1);
-    load(rl, tload);
+    Frags f[2];
+    read_frags(cb, 0, f[0]);
+#pragma unroll
+    for (int kk = 0; kk < KS; ++kk) {
+      if (kk + 1 < KS) read_frags(cb, kk + 1, f[(kk + 1) & 1]);
+      mfmas(f[kk & 1]);
+      expand_piece(r, cb ^ 1, kk);
+      load_piece(rl, tload, kk);
+    }
     __syncthreads();
   };
 
   Regs r0, r1;
-  load(r0, 0);
-  load(r1, 1);
-  expand_store(r0, 0);
+#pragma unroll
+  for (int kk = 0; kk < KS; ++kk) load_piece(r0, 0, kk);
+#pragma unroll
+  for (int kk = 0; kk < KS; ++kk) load_piece(r1, 1, kk);
+#pragma unroll
+  for (int kk = 0; kk < KS; ++kk) expand_piece(r0, 0, kk);
   __syncthreads();
-  load(r0, 2);
+#pragma unroll
+  for (int kk = 0; kk < KS; ++kk) load_piece(r0, 2, kk);
   // Stages beyond nkt load as zeros (masked), so an odd stage count ends on
   // a zero-filled buffer that adds nothing.
   for (int t = 0; t < nkt; t += 2) {
@@ -274,48 +295,61 @@ __global__ __launch_bounds__(kGemmThreads, 1) void gemm_luq_int4_kernel(GemmArgs
     step(1, r0, r0, t + 4);   // multiply t+1, expand t+2 (r0), then reuse r0 for t+4
   }
 
-  // C[m][n] from the swapped MFMA: in tile (i, j), lane l holds row l%32 and,
-  // in registers 4q..4q+3, the 4 consecutive columns 8q + 4*(l/32) + 0..3.
-  const int64_t row0 = m0 + wm * (BM / 2) + (lane & 31);
-  const int64_t col0 = n0 + wn * (BN / 2) + 4 * (lane >> 5);
-  const float sc = a.partial ? 0.0f
-                             : __fmul_rn(__fmul_rn(*a.alpha, 1.0f / NS), *a.bscale) * (BSIGNED ? 0x1p-4f : 0x1p-3f);
+  // Epilogue through LDS.  In MFMA tile (i, j), lane l holds row l%32 and, in
+  // registers 4q..4q+3, the 4 consecutive columns 8q + 4*(l/32) + 0..3 (the
+  // swapped operands).  Each wave stages 32 rows of its block at a time as a
+  // row-major slab in its own part of the (now idle) stage buffers, then
+  // stores whole row segments: WN/4 consecutive lanes cover one row of the
+  // wave's block, so a store instruction writes 64*16/WN-row runs of
+  // contiguous 16-byte chunks.  C gets the scaled fp32 values, the split-K
+  // workspace the raw int32 sums.
+  constexpr int WM = BM / 2, WN = BN / 2;
+  constexpr int EP = WN + 4;      // slab row pitch in 32-bit words
+  constexpr int LPR = WN / 4;     // lanes per row in the store phase
+  constexpr int RPI = 64 / LPR;   // rows per store instruction
+  static_assert(4 * 32 * EP * 4 <= 2 * STAGE, "epilogue slabs fit in the stage buffers");
+  static_assert(WM % 32 == 0 && 64 % LPR == 0, "slab shape");
+  uint32_t* E = reinterpret_cast<uint32_t*>(lds) + wave * 32 * EP;
+  const bool part = a.partial != nullptr;
+  const float sc = part ? 0.0f
+                        : __fmul_rn(__fmul_rn(*a.alpha, 1.0f / NS), *a.bscale) * (BSIGNED ? 0x1p-4f : 0x1p-3f);
+  uint32_t* out = part ? reinterpret_cast<uint32_t*>(a.partial + (int64_t)blockIdx.y * a.M * a.N)
+                       : reinterpret_cast<uint32_t*>(a.C);
+  const int64_t rbase = m0 + wm * WM, cbase = n0 + wn * WN;
+  const int srow = lane / LPR, scol = (lane % LPR) * 4;
+  __syncthreads();  // every wave is done with the stage buffers
 #pragma unroll
   for (int i = 0; i < TM; ++i) {
-    const int64_t row = row0 + i * 32;
-    if (row >= a.M) continue;
 #pragma unroll
     for (int j = 0; j < TN; ++j)
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
-        const int64_t col = col0 + j * 32 + 8 * q;
-        const v4i v = {acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]};
-        if (a.partial) {
-          int32_t* P = a.partial + (int64_t)blockIdx.y * a.M * a.N + row * a.N;
-          if (a.vec && col + 3 < a.N) {
-            *reinterpret_cast<v4i*>(P + col) = v;
-          } else {
+        v4u v;
 #pragma unroll
-            for (int r = 0; r < 4; ++r)
-              if (col + r < a.N) P[col + r] = v[r];
-          }
+        for (int r = 0; r < 4; ++r) {
+          const int32_t x = acc[i][j][4 * q + r];
+          v[r] = part ? (uint32_t)x : __float_as_uint(__fmul_rn((float)x, sc));
+        }
+        *reinterpret_cast<v4u*>(E + (lane & 31) * EP + j * 32 + 8 * q + 4 * (lane >> 5)) = v;
+      }
+    __syncthreads();
+#pragma unroll
+    for (int rr = 0; rr < 32; rr += RPI) {
+      const int64_t row = rbase + i * 32 + rr + srow;
+      const int64_t col = cbase + scol;
+      if (row < a.M) {
+        const v4u v = *reinterpret_cast<const v4u*>(E + (rr + srow) * EP + scol);
+        uint32_t* dst = out + row * a.N + col;
+        if (a.vec && col + 3 < a.N) {
+          *reinterpret_cast<v4u*>(dst) = v;
         } else {
-          float4 f;
-          f.x = __fmul_rn((float)v[0], sc);
-          f.y = __fmul_rn((float)v[1], sc);
-          f.z = __fmul_rn((float)v[2], sc);
-          f.w = __fmul_rn((float)v[3], sc);
-          float* Cr = a.C + row * a.N;
-          if (a.vec && col + 3 < a.N) {
-            *reinterpret_cast<float4*>(Cr + col) = f;
-          } else {
-            const float ff[4] = {f.x, f.y, f.z, f.w};
 #pragma unroll
-            for (int r = 0; r < 4; ++r)
-              if (col + r < a.N) Cr[col + r] = ff[r];
-          }
+          for (int r = 0; r < 4; ++r)
+            if (col + r < a.N) dst[r] = v[r];
         }
       }
+    }
+    __syncthreads();  // the slab is rewritten by the next i
   }
 }
 
@@ -352,7 +386,7 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(const int32_t* __res
 // ---- planning and launch ----------------------------------------------------------
 
 struct GemmPlan {
-  int bm, bn;
+  int bm, bn, bk;
   int64_t tiles_m, tiles_n;
   int splits;
   int64_t k_chunk;
@@ -375,6 +409,9 @@ static GemmPlan plan_gemm(int64_t M, int64_t N, int64_t K) {
     p.bm = 64;
     p.bn = 64;
   }
+  // a reduction of at most 64 fits one 64-deep stage: half the LDS, so more
+  // workgroups per CU overlap their loads with other tiles' output stores
+  p.bk = (K <= 64 && p.bm == 128) ? 64 : 128;
   p.tiles_m = (M + p.bm - 1) / p.bm;
   p.tiles_n = (N + p.bn - 1) / p.bn;
   const int64_t nt = p.tiles_m * p.tiles_n;
@@ -418,6 +455,8 @@ static hipError_t gemm_launch_t(const GemmArgs& a0, const GemmPlan& p, hipStream
   a.vec = (a.N % 4) == 0 && (((uintptr_t)(a.partial ? (void*)a.partial : (void*)a.C)) & 15) == 0;
   if (p.bm == 256)
     launch_tile<256, 256, 128, NS, BSIGNED>(a, grid, st);
+  else if (p.bm == 128 && p.bk == 64)
+    launch_tile<128, 128, 64, NS, BSIGNED>(a, grid, st);
   else if (p.bm == 128)
     launch_tile<128, 128, 128, NS, BSIGNED>(a, grid, st);
   else

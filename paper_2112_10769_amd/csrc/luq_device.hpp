@@ -50,22 +50,33 @@ struct U8 {
   uint32_t v[8];
 };
 
-template <bool BF16>
+typedef uint32_t v4u32 __attribute__((ext_vector_type(4)));
+
+// 16 bytes at p; NT marks the load non-temporal (streaming data read once).
+template <bool NT>
+__device__ __forceinline__ v4u32 load16(const void* p) {
+  if constexpr (NT) return __builtin_nontemporal_load(static_cast<const v4u32*>(p));
+  return *static_cast<const v4u32*>(p);
+}
+
+template <bool BF16, bool NT = false>
 __device__ __forceinline__ U8 load8(const void* base, int64_t elem) {
   U8 r;
   if constexpr (BF16) {
-    const uint4 q = *reinterpret_cast<const uint4*>(static_cast<const uint16_t*>(base) + elem);
-    const uint32_t w[4] = {q.x, q.y, q.z, q.w};
+    const v4u32 q = load16<NT>(static_cast<const uint16_t*>(base) + elem);
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      r.v[2 * i] = w[i] << 16;
-      r.v[2 * i + 1] = w[i] & 0xFFFF0000u;
+      r.v[2 * i] = q[i] << 16;
+      r.v[2 * i + 1] = q[i] & 0xFFFF0000u;
     }
   } else {
-    const uint4* p = reinterpret_cast<const uint4*>(static_cast<const float*>(base) + elem);
-    const uint4 a = p[0], b = p[1];
-    r.v[0] = a.x; r.v[1] = a.y; r.v[2] = a.z; r.v[3] = a.w;
-    r.v[4] = b.x; r.v[5] = b.y; r.v[6] = b.z; r.v[7] = b.w;
+    const float* p = static_cast<const float*>(base) + elem;
+    const v4u32 a = load16<NT>(p), b = load16<NT>(p + 4);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      r.v[i] = a[i];
+      r.v[4 + i] = b[i];
+    }
   }
   return r;
 }

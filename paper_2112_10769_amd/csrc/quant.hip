@@ -28,7 +28,7 @@
 namespace luq {
 
 constexpr int kThreads = 256;
-constexpr int kMaxPartials = 1024;
+constexpr int kMaxPartials = 2048;
 constexpr int kMaxEncodeBlocks = 4096;
 
 // Max-pass keys.  MODE 0: |x| (LUQ, signed INT4).  MODE 1: max(x, 0) with
@@ -40,7 +40,7 @@ __device__ __forceinline__ uint32_t max_key(uint32_t b) {
   return (a >= 0x7F800000u) ? a : ((b >> 31) ? 0u : b);
 }
 
-template <bool BF16, int MODE>
+template <bool BF16, int MODE, bool NT>
 __global__ __launch_bounds__(kThreads) void max_partial_kernel(const void* __restrict__ x, int64_t n,
                                                               uint32_t* __restrict__ partial) {
   // groups of 8 elements per trip: eight 16-byte loads in flight per thread
@@ -55,7 +55,7 @@ __global__ __launch_bounds__(kThreads) void max_partial_kernel(const void* __res
   for (; g + (G - 1) * stride < ngroups; g += G * stride) {
     U8 v[G];
 #pragma unroll
-    for (int i = 0; i < G; ++i) v[i] = load8<BF16>(x, (g + i * stride) * 8);
+    for (int i = 0; i < G; ++i) v[i] = load8<BF16, NT>(x, (g + i * stride) * 8);
 #pragma unroll
     for (int i = 0; i < G; ++i)
 #pragma unroll
@@ -103,23 +103,38 @@ __device__ __forceinline__ void encode_tiles(const Enc& enc, int64_t rows, int64
   const int64_t ntr = (rows + tr - 1) / tr, ntc = (cgs + tg - 1) / tg;
   for (int64_t t = blockIdx.x; t < ntr * ntc; t += gridDim.x) {
     const int64_t r0 = (t / ntc) * tr, g0 = (t % ntc) * tg;
-    for (int q = threadIdx.x; q < tw; q += kThreads) {
-      const int g = q & (tg - 1), r = q >> lg;
-      const int64_t row = r0 + r, cg = g0 + g;
-      uint32_t w[NS];
+    // two items per trip (tw is a multiple of 2 * kThreads): both loads are
+    // in flight before either is encoded
+    for (int q0 = threadIdx.x; q0 < tw; q0 += 2 * kThreads) {
+      int g[2], r[2];
+      bool ok[2];
+      int64_t e0[2];
+      U8 v[2];
 #pragma unroll
-      for (int s = 0; s < NS; ++s) w[s] = 0;
-      if (row < rows && cg < cgs) {
-        const int64_t e0 = row * cols + cg * 8;
-        const U8 v = enc.load(e0);
-#pragma unroll
-        for (int s = 0; s < NS; ++s) {
-          w[s] = enc.word(v, (uint64_t)(e0 >> 3), s);
-          if (codes) *reinterpret_cast<uint32_t*>(codes + s * plane + (e0 >> 1)) = w[s];
-        }
+      for (int u = 0; u < 2; ++u) {
+        const int q = q0 + u * kThreads;
+        g[u] = q & (tg - 1);
+        r[u] = q >> lg;
+        const int64_t row = r0 + r[u], cg = g0 + g[u];
+        ok[u] = row < rows && cg < cgs;
+        e0[u] = row * cols + cg * 8;
+        if (ok[u]) v[u] = enc.load(e0[u]);
       }
 #pragma unroll
-      for (int s = 0; s < NS; ++s) lds[(s * tg + g) * pitch + r] = w[s];
+      for (int u = 0; u < 2; ++u) {
+        uint32_t w[NS];
+#pragma unroll
+        for (int s = 0; s < NS; ++s) w[s] = 0;
+        if (ok[u]) {
+#pragma unroll
+          for (int s = 0; s < NS; ++s) {
+            w[s] = enc.word(v[u], (uint64_t)(e0[u] >> 3), s);
+            if (codes) *reinterpret_cast<uint32_t*>(codes + s * plane + (e0[u] >> 1)) = w[s];
+          }
+        }
+#pragma unroll
+        for (int s = 0; s < NS; ++s) lds[(s * tg + g[u]) * pitch + r[u]] = w[s];
+      }
     }
     __syncthreads();
     const int rbs = tr >> 3;  // 8-row blocks per tile
@@ -268,12 +283,25 @@ __device__ __forceinline__ LuqParams luq_block_params(const LuqArgs& a) {
 }
 
 // Flat row-major codes; groups of 8 elements along the flattened tensor.
-template <bool BF16, int NS, bool SCALED>
+template <bool BF16, bool NT, int NS, bool SCALED>
 __device__ __forceinline__ void luq_flat_body(const LuqArgs& a, const LuqParams& p) {
   const int64_t nfull = a.n >> 3;
-  for (int64_t g = (int64_t)blockIdx.x * kThreads + threadIdx.x; g < nfull;
-       g += (int64_t)gridDim.x * kThreads) {
-    const U8 v = load8<BF16>(a.g, g * 8);
+  const int64_t stride = (int64_t)gridDim.x * kThreads;
+  int64_t g = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+  // two groups per trip: both loads are in flight before either is encoded
+  for (; g + stride < nfull; g += 2 * stride) {
+    const U8 v0 = load8<BF16, NT>(a.g, g * 8);
+    const U8 v1 = load8<BF16, NT>(a.g, (g + stride) * 8);
+#pragma unroll
+    for (int s = 0; s < NS; ++s) {
+      *reinterpret_cast<uint32_t*>(a.codes + s * a.plane + g * 4) =
+          luq_word<SCALED>(v0, (uint64_t)g, s, a.counter, a.k0, a.k1, p);
+      *reinterpret_cast<uint32_t*>(a.codes + s * a.plane + (g + stride) * 4) =
+          luq_word<SCALED>(v1, (uint64_t)(g + stride), s, a.counter, a.k0, a.k1, p);
+    }
+  }
+  if (g < nfull) {
+    const U8 v = load8<BF16, NT>(a.g, g * 8);
 #pragma unroll
     for (int s = 0; s < NS; ++s)
       *reinterpret_cast<uint32_t*>(a.codes + s * a.plane + g * 4) =
@@ -289,7 +317,7 @@ __device__ __forceinline__ void luq_flat_body(const LuqArgs& a, const LuqParams&
   }
 }
 
-template <bool BF16, int NS>
+template <bool BF16, bool NT, int NS>
 __global__ __launch_bounds__(kThreads) void luq_encode_flat_kernel(LuqArgs a) {
   const LuqParams p = luq_block_params(a);
   if (p.zero) {  // alpha is 0 or NaN: every code is 0
@@ -299,29 +327,29 @@ __global__ __launch_bounds__(kThreads) void luq_encode_flat_kernel(LuqArgs a) {
     return;
   }
   if (p.S != 1.0f)
-    luq_flat_body<BF16, NS, true>(a, p);
+    luq_flat_body<BF16, NT, NS, true>(a, p);
   else
-    luq_flat_body<BF16, NS, false>(a, p);
+    luq_flat_body<BF16, NT, NS, false>(a, p);
 }
 
-template <bool BF16, bool SCALED>
+template <bool BF16, bool NT, bool SCALED>
 struct LuqEnc {
   const LuqArgs* a;
   const LuqParams* p;
-  __device__ U8 load(int64_t e0) const { return load8<BF16>(a->g, e0); }
+  __device__ U8 load(int64_t e0) const { return load8<BF16, NT>(a->g, e0); }
   __device__ uint32_t word(const U8& v, uint64_t blk, int s) const {
     return p->zero ? 0u : luq_word<SCALED>(v, blk, s, a->counter, a->k0, a->k1, *p);
   }
 };
 
-template <bool BF16, int NS>
+template <bool BF16, bool NT, int NS>
 __global__ __launch_bounds__(kThreads) void luq_encode_tile_kernel(LuqArgs a, int lg, int lt) {
   __shared__ __attribute__((aligned(16))) uint32_t lds[NS * (kTileWords + 32 * kTilePad)];
   const LuqParams p = luq_block_params(a);
   if (p.S != 1.0f)
-    encode_tiles<NS>(LuqEnc<BF16, true>{&a, &p}, a.rows, a.cols, lg, lt, a.codes, a.codes_t, a.plane, lds);
+    encode_tiles<NS>(LuqEnc<BF16, NT, true>{&a, &p}, a.rows, a.cols, lg, lt, a.codes, a.codes_t, a.plane, lds);
   else
-    encode_tiles<NS>(LuqEnc<BF16, false>{&a, &p}, a.rows, a.cols, lg, lt, a.codes, a.codes_t, a.plane, lds);
+    encode_tiles<NS>(LuqEnc<BF16, NT, false>{&a, &p}, a.rows, a.cols, lg, lt, a.codes, a.codes_t, a.plane, lds);
 }
 
 __global__ void write_two_floats_kernel(float* a, float va, float* b, float vb) {
@@ -396,14 +424,14 @@ __device__ __forceinline__ uint32_t int4_word(const U8& v, const Int4Params& p) 
   return out;
 }
 
-template <bool BF16>
+template <bool BF16, bool NT>
 __global__ __launch_bounds__(kThreads) void int4_encode_flat_kernel(Int4Args a) {
   const Int4Params p = int4_block_params(a);
   const int64_t ngroups = (a.n + 7) >> 3;
   for (int64_t g = (int64_t)blockIdx.x * kThreads + threadIdx.x; g < ngroups;
        g += (int64_t)gridDim.x * kThreads) {
     const bool full = (g * 8 + 8) <= a.n;
-    const U8 v = full ? load8<BF16>(a.x, g * 8) : load8_tail<BF16>(a.x, g * 8, a.n);
+    const U8 v = full ? load8<BF16, NT>(a.x, g * 8) : load8_tail<BF16>(a.x, g * 8, a.n);
     const uint32_t word = p.zero ? 0u : int4_word(v, p);
     if (full)
       *reinterpret_cast<uint32_t*>(a.codes + g * 4) = word;
@@ -412,26 +440,29 @@ __global__ __launch_bounds__(kThreads) void int4_encode_flat_kernel(Int4Args a) 
   }
 }
 
-template <bool BF16>
+template <bool BF16, bool NT>
 struct Int4Enc {
   const Int4Args* a;
   const Int4Params* p;
-  __device__ U8 load(int64_t e0) const { return load8<BF16>(a->x, e0); }
+  __device__ U8 load(int64_t e0) const { return load8<BF16, NT>(a->x, e0); }
   __device__ uint32_t word(const U8& v, uint64_t, int) const { return p->zero ? 0u : int4_word(v, *p); }
 };
 
-template <bool BF16>
+template <bool BF16, bool NT>
 __global__ __launch_bounds__(kThreads) void int4_encode_tile_kernel(Int4Args a, int lg, int lt) {
   __shared__ __attribute__((aligned(16))) uint32_t lds[kTileWords + 32 * kTilePad];
   const Int4Params p = int4_block_params(a);
-  encode_tiles<1>(Int4Enc<BF16>{&a, &p}, a.rows, a.cols, lg, lt, a.codes, a.codes_t, 0, lds);
+  encode_tiles<1>(Int4Enc<BF16, NT>{&a, &p}, a.rows, a.cols, lg, lt, a.codes, a.codes_t, 0, lds);
 }
 
 // ------------------------------- launchers ---------------------------------
 
+// Every encode block folds all partials before it starts, so the partial
+// count is kept proportional to the tensor: at least 16 groups of 8
+// elements per max-pass thread.
 static int max_pass_blocks(int64_t n) {
   const int64_t groups = (n + 7) >> 3;
-  int64_t b = (groups + kThreads * 4 - 1) / (kThreads * 4);
+  int64_t b = (groups + kThreads * 16 - 1) / (kThreads * 16);
   if (b < 1) b = 1;
   if (b > kMaxPartials) b = kMaxPartials;
   return (int)b;
@@ -449,7 +480,7 @@ static int encode_blocks_flat(int64_t n) {
 
 // Transposing tile shape: log2 of the column groups per tile (lg) and of the
 // code words per tile (lt).  Tiles shrink from 8192 words until there are at
-// least four per compute unit or a tile is 1024 words (or 8 rows) small.
+// least three per compute unit or a tile is 1024 words (or 8 rows) small.
 struct TileShape {
   int lg, lt, blocks;
 };
@@ -460,7 +491,7 @@ static int64_t tile_count(int64_t rows, int64_t cols, int lg, int lt) {
 }
 
 static TileShape tile_shape(int64_t rows, int64_t cols) {
-  constexpr int64_t kWantTiles = 1024;
+  constexpr int64_t kWantTiles = 768;
   const int64_t cgs = cols >> 3;
   TileShape t;
   t.lg = 0;
@@ -474,23 +505,49 @@ static TileShape tile_shape(int64_t rows, int64_t cols) {
   return t;
 }
 
-template <bool BF16>
-static hipError_t luq_launch_t(const LuqArgs& a, int ns, int nmax, hipStream_t st) {
-  hipLaunchKernelGGL((max_partial_kernel<BF16, 0>), dim3(nmax), dim3(kThreads), 0, st, a.g, a.n,
-                     const_cast<uint32_t*>(a.partial));
+// Max pass.  Tensors that fit in the 256 MB last-level cache are read with
+// ordinary loads so that the encode pass can find them there; larger ones
+// are streamed with non-temporal loads.
+constexpr int64_t kCacheBytes = 256LL << 20;
+
+template <bool BF16, int MODE>
+static void launch_max_pass(const void* x, int64_t n, int nblocks, uint32_t* partial, hipStream_t st) {
+  if (n * (BF16 ? 2 : 4) > kCacheBytes)
+    hipLaunchKernelGGL((max_partial_kernel<BF16, MODE, true>), dim3(nblocks), dim3(kThreads), 0, st, x, n,
+                       partial);
+  else
+    hipLaunchKernelGGL((max_partial_kernel<BF16, MODE, false>), dim3(nblocks), dim3(kThreads), 0, st, x, n,
+                       partial);
+}
+
+// Encode pass.  Its read is the tensor's second; it is non-temporal exactly
+// when the max pass's was (tensors too large to stay in the last-level cache).
+static bool stream_reads(int64_t n, bool bf16) { return n * (bf16 ? 2 : 4) > kCacheBytes; }
+
+template <bool BF16, bool NT>
+static void luq_encode_launch(const LuqArgs& a, int ns, hipStream_t st) {
   if (a.codes_t) {
     const TileShape t = tile_shape(a.rows, a.cols);
     if (ns == 1)
-      hipLaunchKernelGGL((luq_encode_tile_kernel<BF16, 1>), dim3(t.blocks), dim3(kThreads), 0, st, a, t.lg, t.lt);
+      hipLaunchKernelGGL((luq_encode_tile_kernel<BF16, NT, 1>), dim3(t.blocks), dim3(kThreads), 0, st, a, t.lg, t.lt);
     else
-      hipLaunchKernelGGL((luq_encode_tile_kernel<BF16, 2>), dim3(t.blocks), dim3(kThreads), 0, st, a, t.lg, t.lt);
+      hipLaunchKernelGGL((luq_encode_tile_kernel<BF16, NT, 2>), dim3(t.blocks), dim3(kThreads), 0, st, a, t.lg, t.lt);
   } else {
     const int nb = encode_blocks_flat(a.n);
     if (ns == 1)
-      hipLaunchKernelGGL((luq_encode_flat_kernel<BF16, 1>), dim3(nb), dim3(kThreads), 0, st, a);
+      hipLaunchKernelGGL((luq_encode_flat_kernel<BF16, NT, 1>), dim3(nb), dim3(kThreads), 0, st, a);
     else
-      hipLaunchKernelGGL((luq_encode_flat_kernel<BF16, 2>), dim3(nb), dim3(kThreads), 0, st, a);
+      hipLaunchKernelGGL((luq_encode_flat_kernel<BF16, NT, 2>), dim3(nb), dim3(kThreads), 0, st, a);
   }
+}
+
+template <bool BF16>
+static hipError_t luq_launch_t(const LuqArgs& a, int ns, int nmax, hipStream_t st) {
+  launch_max_pass<BF16, 0>(a.g, a.n, nmax, const_cast<uint32_t*>(a.partial), st);
+  if (stream_reads(a.n, BF16))
+    luq_encode_launch<BF16, true>(a, ns, st);
+  else
+    luq_encode_launch<BF16, false>(a, ns, st);
   return hipGetLastError();
 }
 
@@ -526,20 +583,22 @@ template <bool BF16>
 static hipError_t int4_launch_t(const Int4Args& a, hipStream_t st) {
   if (a.clip <= 0.0f) {
     if (a.is_signed)
-      hipLaunchKernelGGL((max_partial_kernel<BF16, 0>), dim3(a.nparts), dim3(kThreads), 0, st, a.x,
-                         a.n, const_cast<uint32_t*>(a.partial));
+      launch_max_pass<BF16, 0>(a.x, a.n, a.nparts, const_cast<uint32_t*>(a.partial), st);
     else
-      hipLaunchKernelGGL((max_partial_kernel<BF16, 1>), dim3(a.nparts), dim3(kThreads), 0, st, a.x,
-                         a.n, const_cast<uint32_t*>(a.partial));
+      launch_max_pass<BF16, 1>(a.x, a.n, a.nparts, const_cast<uint32_t*>(a.partial), st);
   }
+  const bool nt = stream_reads(a.n, BF16);
   if (a.codes_t) {
     const TileShape t = tile_shape(a.rows, a.cols);
-    hipLaunchKernelGGL((int4_encode_tile_kernel<BF16>), dim3(t.blocks), dim3(kThreads), 0, st, a,
-                       t.lg, t.lt);
+    if (nt)
+      hipLaunchKernelGGL((int4_encode_tile_kernel<BF16, true>), dim3(t.blocks), dim3(kThreads), 0, st, a, t.lg, t.lt);
+    else
+      hipLaunchKernelGGL((int4_encode_tile_kernel<BF16, false>), dim3(t.blocks), dim3(kThreads), 0, st, a, t.lg, t.lt);
+  } else if (nt) {
+    hipLaunchKernelGGL((int4_encode_flat_kernel<BF16, true>), dim3(encode_blocks_flat(a.n)), dim3(kThreads), 0, st, a);
+  } else {
+    hipLaunchKernelGGL((int4_encode_flat_kernel<BF16, false>), dim3(encode_blocks_flat(a.n)), dim3(kThreads), 0, st, a);
   }
-  else
-    hipLaunchKernelGGL((int4_encode_flat_kernel<BF16>), dim3(encode_blocks_flat(a.n)),
-                       dim3(kThreads), 0, st, a);
   return hipGetLastError();
 }
 
