@@ -120,8 +120,14 @@ __device__ __forceinline__ void tile_coords(int bid, int ntm, int ntn, int& tm, 
 // into one piece per 32-deep k-step and placed after that k-step's MFMAs, so
 // the VALU work issues between MFMAs.  The MFMA takes the B fragment as its
 // first operand, so each lane ends up with 4 consecutive columns of one C row.
-template <int BM, int BN, int BK, int NS, bool BSIGNED>
-__global__ __launch_bounds__(kGemmThreads, 1) void gemm_luq_int4_kernel(GemmArgs a) {
+//
+// FULLK: K is a multiple of kKAlign, so every stage of a split lies inside
+// the operands' rows and no chunk needs a per-lane range check; stages past
+// the end of the split are then never multiplied.  Otherwise chunks past
+// the split's end read as zeros and the loop may multiply one zero stage.
+// The 64-deep variant keeps three waves per SIMD.
+template <int BM, int BN, int BK, int NS, bool BSIGNED, bool FULLK>
+__global__ __launch_bounds__(kGemmThreads, BK == 64 ? 3 : 1) void gemm_luq_int4_kernel(GemmArgs a) {
   static_assert(BM % 64 == 0 && BN % 64 == 0, "wave tiles are multiples of 32");
   static_assert(BK == 64 || BK == 128, "k per stage");
   constexpr int kBK = BK;
@@ -181,14 +187,14 @@ __global__ __launch_bounds__(kGemmThreads, 1) void gemm_luq_int4_kernel(GemmArgs
 #pragma unroll
     for (int i = 0; i < ACH; ++i) {
       if (i % KS != kk) continue;
-      const int off = (k0 + kca[i]) < kend ? offa[i] + t * (kBK / 2) : kOutOfRange;
+      const int off = FULLK || (k0 + kca[i]) < kend ? offa[i] + t * (kBK / 2) : kOutOfRange;
 #pragma unroll
       for (int s = 0; s < NS; ++s) r.a[s][i] = __builtin_amdgcn_raw_buffer_load_b128(rsa[s], off, 0, 0);
     }
 #pragma unroll
     for (int i = 0; i < BCH; ++i) {
       if (i % KS != kk) continue;
-      const int off = (k0 + kcb[i]) < kend ? offb[i] + t * (kBK / 2) : kOutOfRange;
+      const int off = FULLK || (k0 + kcb[i]) < kend ? offb[i] + t * (kBK / 2) : kOutOfRange;
       r.b[i] = __builtin_amdgcn_raw_buffer_load_b128(rsb, off, 0, 0);
     }
   };
@@ -288,12 +294,14 @@ __global__ __launch_bounds__(kGemmThreads, 1) void gemm_luq_int4_kernel(GemmArgs
   __syncthreads();
 #pragma unroll
   for (int kk = 0; kk < KS; ++kk) load_piece(r0, 2, kk);
-  // Stages beyond nkt load as zeros (masked), so an odd stage count ends on
-  // a zero-filled buffer that adds nothing.
-  for (int t = 0; t < nkt; t += 2) {
+  int t = 0;
+  for (; t + 2 <= nkt; t += 2) {
     step(0, r1, r1, t + 3);   // multiply t, expand t+1 (r1), then reuse r1 for t+3
     step(1, r0, r0, t + 4);   // multiply t+1, expand t+2 (r0), then reuse r0 for t+4
   }
+  // an odd stage count leaves stage t in buffer 0 (with FULLK the stage
+  // expanded beside it may hold another split's codes; it is not multiplied)
+  if (t < nkt) step(0, r1, r1, t + 3);
 
   // Epilogue through LDS.  In MFMA tile (i, j), lane l holds row l%32 and, in
   // registers 4q..4q+3, the 4 consecutive columns 8q + 4*(l/32) + 0..3 (the
@@ -441,7 +449,10 @@ size_t gemm_workspace_bytes(int64_t M, int64_t N, int64_t K, int /*ns*/) {
 
 template <int BM, int BN, int BK, int NS, bool BSIGNED>
 static void launch_tile(const GemmArgs& a, dim3 grid, hipStream_t st) {
-  hipLaunchKernelGGL((gemm_luq_int4_kernel<BM, BN, BK, NS, BSIGNED>), grid, dim3(kGemmThreads), 0, st, a);
+  if (a.K % kKAlign == 0)
+    hipLaunchKernelGGL((gemm_luq_int4_kernel<BM, BN, BK, NS, BSIGNED, true>), grid, dim3(kGemmThreads), 0, st, a);
+  else
+    hipLaunchKernelGGL((gemm_luq_int4_kernel<BM, BN, BK, NS, BSIGNED, false>), grid, dim3(kGemmThreads), 0, st, a);
 }
 
 template <int NS, bool BSIGNED>
