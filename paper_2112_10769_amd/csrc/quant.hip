@@ -82,8 +82,8 @@ __global__ __launch_bounds__(kThreads) void max_partial_kernel(const void* __res
 // When the transposed code layout is requested, work goes by tiles of
 // TW = 2^lt code words: TG = 2^lg column groups (8 columns each) by
 // TR = TW / TG rows.  TG is 32, or the next power of two above the number of
-// column groups for narrow matrices; TW is 8192, or smaller (down to 1024)
-// when that leaves too few tiles to fill the chip.
+// column groups for narrow matrices; TW is 4096 (LUQ) or 8192 (INT4), or
+// smaller (down to 1024) when that leaves too few tiles to fill the chip.
 //   Phase A: consecutive lanes take consecutive column groups of a row, so
 //            the loads and the row-major code stores of a row are contiguous;
 //            every 8-element code word also goes to LDS at [group][row].
@@ -91,7 +91,10 @@ __global__ __launch_bounds__(kThreads) void max_partial_kernel(const void* __res
 //            group, read the block's 8 words (two 16-byte LDS reads),
 //            transpose them in registers and store one word per column, so
 //            consecutive lanes write consecutive words of a transposed row.
-constexpr int kTileWords = 8192;
+// Largest tiles (words): the LUQ encoder is ALU-bound and prefers more,
+// smaller tiles in flight; the INT4 encoder is bound by memory and prefers
+// longer contiguous stores.
+constexpr int kLuqTileLg = 12, kInt4TileLg = 13;
 constexpr int kTilePad = 4;  // LDS words between column groups (keeps 16-byte alignment)
 
 template <int NS, typename Enc>
@@ -105,13 +108,14 @@ __device__ __forceinline__ void encode_tiles(const Enc& enc, int64_t rows, int64
     const int64_t r0 = (t / ntc) * tr, g0 = (t % ntc) * tg;
     // two items per trip (tw is a multiple of 2 * kThreads): both loads are
     // in flight before either is encoded
-    for (int q0 = threadIdx.x; q0 < tw; q0 += 2 * kThreads) {
-      int g[2], r[2];
-      bool ok[2];
-      int64_t e0[2];
-      U8 v[2];
+    constexpr int U = 2;
+    for (int q0 = threadIdx.x; q0 < tw; q0 += U * kThreads) {
+      int g[U], r[U];
+      bool ok[U];
+      int64_t e0[U];
+      U8 v[U];
 #pragma unroll
-      for (int u = 0; u < 2; ++u) {
+      for (int u = 0; u < U; ++u) {
         const int q = q0 + u * kThreads;
         g[u] = q & (tg - 1);
         r[u] = q >> lg;
@@ -121,7 +125,7 @@ __device__ __forceinline__ void encode_tiles(const Enc& enc, int64_t rows, int64
         if (ok[u]) v[u] = enc.load(e0[u]);
       }
 #pragma unroll
-      for (int u = 0; u < 2; ++u) {
+      for (int u = 0; u < U; ++u) {
         uint32_t w[NS];
 #pragma unroll
         for (int s = 0; s < NS; ++s) w[s] = 0;
@@ -344,7 +348,7 @@ struct LuqEnc {
 
 template <bool BF16, bool NT, int NS>
 __global__ __launch_bounds__(kThreads) void luq_encode_tile_kernel(LuqArgs a, int lg, int lt) {
-  __shared__ __attribute__((aligned(16))) uint32_t lds[NS * (kTileWords + 32 * kTilePad)];
+  __shared__ __attribute__((aligned(16))) uint32_t lds[NS * ((1 << kLuqTileLg) + 32 * kTilePad)];
   const LuqParams p = luq_block_params(a);
   if (p.S != 1.0f)
     encode_tiles<NS>(LuqEnc<BF16, NT, true>{&a, &p}, a.rows, a.cols, lg, lt, a.codes, a.codes_t, a.plane, lds);
@@ -450,7 +454,7 @@ struct Int4Enc {
 
 template <bool BF16, bool NT>
 __global__ __launch_bounds__(kThreads) void int4_encode_tile_kernel(Int4Args a, int lg, int lt) {
-  __shared__ __attribute__((aligned(16))) uint32_t lds[kTileWords + 32 * kTilePad];
+  __shared__ __attribute__((aligned(16))) uint32_t lds[(1 << kInt4TileLg) + 32 * kTilePad];
   const Int4Params p = int4_block_params(a);
   encode_tiles<1>(Int4Enc<BF16, NT>{&a, &p}, a.rows, a.cols, lg, lt, a.codes, a.codes_t, 0, lds);
 }
@@ -479,7 +483,7 @@ static int encode_blocks_flat(int64_t n) {
 }
 
 // Transposing tile shape: log2 of the column groups per tile (lg) and of the
-// code words per tile (lt).  Tiles shrink from 8192 words until there are at
+// code words per tile (lt).  Tiles shrink from 2^max_lt words until there are at
 // least three per compute unit or a tile is 1024 words (or 8 rows) small.
 struct TileShape {
   int lg, lt, blocks;
@@ -490,13 +494,13 @@ static int64_t tile_count(int64_t rows, int64_t cols, int lg, int lt) {
   return ((rows + tr - 1) / tr) * (((cols >> 3) + tg - 1) / tg);
 }
 
-static TileShape tile_shape(int64_t rows, int64_t cols) {
+static TileShape tile_shape(int64_t rows, int64_t cols, int max_lt) {
   constexpr int64_t kWantTiles = 768;
   const int64_t cgs = cols >> 3;
   TileShape t;
   t.lg = 0;
   while (t.lg < 5 && (1LL << t.lg) < cgs) ++t.lg;
-  t.lt = 13;
+  t.lt = max_lt;
   while (t.lt > 10 && t.lt - 1 - t.lg >= 3 && tile_count(rows, cols, t.lg, t.lt) < kWantTiles) --t.lt;
   int64_t b = tile_count(rows, cols, t.lg, t.lt);
   if (b < 1) b = 1;
@@ -527,7 +531,7 @@ static bool stream_reads(int64_t n, bool bf16) { return n * (bf16 ? 2 : 4) > kCa
 template <bool BF16, bool NT>
 static void luq_encode_launch(const LuqArgs& a, int ns, hipStream_t st) {
   if (a.codes_t) {
-    const TileShape t = tile_shape(a.rows, a.cols);
+    const TileShape t = tile_shape(a.rows, a.cols, kLuqTileLg);
     if (ns == 1)
       hipLaunchKernelGGL((luq_encode_tile_kernel<BF16, NT, 1>), dim3(t.blocks), dim3(kThreads), 0, st, a, t.lg, t.lt);
     else
@@ -589,7 +593,7 @@ static hipError_t int4_launch_t(const Int4Args& a, hipStream_t st) {
   }
   const bool nt = stream_reads(a.n, BF16);
   if (a.codes_t) {
-    const TileShape t = tile_shape(a.rows, a.cols);
+    const TileShape t = tile_shape(a.rows, a.cols, kInt4TileLg);
     if (nt)
       hipLaunchKernelGGL((int4_encode_tile_kernel<BF16, true>), dim3(t.blocks), dim3(kThreads), 0, st, a, t.lg, t.lt);
     else

@@ -260,7 +260,10 @@ def test_gemm_long_reduction_exact_split(L):
 
 # ------------------------------- im2col -------------------------------------
 
-@pytest.mark.parametrize("B,H,W,C", [(2, 6, 8, 16), (1, 5, 8, 6), (3, 7, 8, 64), (2, 4, 12, 8), (1, 1, 8, 8)])
+# fast path (C and W multiples of 8) over several blocks and odd channel-group
+# counts; generic path otherwise
+@pytest.mark.parametrize("B,H,W,C", [(2, 6, 8, 16), (1, 5, 8, 6), (3, 7, 8, 64), (2, 4, 12, 8), (1, 1, 8, 8),
+                                     (4, 30, 32, 24), (3, 20, 16, 64), (1, 3, 8, 512), (1, 3, 8, 520)])
 def test_im2col_parity(L, B, H, W, C):
     act = synth.half_normal((B, H, W, C), [400, C])
     announce("im2col", B, H, W, C)
