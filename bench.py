@@ -382,7 +382,7 @@ def main():
         rows, value, roof, cfg = run_sweep(L, torch, args.steps, sizes)
         out = {"metric": METRIC, "value": round(value, 2), "unit": "% of roofline", "n_gpus": 1,
                "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(roof["launch_us"] / 1e3, 4), "higher_is_better": True,
-               "scaling": "weak", "vs_baseline": None, "dtype": "f32/bf16 in, u4 codes out",
+               "scaling": "weak", "vs_baseline": None, "dtype": "f32",
                "data": "synthetic", "config": cfg, "roofline": roof, "sweep": rows}
         if not args.no_cpu:
             out["cpu_baseline"] = cpu_sweep_baseline()
