@@ -201,20 +201,21 @@ def run_sweep(L, torch, steps, sizes=None):
 
 
 def cpu_sweep_baseline():
-    """The oracle's LUQ on 2^25 fp32 elements."""
-    import numpy as np
-    from threadpoolctl import threadpool_info
+    """The oracle's LUQ on 2^25 fp32 elements, repeated until at least 10 s."""
     from oracle import luq as oluq
     import synth
     n = 1 << 25
     g = synth.grad_1d(n, "f32", 0.25, seed=4)
-    t0 = time.perf_counter()
-    oluq.luq_quantize(g, R=4)
-    dt = time.perf_counter() - t0
-    alg = 2 * n * 4 + n / 2
+    dt, reps = 0.0, 0
+    while dt < 10.0:
+        t0 = time.perf_counter()
+        oluq.luq_quantize(g, R=4)
+        dt += time.perf_counter() - t0
+        reps += 1
+    alg = (2 * n * 4 + n / 2) * reps
     return {"value": round(100.0 * alg / dt / HBM_PEAK, 6), "unit": "% of MI355X HBM roofline",
             "cores": 1, "kind": "oracle", "GB/s": round(alg / dt / 1e9, 4),
-            "sample": f"LUQ of 2^25 fp32 elements ({dt:.2f}s, NumPy, one core)"}
+            "sample": f"LUQ of 2^25 fp32 elements, {reps} times ({dt:.2f}s, NumPy, one core)"}
 
 
 def capture(torch, fns):
@@ -313,19 +314,27 @@ def cpu_baseline(workload, d):
         sample = f"the whole step, {reps} times (last: " + ", ".join(parts) + ")"
         parts.clear()
     else:
+        # LUQ and INT4 on 2^20 elements and dX on 64 token rows, repeated until
+        # at least 10 s of CPU work
         n = 1 << 20
         g = d["g"].reshape(-1)[:n]
-        timed("luq 2^20 bf16", lambda: oluq.luq_quantize(g, dtype="bf16", R=4), 2 * 2 * n + n / 2)
         x = d["x"].reshape(-1)[:n]
-        timed("int4 2^20 bf16", lambda: oint4.int4_quantize(x, dtype="bf16"), 2 * 2 * n + n / 2)
         F = d["g"].shape[1]
         D = d["x"].shape[1]
         rows = 64
         gcodes, alpha, _ = oluq.luq_quantize(d["g"][:rows], dtype="bf16", R=4)
         wc, ws = oint4.int4_quantize(d["W"], is_signed=True)             # [F, D] = [K, N]
-        timed(f"dgrad {rows} rows", lambda: ogemm.gemm_dgrad_ref(gcodes, alpha, wc, ws, True, rows, D, F),
-              rows * F / 2 + 4 * rows * D, 2.0 * rows * D * F)
-        sample = f"LUQ and INT4 on 2^20 elements, dX on {rows} token rows"
+        reps = 0
+        while t_cpu < 10.0:
+            parts.clear()
+            timed("luq 2^20 bf16", lambda: oluq.luq_quantize(g, dtype="bf16", R=4), 2 * 2 * n + n / 2)
+            timed("int4 2^20 bf16", lambda: oint4.int4_quantize(x, dtype="bf16"), 2 * 2 * n + n / 2)
+            timed(f"dgrad {rows} rows", lambda: ogemm.gemm_dgrad_ref(gcodes, alpha, wc, ws, True, rows, D, F),
+                  rows * F / 2 + 4 * rows * D, 2.0 * rows * D * F)
+            reps += 1
+        sample = (f"LUQ and INT4 on 2^20 elements, dX on {rows} token rows, {reps} times (last: "
+                  + ", ".join(parts) + ")")
+        parts.clear()
     blas = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
     return {"value": 100.0 * t_roof / t_cpu, "unit": "% of MI355X roofline", "cores": int(blas),
             "kind": "oracle", "sample": sample + ("; " + ", ".join(parts) if parts else ""),
