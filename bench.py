@@ -92,10 +92,12 @@ def build_resnet(L, torch, dev):
         Stage("int4_im2col3x3_t", lambda: L.int4_im2col3x3_t(ac, B, H, W, C, colt), n_a / 2 + Ki * T / 2),
         Stage("int4_quantize(W)", lambda: L.int4_quantize(w, True, 0.0, False, wct, sw, wsw),
               2 * 4 * n_w + n_w / 2),
-        Stage("luq_gemm_dgrad", lambda: L.luq_gemm_dgrad(gc, alpha, wct, sw, True, T, Ki, Co, 1, dx, wsd),
-              T * Co / 2 + Ki * Co / 2 + 4 * T * Ki, 2.0 * T * Ki * Co),
+        # dW right after im2col, while its 58 MB of column codes may still be in
+        # the last-level cache; the dX GEMM's 462 MB of output would evict them
         Stage("luq_gemm_wgrad", lambda: L.luq_gemm_wgrad(gct, alpha, colt, sa, False, T, Co, Ki, 1, dw, wsg),
               Co * T / 2 + Ki * T / 2 + 4 * Co * Ki, 2.0 * T * Ki * Co),
+        Stage("luq_gemm_dgrad", lambda: L.luq_gemm_dgrad(gc, alpha, wct, sw, True, T, Ki, Co, 1, dx, wsd),
+              T * Co / 2 + Ki * Co / 2 + 4 * T * Ki, 2.0 * T * Ki * Co),
     ]
     d["dev"] = dict(g=g, act=act, w=w, gc=gc, gct=gct, alpha=alpha, gmax=gmax, ac=ac, sa=sa, colt=colt,
                     wct=wct, sw=sw, dx=dx, dw=dw)
