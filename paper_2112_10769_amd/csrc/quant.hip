@@ -28,7 +28,11 @@
 namespace luq {
 
 constexpr int kThreads = 256;
-constexpr int kMaxPartials = 2048;
+// Partials of the max pass.  Up to kDirectPartials, every encode block
+// folds them itself; beyond that (large tensors, more max-pass blocks in
+// flight) one extra block folds them into the word after the partials.
+constexpr int kDirectPartials = 2048;
+constexpr int kMaxPartials = 16384;
 constexpr int kMaxEncodeBlocks = 4096;
 
 // Max-pass keys.  MODE 0: |x| (LUQ, signed INT4).  MODE 1: max(x, 0) with
@@ -75,6 +79,22 @@ __global__ __launch_bounds__(kThreads) void max_partial_kernel(const void* __res
   for (int i = 1; i < G; ++i) m[0] = max(m[0], m[i]);
   const uint32_t r = block_max_u32(m[0], scratch);
   if (threadIdx.x == 0) partial[blockIdx.x] = r;
+}
+
+// Folds `nparts` (<= 16 * 1024) partial keys into one (one block): each
+// thread reads its 16 consecutive keys with independent loads.
+__global__ __launch_bounds__(1024) void fold_partials_kernel(const uint32_t* __restrict__ partial, int nparts,
+                                                            uint32_t* __restrict__ out) {
+  __shared__ uint32_t scratch[1024 / kWave];
+  const int i0 = threadIdx.x * 16;
+  uint32_t v[16];
+#pragma unroll
+  for (int k = 0; k < 16; ++k) v[k] = i0 + k < nparts ? partial[i0 + k] : 0u;
+  uint32_t m = 0;
+#pragma unroll
+  for (int k = 0; k < 16; ++k) m = max(m, v[k]);
+  m = block_max_u32(m, scratch);
+  if (threadIdx.x == 0) *out = m;
 }
 
 // ---------------------------- transposing tiles ----------------------------
@@ -461,18 +481,20 @@ __global__ __launch_bounds__(kThreads) void int4_encode_tile_kernel(Int4Args a, 
 
 // ------------------------------- launchers ---------------------------------
 
-// Every encode block folds all partials before it starts, so the partial
-// count is kept proportional to the tensor: at least 16 groups of 8
-// elements per max-pass thread.
+// Every encode block folds the partials it is given before it starts, so
+// while they are given directly their count is kept proportional to the
+// tensor (at least 16 groups of 8 elements per max-pass thread); large
+// tensors get up to kMaxPartials blocks (8 groups per thread) and one fold.
 static int max_pass_blocks(int64_t n) {
   const int64_t groups = (n + 7) >> 3;
   int64_t b = (groups + kThreads * 16 - 1) / (kThreads * 16);
+  if (b > kDirectPartials) b = (groups + kThreads * 8 - 1) / (kThreads * 8);
   if (b < 1) b = 1;
   if (b > kMaxPartials) b = kMaxPartials;
   return (int)b;
 }
 
-size_t quant_workspace_bytes(int64_t /*n*/) { return kMaxPartials * sizeof(uint32_t); }
+size_t quant_workspace_bytes(int64_t /*n*/) { return (kMaxPartials + 1) * sizeof(uint32_t); }
 
 static int encode_blocks_flat(int64_t n) {
   const int64_t groups = (n + 7) >> 3;
@@ -522,6 +544,14 @@ static void launch_max_pass(const void* x, int64_t n, int nblocks, uint32_t* par
   else
     hipLaunchKernelGGL((max_partial_kernel<BF16, MODE, false>), dim3(nblocks), dim3(kThreads), 0, st, x, n,
                        partial);
+  if (nblocks > kDirectPartials)
+    hipLaunchKernelGGL(fold_partials_kernel, dim3(1), dim3(1024), 0, st, partial, nblocks, partial + kMaxPartials);
+}
+
+// What the encode blocks fold: the partials themselves, or the one folded word.
+static const uint32_t* encode_partials(const uint32_t* partial, int nblocks, int* nparts) {
+  *nparts = nblocks > kDirectPartials ? 1 : nblocks;
+  return nblocks > kDirectPartials ? partial + kMaxPartials : partial;
 }
 
 // Encode pass.  Its read is the tensor's second; it is non-temporal exactly
@@ -546,8 +576,10 @@ static void luq_encode_launch(const LuqArgs& a, int ns, hipStream_t st) {
 }
 
 template <bool BF16>
-static hipError_t luq_launch_t(const LuqArgs& a, int ns, int nmax, hipStream_t st) {
-  launch_max_pass<BF16, 0>(a.g, a.n, nmax, const_cast<uint32_t*>(a.partial), st);
+static hipError_t luq_launch_t(LuqArgs a, int ns, int nmax, hipStream_t st) {
+  uint32_t* ws = const_cast<uint32_t*>(a.partial);
+  launch_max_pass<BF16, 0>(a.g, a.n, nmax, ws, st);
+  a.partial = encode_partials(ws, nmax, &a.nparts);
   if (stream_reads(a.n, BF16))
     luq_encode_launch<BF16, true>(a, ns, st);
   else
@@ -584,12 +616,13 @@ hipError_t launch_luq_quantize(const void* g, int bf16, int64_t rows, int64_t co
 }
 
 template <bool BF16>
-static hipError_t int4_launch_t(const Int4Args& a, hipStream_t st) {
+static hipError_t int4_launch_t(Int4Args a, hipStream_t st) {
   if (a.clip <= 0.0f) {
     if (a.is_signed)
       launch_max_pass<BF16, 0>(a.x, a.n, a.nparts, const_cast<uint32_t*>(a.partial), st);
     else
       launch_max_pass<BF16, 1>(a.x, a.n, a.nparts, const_cast<uint32_t*>(a.partial), st);
+    a.partial = encode_partials(a.partial, a.nparts, &a.nparts);
   }
   const bool nt = stream_reads(a.n, BF16);
   if (a.codes_t) {
