@@ -119,12 +119,24 @@ def _edge_cases():
     return cases
 
 
+def _big(x, at_least=70000, multiple=64):
+    """x repeated to at least `at_least` elements (several max-pass and encode
+    workgroups), cut to a multiple of `multiple` elements."""
+    reps = -(-at_least // x.size)
+    y = np.tile(x, reps)
+    return y[: (y.size // multiple) * multiple] if y.size >= multiple else y
+
+
+# each case as given (one or a few workgroups) and repeated to a larger size
+@pytest.mark.parametrize("size", ["small", "large"])
 @pytest.mark.parametrize("name", list(_edge_cases().keys()))
-def test_luq_edge_values(L, name):
+def test_luq_edge_values(L, name, size):
     x = _edge_cases()[name]
-    _check_luq(L, x, 1, x.size, seed=11, counter=2, what=name)
+    if size == "large":
+        x = _big(x)
+    _check_luq(L, x, 1, x.size, seed=11, counter=2, what=f"{name} {size}")
     if x.size % 64 == 0:
-        _check_luq(L, x, 8, x.size // 8, seed=11, counter=2, want_t=True, what=name + " tile")
+        _check_luq(L, x, 8, x.size // 8, seed=11, counter=2, want_t=True, what=f"{name} {size} tile")
 
 
 def test_luq_empty(L):
@@ -170,20 +182,21 @@ def test_int4_parity(L, signed, dtype, shape):
     _check_int4(L, x, r, c, signed, want_t=(r % 8 == 0 and c % 8 == 0), what="int4")
 
 
-def test_int4_clip_and_edges(L):
-    x = synth.normal((4096,), 1.0, [301])
-    _check_int4(L, x, 1, 4096, True, clip=0.75, what="clip")
-    _check_int4(L, x, 64, 64, False, clip=2.0, want_t=True, what="clip unsigned")
+@pytest.mark.parametrize("n", [4096, 81920])
+def test_int4_clip_and_edges(L, n):
+    x = synth.normal((n,), 1.0, [301])
+    _check_int4(L, x, 1, n, True, clip=0.75, what="clip")
+    _check_int4(L, x, 64, n // 64, False, clip=2.0, want_t=True, what="clip unsigned")
     _check_int4(L, np.zeros(100, np.float32), 1, 100, True, what="zeros")
-    _check_int4(L, -np.abs(x), 1, 4096, False, what="all negative unsigned")
+    _check_int4(L, -np.abs(x), 1, n, False, what="all negative unsigned")
     y = x.copy()
     y[9] = np.nan
-    _check_int4(L, y, 1, 4096, True, what="nan")
+    _check_int4(L, y, 1, n, True, what="nan")
     y = x.copy()
-    y[9] = -np.inf
-    _check_int4(L, y, 1, 4096, False, what="-inf unsigned")
+    y[n - 9] = -np.inf
+    _check_int4(L, y, 1, n, False, what="-inf unsigned")
     _check_int4(L, np.array([0.5, -0.5, 1.5, 2.5, -2.5, 7, -7, 3.5] * 8, np.float32), 1, 64, True, what="ties")
-    _check_int4(L, (x * np.float32(2.0e-38)).astype(np.float32), 1, 4096, True, what="tiny max")
+    _check_int4(L, (x * np.float32(2.0e-38)).astype(np.float32), 1, n, True, what="tiny max")
 
 
 # ------------------------------- GEMMs --------------------------------------
