@@ -314,9 +314,9 @@ __global__ __launch_bounds__(kGemmThreads, BK == 64 ? 3 : 1) void gemm_luq_int4_
   constexpr int WM = BM / 2, WN = BN / 2;
   constexpr int EP = WN + 4;      // slab row pitch in 32-bit words
   constexpr int LPR = WN / 4;     // lanes per row in the store phase
-  constexpr int RPI = 64 / LPR;   // rows per store instruction
+  constexpr int RPI = 64 / LPR;   // rows per store instruction (lanes past RPI * LPR idle)
   static_assert(4 * 32 * EP * 4 <= 2 * STAGE, "epilogue slabs fit in the stage buffers");
-  static_assert(WM % 32 == 0 && 64 % LPR == 0, "slab shape");
+  static_assert(WM % 32 == 0 && LPR <= 64 && 32 % RPI == 0, "slab shape");
   uint32_t* E = reinterpret_cast<uint32_t*>(lds) + wave * 32 * EP;
   const bool part = a.partial != nullptr;
   const float sc = part ? 0.0f
@@ -325,6 +325,7 @@ __global__ __launch_bounds__(kGemmThreads, BK == 64 ? 3 : 1) void gemm_luq_int4_
                        : reinterpret_cast<uint32_t*>(a.C);
   const int64_t rbase = m0 + wm * WM, cbase = n0 + wn * WN;
   const int srow = lane / LPR, scol = (lane % LPR) * 4;
+  const bool sact = lane < RPI * LPR;
   __syncthreads();  // every wave is done with the stage buffers
 #pragma unroll
   for (int i = 0; i < TM; ++i) {
@@ -345,7 +346,7 @@ __global__ __launch_bounds__(kGemmThreads, BK == 64 ? 3 : 1) void gemm_luq_int4_
     for (int rr = 0; rr < 32; rr += RPI) {
       const int64_t row = rbase + i * 32 + rr + srow;
       const int64_t col = cbase + scol;
-      if (row < a.M) {
+      if (sact && row < a.M) {
         const v4u v = *reinterpret_cast<const v4u*>(E + (rr + srow) * EP + scol);
         uint32_t* dst = out + row * a.N + col;
         if (a.vec && col + 3 < a.N) {
@@ -410,6 +411,11 @@ static GemmPlan plan_gemm(int64_t M, int64_t N, int64_t K) {
   if (K >= 1024 && tiles(256, 256) >= 256) {
     p.bm = 256;
     p.bn = 256;
+  } else if (M <= 64 && N >= 192 && K >= 65536) {
+    // few output rows and a long reduction (the conv dW: 64 x 576 x 200704):
+    // wide tiles so that the A rows are re-read for fewer column tiles
+    p.bm = 64;
+    p.bn = 192;
   } else if (tiles(128, 128) >= 128) {
     p.bm = 128;
     p.bn = 128;
@@ -425,9 +431,12 @@ static GemmPlan plan_gemm(int64_t M, int64_t N, int64_t K) {
   const int64_t nt = p.tiles_m * p.tiles_n;
   const int64_t ktiles = (K + kKAlign - 1) / kKAlign;
   int64_t splits = 1;
-  // too few tiles to fill 256 CUs: split the reduction (>= 8 k-stages each)
+  // too few tiles to fill 256 CUs: split the reduction (>= 8 k-stages each);
+  // the wide tiles aim at one workgroup per CU, since every split adds
+  // M x N partial sums to write and read back
   if (nt < 256) {
-    splits = (512 + nt - 1) / nt;
+    const int64_t target = p.bn == 192 ? 256 : 512;
+    splits = (target + nt - 1) / nt;
     const int64_t max_by_len = ktiles / 8 > 0 ? ktiles / 8 : 1;
     if (splits > max_by_len) splits = max_by_len;
   }
@@ -470,6 +479,8 @@ static hipError_t gemm_launch_t(const GemmArgs& a0, const GemmPlan& p, hipStream
     launch_tile<128, 128, 64, NS, BSIGNED>(a, grid, st);
   else if (p.bm == 128)
     launch_tile<128, 128, 128, NS, BSIGNED>(a, grid, st);
+  else if (p.bn == 192)
+    launch_tile<64, 192, 128, NS, BSIGNED>(a, grid, st);
   else
     launch_tile<64, 64, 128, NS, BSIGNED>(a, grid, st);
   if (p.splits > 1) {

@@ -266,6 +266,13 @@ def test_wgrad_signed_activations(L):
     _wgrad_case(L, 512, 64, 72, 1, signed=True, seed=9)
 
 
+# few output rows, long reduction: the 64x192 split-K tile (ragged and
+# 128-aligned reductions, ragged columns)
+@pytest.mark.parametrize("T,Nout,Kin,ns", [(70048, 40, 200, 1), (66560, 64, 576, 1), (65696, 24, 392, 2)])
+def test_wgrad_wide_tile(L, T, Nout, Kin, ns):
+    _wgrad_case(L, T, Nout, Kin, ns, signed=False, seed=T % 1000 + Kin)
+
+
 def test_gemm_long_reduction_exact_split(L):
     """K beyond the int32-exact chunk: chunk sums are combined in int64."""
     _wgrad_case(L, (1 << 18) + 4096, 8, 16, 1, signed=False, seed=13)
