@@ -12,7 +12,8 @@
 // global memory into LDS:
 //   LUQ  : a byte LUT (v_perm_b32) maps the exponent field e to 2^(e-1) (or
 //          0), then bytes whose sign bit is set are negated with a SWAR
-//          xor/add.  SMP planes are added bytewise (|sum| <= 64).
+//          xor/add.  Two SMP planes are expanded to excess-64 bytes and
+//          summed with one word add (|sum| <= 64, no carries).
 //   INT4 : the nibble is moved to the top of its byte, giving 16*q (signed,
 //          two's complement) or 8*q (unsigned) with no further work; the
 //          extra power of two is removed exactly in the epilogue.
@@ -60,6 +61,22 @@ __device__ __forceinline__ void expand_luq(uint32_t x, uint32_t& lo, uint32_t& h
   hi = (m_hi ^ k_hi) + (q_hi & 0x01010101u);
 }
 
+// SMP operand (two LUQ planes, R <= 5 so every value is in [-32, 32]): each
+// plane is expanded to excess-64 bytes u = 64 + v (a LUT of 64 + 2^(e-1),
+// and 128 - that for negative codes, as (P ^ 0x7F) + 1), so that the byte
+// sum u0 + u1 = 128 + v0 + v1 lies in [64, 192] and one word add carries
+// nothing across bytes; flipping bit 7 then gives v0 + v1 in two's
+// complement.
+__device__ __forceinline__ void expand_luq_excess64(uint32_t x, uint32_t& lo, uint32_t& hi) {
+  // bytes 0..7: 64 + {0, 1, 2, 4, 8, 16, 32, 64}
+  const uint32_t t_lo = 0x44424140u, t_hi = 0x80605048u;
+  const uint32_t p_lo = __builtin_amdgcn_perm(t_hi, t_lo, x & 0x07070707u);
+  const uint32_t p_hi = __builtin_amdgcn_perm(t_hi, t_lo, (x >> 4) & 0x07070707u);
+  const uint32_t s_lo = (x >> 3) & 0x01010101u, s_hi = (x >> 7) & 0x01010101u;
+  lo = (p_lo ^ ((s_lo << 7) - s_lo)) + s_lo;
+  hi = (p_hi ^ ((s_hi << 7) - s_hi)) + s_hi;
+}
+
 template <bool SIGNED>
 __device__ __forceinline__ void expand_int4(uint32_t x, uint32_t& lo, uint32_t& hi) {
   if constexpr (SIGNED) {
@@ -69,12 +86,6 @@ __device__ __forceinline__ void expand_int4(uint32_t x, uint32_t& lo, uint32_t& 
     lo = (x << 3) & 0x78787878u;  // 8 * q
     hi = (x >> 1) & 0x78787878u;
   }
-}
-
-// Bytewise int8 addition without carries between bytes.
-__device__ __forceinline__ uint32_t add_i8x4(uint32_t a, uint32_t b) {
-  const uint32_t s = (a & 0x7F7F7F7Fu) + (b & 0x7F7F7F7Fu);
-  return s ^ ((a ^ b) & 0x80808080u);
 }
 
 struct GemmArgs {
@@ -207,16 +218,18 @@ __global__ __launch_bounds__(kGemmThreads, BK == 64 ? 3 : 1) void gemm_luq_int4_
       const int c = tid + i * kGemmThreads, row = c / KC, kc = c % KC;
       uint32_t w[8];
       const uint32_t x0[4] = {r.a[0][i][0], r.a[0][i][1], r.a[0][i][2], r.a[0][i][3]};
+      if constexpr (NS == 1) {
 #pragma unroll
-      for (int d = 0; d < 4; ++d) expand_luq(x0[d], w[2 * d], w[2 * d + 1]);
-      if constexpr (NS == 2) {
+        for (int d = 0; d < 4; ++d) expand_luq(x0[d], w[2 * d], w[2 * d + 1]);
+      } else {
         const uint32_t x1[4] = {r.a[1][i][0], r.a[1][i][1], r.a[1][i][2], r.a[1][i][3]};
 #pragma unroll
         for (int d = 0; d < 4; ++d) {
-          uint32_t l, h;
-          expand_luq(x1[d], l, h);
-          w[2 * d] = add_i8x4(w[2 * d], l);
-          w[2 * d + 1] = add_i8x4(w[2 * d + 1], h);
+          uint32_t l0, h0, l1, h1;
+          expand_luq_excess64(x0[d], l0, h0);
+          expand_luq_excess64(x1[d], l1, h1);
+          w[2 * d] = (l0 + l1) ^ 0x80808080u;
+          w[2 * d + 1] = (h0 + h1) ^ 0x80808080u;
         }
       }
       uint4* dst = reinterpret_cast<uint4*>(As + row * kPitch + kc * 32);
