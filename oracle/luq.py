@@ -141,6 +141,59 @@ def luq_quantize(x, dtype="f32", R=4, seed=0, counter=0, n_samples=1):
     return codes, alpha, maxabs
 
 
+def hindsight_estimate(m_hat):
+    """The estimate as the quantizer reads it: NaN stays NaN, anything not
+    positive is 0."""
+    m = np.float32(m_hat)
+    if np.isnan(m):
+        return np.float32(np.nan)
+    return m if m > 0 else np.float32(0.0)
+
+
+def hindsight_update(maxabs, m_hat, eta):
+    """Eq. hindsight: m^t = (1 - eta) max|x^(t-1)| + eta m^(t-1), in float32:
+    fl32(fl32(fl32(1 - eta) * max) + fl32(fl32(eta) * m))."""
+    c1 = np.float32(np.float32(1.0) - np.float32(eta))
+    c0 = np.float32(eta)
+    with np.errstate(invalid="ignore", over="ignore"):
+        return np.float32(np.float32(c1 * np.float32(maxabs)) + np.float32(c0 * np.float32(m_hat)))
+
+
+def luq_quantize_hindsight(x, m_hat, dtype="f32", R=4, seed=0, counter=0, n_samples=1, eta=0.1):
+    """LUQ in one pass with the in-hindsight maximum (Section 4, "Reducing the
+    data movement"; Appendix on hindsight).
+
+    The tensor is quantized with alpha = fl32(m_hat / 2^R) from the estimate
+    carried over from the previous step, while its own max|x| is measured;
+    the estimate for the next step follows Eq. hindsight.  Magnitudes at or
+    above alpha 2^R (the estimate may be below this tensor's maximum) take the
+    top level with their sign, as does a NaN element; codes are otherwise
+    those of ``luq_fields`` (Section 4).  A non-finite estimate gives alpha =
+    NaN and all codes 0, a zero estimate all codes 0.
+
+    Returns (codes, alpha, maxabs, m_next).
+    """
+    xf = to_float32(x, dtype).ravel()
+    N = xf.size
+    codes = np.zeros((n_samples, (N + 1) // 2), dtype=np.uint8)
+    m = hindsight_estimate(m_hat)
+    alpha = np.float32(np.nan) if not np.isfinite(m) else luq_alpha(m, R)
+    a = np.abs(xf.astype(np.float64))
+    if N == 0:
+        maxabs = np.float32(0.0)
+    elif np.any(np.isnan(a)):
+        maxabs = np.float32(np.nan)
+    else:
+        maxabs = np.float32(a.max())
+    if np.isfinite(alpha) and alpha > 0 and N > 0:
+        a_top = np.where(np.isnan(a), np.inf, a)
+        for s in range(n_samples):
+            e = luq_fields(a_top, alpha, R, luq_uniforms(N, seed, counter, s))
+            nib = e | np.where((e != 0) & np.signbit(xf), 8, 0).astype(np.uint8)
+            codes[s] = pack_nibbles(nib)
+    return codes, alpha, maxabs, hindsight_update(maxabs, m, eta)
+
+
 def luq_nibbles_range(xf, start, alpha, R, seed, counter, sample):
     """Unpacked codes of the elements start .. start+len(xf)-1 of a tensor
     whose alpha is already known (xf: their float32 values).  The codes of a
