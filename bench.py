@@ -21,7 +21,8 @@ of the same workload.
 2^20..2^30 elements (fp32 and bf16, lognormal magnitudes exp(N(-10, 3)),
 random sign, 25% zeros; 0% and 50% zeros at 2^28): `value` is then the
 quantizer's mean fraction of the HBM roofline over the sizes >= 2^27, and
-`sweep` lists every size.
+`sweep` lists every size, with the single-pass in-hindsight variant
+(roofline N * s_in + N/2 bytes) beside it.
 """
 import argparse
 import json
@@ -185,10 +186,20 @@ def run_sweep(L, torch, steps, sizes=None):
         gr.replay()
         t = time_graph(torch, gr, max(3, steps // 4)) / per_graph
         alg = 2 * n * s_in + n / 2
+        # single pass with the in-hindsight maximum (the estimate starts at
+        # this tensor's maximum, so every replay sees the same estimate)
+        state = gmax.clone()
+        hs = lambda: L.luq_quantize_grad_hindsight(g, state, 4, 0, 0, 1, 0.0, codes, False, alpha, None, ws)
+        grh = capture(torch, [hs] * per_graph)
+        grh.replay()
+        th = time_graph(torch, grh, max(3, steps // 4)) / per_graph
+        alg1 = n * s_in + n / 2
         rows.append({"log2_n": k, "dtype": dt, "zeros": z, "us": round(t * 1e6, 2),
                      "GB/s": round(alg / t / 1e9, 1), "frac": round(alg / t / HBM_PEAK, 4),
-                     "single_read_GB/s": round((n * s_in + n / 2) / t / 1e9, 1)})
-        del g, codes, ws, gr
+                     "single_read_GB/s": round((n * s_in + n / 2) / t / 1e9, 1),
+                     "hindsight_us": round(th * 1e6, 2), "hindsight_GB/s": round(alg1 / th / 1e9, 1),
+                     "hindsight_frac": round(alg1 / th / HBM_PEAK, 4)})
+        del g, codes, ws, gr, grh
         torch.cuda.empty_cache()
     big = [r["frac"] for r in rows if r["log2_n"] >= min(27, max(sizes)) and r["zeros"] == 0.25]
     top = max((r for r in rows if r["zeros"] == 0.25 and r["dtype"] == "f32"), key=lambda r: r["log2_n"])

@@ -47,7 +47,7 @@
 extern "C" {
 #endif
 
-#define LUQ_ABI_VERSION 1
+#define LUQ_ABI_VERSION 2
 
 typedef int luq_status;
 enum {
@@ -124,6 +124,40 @@ luq_status luq_quantize_grad(const void* g, luq_dtype dt, int64_t rows, int64_t 
                              uint64_t seed, uint32_t counter, int n_samples, uint8_t* codes,
                              uint8_t* codes_t, float* alpha, float* maxabs, void* ws,
                              size_t ws_bytes, void* stream);
+
+/*
+ * luq_quantize_grad_hindsight -- LUQ in one pass over g with the
+ * in-hindsight maximum (Section 4, "Reducing the data movement"; the
+ * hindsight appendix).
+ *
+ * Instead of measuring max|g| first, alpha = fl32(m / 2^R) comes from the
+ * estimate m in *state, carried over from the previous step; the same pass
+ * measures max|g| of this tensor, and *state becomes the next estimate
+ * (Eq. hindsight):
+ *     m' = fl32( fl32(fl32(1 - eta) * max|g|) + fl32(eta * m) ).
+ * Codes are those of luq_quantize_grad for that alpha, except that
+ * magnitudes at or above alpha * 2^R (the estimate may be below this
+ * tensor's maximum), and NaN elements, take the top code R + 1 with their
+ * sign.  An estimate that is NaN or infinite gives alpha = NaN and all codes
+ * 0; one that is 0 or negative gives alpha = 0 and all codes 0.  With
+ * *state = max|g| the codes equal luq_quantize_grad's.
+ *
+ *  g, dt, rows, cols, R, seed, counter, n_samples, codes, codes_t
+ *           as for luq_quantize_grad.
+ *  eta      momentum in [0, 1] (0.1 in the paper's experiments).
+ *  state    in/out: 1 float on the device, the estimate m (initialise it,
+ *           e.g., with the maxabs of luq_quantize_grad on an earlier step).
+ *  alpha    out: 1 float, the alpha used.
+ *  maxabs   out: 1 float, max|g| of this tensor (NaN if g has a NaN), or NULL.
+ *  ws       workspace of luq_workspace_size(LUQ_OP_QUANTIZE_GRAD, rows*cols).
+ *
+ * Errors as for luq_quantize_grad; LUQ_ERR_PARAM for eta outside [0, 1],
+ * LUQ_ERR_NULL for a NULL state.
+ */
+luq_status luq_quantize_grad_hindsight(const void* g, luq_dtype dt, int64_t rows, int64_t cols, int R,
+                                       uint64_t seed, uint32_t counter, int n_samples, float eta,
+                                       uint8_t* codes, uint8_t* codes_t, float* state, float* alpha,
+                                       float* maxabs, void* ws, size_t ws_bytes, void* stream);
 
 /*
  * int4_quantize -- uniform INT4 round-to-nearest quantizer (Section 3.3;

@@ -22,8 +22,8 @@ OP_QUANTIZE_GRAD, OP_INT4_QUANTIZE, OP_GEMM_DGRAD, OP_GEMM_WGRAD = 0, 1, 2, 3
 
 EXPORTS = (
     "luq_abi_version", "luq_status_string", "luq_last_error", "luq_plane_bytes",
-    "luq_workspace_size", "luq_quantize_grad", "int4_quantize", "luq_gemm_dgrad",
-    "luq_gemm_wgrad", "int4_im2col3x3_t",
+    "luq_workspace_size", "luq_quantize_grad", "luq_quantize_grad_hindsight", "int4_quantize",
+    "luq_gemm_dgrad", "luq_gemm_wgrad", "int4_im2col3x3_t",
 )
 
 
@@ -49,6 +49,9 @@ def _load():
     lib.luq_workspace_size.argtypes = [i32, i64, i64, i64]
     lib.luq_quantize_grad.restype = i32
     lib.luq_quantize_grad.argtypes = [vp, i32, i64, i64, i32, u64, u32, i32, vp, vp, vp, vp, vp, sz, vp]
+    lib.luq_quantize_grad_hindsight.restype = i32
+    lib.luq_quantize_grad_hindsight.argtypes = [vp, i32, i64, i64, i32, u64, u32, i32, f32, vp, vp, vp, vp, vp, vp,
+                                                sz, vp]
     lib.int4_quantize.restype = i32
     lib.int4_quantize.argtypes = [vp, i32, i64, i64, i32, f32, vp, vp, vp, vp, sz, vp]
     lib.luq_gemm_dgrad.restype = i32
@@ -132,6 +135,34 @@ def luq_quantize_grad(g, R=4, seed=0, counter=0, n_samples=1, codes=True, codes_
                                _ptr(codes), _ptr(codes_t), _ptr(alpha), _ptr(maxabs), _ptr(ws),
                                ws.numel(), _stream(dev))
     _check(st, "luq_quantize_grad")
+    return codes, codes_t, alpha, maxabs
+
+
+def luq_quantize_grad_hindsight(g, state, R=4, seed=0, counter=0, n_samples=1, eta=0.1, codes=True,
+                                codes_t=False, alpha=None, maxabs=None, ws=None):
+    """Single-pass LUQ with the in-hindsight maximum: alpha from the estimate
+    in `state` (a 1-element float32 device tensor, updated in place to the
+    next estimate).  Returns (codes, codes_t, alpha, maxabs)."""
+    rows, cols = _shape2d(g)
+    n = rows * cols
+    dev = g.device
+    pb = plane_bytes(n)
+    if codes is True:
+        codes = _bytes(n_samples * pb, dev).view(n_samples, -1) if n else _bytes(1, dev)
+    if codes_t is True:
+        codes_t = _bytes(n_samples * pb, dev).view(n_samples, -1) if n else _bytes(1, dev)
+    codes = codes if codes is not False else None
+    codes_t = codes_t if codes_t is not False else None
+    alpha = torch.empty(1, dtype=torch.float32, device=dev) if alpha is None else alpha
+    maxabs = torch.empty(1, dtype=torch.float32, device=dev) if maxabs is None else maxabs
+    wsb = workspace_size(OP_QUANTIZE_GRAD, n)
+    ws = _bytes(wsb, dev) if ws is None else ws
+    g = g.contiguous()
+    st = LIB.luq_quantize_grad_hindsight(_ptr(g) if n else None, _dtype(g), rows, cols, R,
+                                         seed & (2**64 - 1), counter & 0xFFFFFFFF, n_samples, float(eta),
+                                         _ptr(codes), _ptr(codes_t), _ptr(state), _ptr(alpha), _ptr(maxabs),
+                                         _ptr(ws), ws.numel(), _stream(dev))
+    _check(st, "luq_quantize_grad_hindsight")
     return codes, codes_t, alpha, maxabs
 
 

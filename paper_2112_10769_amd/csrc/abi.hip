@@ -105,6 +105,37 @@ luq_status luq_quantize_grad(const void* g, luq_dtype dt, int64_t rows, int64_t 
                                              static_cast<hipStream_t>(stream)));
 }
 
+luq_status luq_quantize_grad_hindsight(const void* g, luq_dtype dt, int64_t rows, int64_t cols, int R,
+                                       uint64_t seed, uint32_t counter, int n_samples, float eta,
+                                       uint8_t* codes, uint8_t* codes_t, float* state, float* alpha,
+                                       float* maxabs, void* ws, size_t ws_bytes, void* stream) {
+  const char* fn = "luq_quantize_grad_hindsight";
+  g_last_error[0] = 0;
+  if (dt != LUQ_F32 && dt != LUQ_BF16) return fail(LUQ_ERR_DTYPE, "%s: dtype", fn);
+  luq_status st = check_matrix(rows, cols, codes_t != nullptr, fn);
+  if (st != LUQ_OK) return st;
+  if (R < 4 || R > 6) return fail(LUQ_ERR_PARAM, "%s: R must be 4, 5 or 6", fn);
+  if (n_samples != 1 && n_samples != 2) return fail(LUQ_ERR_PARAM, "%s: n_samples must be 1 or 2", fn);
+  if (n_samples == 2 && R > 5) return fail(LUQ_ERR_PARAM, "%s: n_samples = 2 needs R <= 5", fn);
+  if (!(eta >= 0.0f && eta <= 1.0f)) return fail(LUQ_ERR_PARAM, "%s: eta must be in [0, 1]", fn);
+  if (!alpha) return fail(LUQ_ERR_NULL, "%s: alpha is NULL", fn);
+  if (!state) return fail(LUQ_ERR_NULL, "%s: state is NULL", fn);
+  const int64_t n = rows * cols;
+  if (n > 0) {
+    if (!g) return fail(LUQ_ERR_NULL, "%s: g is NULL", fn);
+    if (!codes && !codes_t) return fail(LUQ_ERR_NULL, "%s: no code output", fn);
+    if (!ws || ws_bytes < luq_workspace_size(LUQ_OP_QUANTIZE_GRAD, n, 0, 0))
+      return fail(LUQ_ERR_WORKSPACE, "%s: workspace too small", fn);
+    if (!aligned16(g) || !aligned16(codes) || !aligned16(codes_t) || !aligned16(ws))
+      return fail(LUQ_ERR_ALIGN, "%s: g, codes, codes_t and ws must be 16-byte aligned", fn);
+  }
+  if (!aligned4(alpha) || !aligned4(maxabs) || !aligned4(state))
+    return fail(LUQ_ERR_ALIGN, "%s: alpha / maxabs / state misaligned", fn);
+  return hip_status(luq::launch_luq_quantize_hindsight(g, dt == LUQ_BF16, rows, cols, R, seed, counter, n_samples,
+                                                       eta, codes, codes_t, state, alpha, maxabs, ws,
+                                                       static_cast<hipStream_t>(stream)));
+}
+
 luq_status int4_quantize(const void* x, luq_dtype dt, int64_t rows, int64_t cols, int is_signed,
                          float clip, uint8_t* codes, uint8_t* codes_t, float* scale, void* ws,
                          size_t ws_bytes, void* stream) {

@@ -21,6 +21,11 @@ hipError_t launch_luq_quantize(const void* g, int bf16, int64_t rows, int64_t co
                                uint8_t* codes_t, float* alpha, float* maxabs, void* ws,
                                hipStream_t st);
 
+hipError_t launch_luq_quantize_hindsight(const void* g, int bf16, int64_t rows, int64_t cols, int R,
+                                         uint64_t seed, uint32_t counter, int ns, float eta, uint8_t* codes,
+                                         uint8_t* codes_t, float* state, float* alpha, float* maxabs, void* ws,
+                                         hipStream_t st);
+
 hipError_t launch_int4_quantize(const void* x, int bf16, int64_t rows, int64_t cols, int is_signed,
                                 float clip, uint8_t* codes, uint8_t* codes_t, float* scale,
                                 void* ws, hipStream_t st);

@@ -44,6 +44,14 @@ __device__ __forceinline__ uint32_t max_key(uint32_t b) {
   return (a >= 0x7F800000u) ? a : ((b >> 31) ? 0u : b);
 }
 
+// Max key |x| over 8 elements.
+__device__ __forceinline__ uint32_t max_key8(const U8& v) {
+  uint32_t m = v.v[0] & 0x7FFFFFFFu;
+#pragma unroll
+  for (int e = 1; e < 8; ++e) m = max(m, v.v[e] & 0x7FFFFFFFu);
+  return m;
+}
+
 template <bool BF16, int MODE, bool NT>
 __global__ __launch_bounds__(kThreads) void max_partial_kernel(const void* __restrict__ x, int64_t n,
                                                               uint32_t* __restrict__ partial) {
@@ -120,7 +128,7 @@ constexpr int kTilePad = 4;  // LDS words between column groups (keeps 16-byte a
 template <int NS, typename Enc>
 __device__ __forceinline__ void encode_tiles(const Enc& enc, int64_t rows, int64_t cols, int lg,
                                              int lt, uint8_t* codes, uint8_t* codes_t,
-                                             int64_t plane, uint32_t* lds) {
+                                             int64_t plane, uint32_t* lds, uint32_t& mx) {
   const int tw = 1 << lt, tg = 1 << lg, tr = tw >> lg, pitch = tr + kTilePad;
   const int64_t cgs = cols >> 3;
   const int64_t ntr = (rows + tr - 1) / tr, ntc = (cgs + tg - 1) / tg;
@@ -142,7 +150,10 @@ __device__ __forceinline__ void encode_tiles(const Enc& enc, int64_t rows, int64
         const int64_t row = r0 + r[u], cg = g0 + g[u];
         ok[u] = row < rows && cg < cgs;
         e0[u] = row * cols + cg * 8;
-        if (ok[u]) v[u] = enc.load(e0[u]);
+        if (ok[u]) {
+          v[u] = enc.load(e0[u]);
+          if constexpr (Enc::kTrack) mx = max(mx, max_key8(v[u]));
+        }
       }
 #pragma unroll
       for (int u = 0; u < U; ++u) {
@@ -235,8 +246,10 @@ __device__ __forceinline__ LuqParams luq_params(uint32_t mbits, int R, float* al
 // is exact.  The field is max(n, -1) + 1 + up.  Unscaled, |x| <= max =
 // alpha * 2^R exactly, so n <= R and at n = R the offset d is 0 and `up` is
 // false: the field never exceeds R + 1.  Scaled, alpha may have been rounded
-// (subnormal alpha), so the field is capped at R + 1.
-template <bool SCALED>
+// (subnormal alpha), and with an estimated maximum (CAP) magnitudes, Inf and
+// NaN may lie above the top level, so the field is capped at R + 1 (the top
+// code, with the element's sign).
+template <bool SCALED, bool CAP = false>
 __device__ __forceinline__ uint32_t luq_field(uint32_t b, uint32_t j, const LuqParams& p) {
   const float mag = fabsf(__uint_as_float(b));
   const float as = SCALED ? mag * p.S : mag;
@@ -246,7 +259,7 @@ __device__ __forceinline__ uint32_t luq_field(uint32_t b, uint32_t j, const LuqP
   const float c = fmaf(w16, su ? 0.0f : 0x1p16f, -as);  // lo - |x|, exact
   const bool up = fmaf((float)j, w16, c) < 0.0f;
   const int32_t f = max(n, -1) + 1 + (int32_t)up;
-  return (uint32_t)(SCALED ? min(f, (int32_t)p.top_field) : f);
+  return (uint32_t)(SCALED || CAP ? min(f, (int32_t)p.top_field) : f);
 }
 
 // Sign bits of 8 elements at the sign position of their nibbles (bit 4e+3):
@@ -264,7 +277,7 @@ __device__ __forceinline__ uint32_t gather_signs(const U8& v) {
 // Codes of 8 consecutive elements (bits in v) for Philox block `blk`: the
 // exponent fields are packed first, then each sign bit is set where its field
 // is non-zero (zero is always +0).
-template <bool SCALED>
+template <bool SCALED, bool CAP = false>
 __device__ __forceinline__ uint32_t luq_word(const U8& v, uint64_t blk, uint32_t sample,
                                              uint32_t counter, uint32_t k0, uint32_t k1,
                                              const LuqParams& p) {
@@ -274,7 +287,7 @@ __device__ __forceinline__ uint32_t luq_word(const U8& v, uint64_t blk, uint32_t
 #pragma unroll
   for (int e = 0; e < 8; ++e) {
     const uint32_t j = (e & 1) ? (w[e >> 1] >> 16) : (w[e >> 1] & 0xFFFFu);
-    fields |= luq_field<SCALED>(v.v[e], j, p) << (4 * e);
+    fields |= luq_field<SCALED, CAP>(v.v[e], j, p) << (4 * e);
   }
   const uint32_t nz = (fields | (fields >> 1) | (fields >> 2)) & 0x11111111u;
   return fields | (gather_signs(v) & (nz << 3));
@@ -292,14 +305,26 @@ struct LuqArgs {
   int64_t plane;
   float* alpha_out;
   float* max_out;
+  // in-hindsight mode: the estimate read at the start, and one partial
+  // maximum per encode block written at the end
+  const float* state;
+  uint32_t* part_out;
 };
 
+// Key of the in-hindsight estimate: NaN stays NaN, anything not positive is 0.
+__device__ __forceinline__ uint32_t estimate_key(float m) {
+  return m != m ? 0x7FC00000u : (m > 0.0f ? __float_as_uint(m) : 0u);
+}
+
+// HS (in-hindsight): alpha comes from the estimate; the fold kernel that
+// runs after the encode writes alpha and the measured maximum.
+template <bool HS = false>
 __device__ __forceinline__ LuqParams luq_block_params(const LuqArgs& a) {
   __shared__ uint32_t scratch[kThreads / kWave];
-  const uint32_t mbits = reduce_partials(a.partial, a.nparts, scratch);
+  const uint32_t mbits = HS ? estimate_key(*a.state) : reduce_partials(a.partial, a.nparts, scratch);
   float alpha;
   const LuqParams p = luq_params(mbits, a.R, &alpha);
-  if (blockIdx.x == 0 && threadIdx.x == 0) {
+  if (!HS && blockIdx.x == 0 && threadIdx.x == 0) {
     *a.alpha_out = alpha;
     if (a.max_out) *a.max_out = __uint_as_float(mbits);
   }
@@ -307,8 +332,10 @@ __device__ __forceinline__ LuqParams luq_block_params(const LuqArgs& a) {
 }
 
 // Flat row-major codes; groups of 8 elements along the flattened tensor.
-template <bool BF16, bool NT, int NS, bool SCALED>
-__device__ __forceinline__ void luq_flat_body(const LuqArgs& a, const LuqParams& p) {
+// With HS the fields are capped and the thread's max key is returned.
+template <bool BF16, bool NT, int NS, bool SCALED, bool HS = false>
+__device__ __forceinline__ uint32_t luq_flat_body(const LuqArgs& a, const LuqParams& p) {
+  uint32_t mx = 0;
   const int64_t nfull = a.n >> 3;
   const int64_t stride = (int64_t)gridDim.x * kThreads;
   int64_t g = (int64_t)blockIdx.x * kThreads + threadIdx.x;
@@ -316,64 +343,112 @@ __device__ __forceinline__ void luq_flat_body(const LuqArgs& a, const LuqParams&
   for (; g + stride < nfull; g += 2 * stride) {
     const U8 v0 = load8<BF16, NT>(a.g, g * 8);
     const U8 v1 = load8<BF16, NT>(a.g, (g + stride) * 8);
+    if (HS) mx = max(mx, max(max_key8(v0), max_key8(v1)));
 #pragma unroll
     for (int s = 0; s < NS; ++s) {
       *reinterpret_cast<uint32_t*>(a.codes + s * a.plane + g * 4) =
-          luq_word<SCALED>(v0, (uint64_t)g, s, a.counter, a.k0, a.k1, p);
+          luq_word<SCALED, HS>(v0, (uint64_t)g, s, a.counter, a.k0, a.k1, p);
       *reinterpret_cast<uint32_t*>(a.codes + s * a.plane + (g + stride) * 4) =
-          luq_word<SCALED>(v1, (uint64_t)(g + stride), s, a.counter, a.k0, a.k1, p);
+          luq_word<SCALED, HS>(v1, (uint64_t)(g + stride), s, a.counter, a.k0, a.k1, p);
     }
   }
   if (g < nfull) {
     const U8 v = load8<BF16, NT>(a.g, g * 8);
+    if (HS) mx = max(mx, max_key8(v));
 #pragma unroll
     for (int s = 0; s < NS; ++s)
       *reinterpret_cast<uint32_t*>(a.codes + s * a.plane + g * 4) =
-          luq_word<SCALED>(v, (uint64_t)g, s, a.counter, a.k0, a.k1, p);
+          luq_word<SCALED, HS>(v, (uint64_t)g, s, a.counter, a.k0, a.k1, p);
   }
   if ((a.n & 7) && blockIdx.x == 0 && threadIdx.x == 0) {
-    const U8 v = load8_tail<BF16>(a.g, nfull * 8, a.n);
+    const U8 v = load8_tail<BF16>(a.g, nfull * 8, a.n);  // missing elements read +0
+    if (HS) mx = max(mx, max_key8(v));
 #pragma unroll
     for (int s = 0; s < NS; ++s)
       store_bytes(a.codes + s * a.plane + nfull * 4,
-                  luq_word<SCALED>(v, (uint64_t)nfull, s, a.counter, a.k0, a.k1, p),
+                  luq_word<SCALED, HS>(v, (uint64_t)nfull, s, a.counter, a.k0, a.k1, p),
                   (int)(((a.n & 7) + 1) >> 1));
   }
+  return mx;
 }
 
-template <bool BF16, bool NT, int NS>
+// Max key over the groups a flat-encode thread owns (in-hindsight mode with
+// all codes 0: the measurement still covers the whole tensor).
+template <bool BF16, bool NT>
+__device__ __forceinline__ uint32_t flat_max_only(const LuqArgs& a) {
+  uint32_t mx = 0;
+  const int64_t nfull = a.n >> 3;
+  for (int64_t g = (int64_t)blockIdx.x * kThreads + threadIdx.x; g < nfull; g += (int64_t)gridDim.x * kThreads)
+    mx = max(mx, max_key8(load8<BF16, NT>(a.g, g * 8)));
+  if ((a.n & 7) && blockIdx.x == 0 && threadIdx.x == 0) mx = max(mx, max_key8(load8_tail<BF16>(a.g, nfull * 8, a.n)));
+  return mx;
+}
+
+// One partial maximum per block (in-hindsight mode).
+__device__ __forceinline__ void write_block_max(uint32_t mx, uint32_t* part_out) {
+  __shared__ uint32_t scratch[kThreads / kWave];
+  const uint32_t m = block_max_u32(mx, scratch);
+  if (threadIdx.x == 0) part_out[blockIdx.x] = m;
+}
+
+template <bool BF16, bool NT, int NS, bool HS = false>
 __global__ __launch_bounds__(kThreads) void luq_encode_flat_kernel(LuqArgs a) {
-  const LuqParams p = luq_block_params(a);
+  const LuqParams p = luq_block_params<HS>(a);
   if (p.zero) {  // alpha is 0 or NaN: every code is 0
     const int64_t nbytes = (a.n + 1) >> 1;
     for (int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x; i < nbytes; i += (int64_t)gridDim.x * kThreads)
       for (int s = 0; s < NS; ++s) a.codes[s * a.plane + i] = 0;
+    if (HS) write_block_max(flat_max_only<BF16, NT>(a), a.part_out);
     return;
   }
-  if (p.S != 1.0f)
-    luq_flat_body<BF16, NT, NS, true>(a, p);
-  else
-    luq_flat_body<BF16, NT, NS, false>(a, p);
+  const uint32_t mx = p.S != 1.0f ? luq_flat_body<BF16, NT, NS, true, HS>(a, p)
+                                  : luq_flat_body<BF16, NT, NS, false, HS>(a, p);
+  if (HS) write_block_max(mx, a.part_out);
 }
 
-template <bool BF16, bool NT, bool SCALED>
+template <bool BF16, bool NT, bool SCALED, bool HS = false>
 struct LuqEnc {
+  static constexpr bool kTrack = HS;
   const LuqArgs* a;
   const LuqParams* p;
   __device__ U8 load(int64_t e0) const { return load8<BF16, NT>(a->g, e0); }
   __device__ uint32_t word(const U8& v, uint64_t blk, int s) const {
-    return p->zero ? 0u : luq_word<SCALED>(v, blk, s, a->counter, a->k0, a->k1, *p);
+    return p->zero ? 0u : luq_word<SCALED, HS>(v, blk, s, a->counter, a->k0, a->k1, *p);
   }
 };
 
-template <bool BF16, bool NT, int NS>
+template <bool BF16, bool NT, int NS, bool HS = false>
 __global__ __launch_bounds__(kThreads) void luq_encode_tile_kernel(LuqArgs a, int lg, int lt) {
   __shared__ __attribute__((aligned(16))) uint32_t lds[NS * ((1 << kLuqTileLg) + 32 * kTilePad)];
-  const LuqParams p = luq_block_params(a);
+  const LuqParams p = luq_block_params<HS>(a);
+  uint32_t mx = 0;
   if (p.S != 1.0f)
-    encode_tiles<NS>(LuqEnc<BF16, NT, true>{&a, &p}, a.rows, a.cols, lg, lt, a.codes, a.codes_t, a.plane, lds);
+    encode_tiles<NS>(LuqEnc<BF16, NT, true, HS>{&a, &p}, a.rows, a.cols, lg, lt, a.codes, a.codes_t, a.plane,
+                     lds, mx);
   else
-    encode_tiles<NS>(LuqEnc<BF16, NT, false>{&a, &p}, a.rows, a.cols, lg, lt, a.codes, a.codes_t, a.plane, lds);
+    encode_tiles<NS>(LuqEnc<BF16, NT, false, HS>{&a, &p}, a.rows, a.cols, lg, lt, a.codes, a.codes_t, a.plane,
+                     lds, mx);
+  if (HS) write_block_max(mx, a.part_out);
+}
+
+// In-hindsight fold, after the encode: the measured maximum (from the encode
+// blocks' partials), alpha of this step (from the estimate the encode read)
+// and the next estimate, Eq. hindsight: m' = fl32(fl32(c1 max) + fl32(c0 m))
+// with c1 = fl32(1 - eta), c0 = eta.
+__global__ __launch_bounds__(1024) void hindsight_fold_kernel(const uint32_t* __restrict__ part, int nparts,
+                                                             float* state, float c1, float c0, int R,
+                                                             float* alpha_out, float* maxabs_out) {
+  __shared__ uint32_t scratch[1024 / kWave];
+  const uint32_t m = reduce_partials(part, nparts, scratch);
+  if (threadIdx.x == 0) {
+    const uint32_t mkey = estimate_key(*state);
+    float alpha;
+    (void)luq_params(mkey, R, &alpha);
+    const float mx = __uint_as_float(m);
+    *alpha_out = alpha;
+    if (maxabs_out) *maxabs_out = mx;
+    *state = __fadd_rn(__fmul_rn(c1, mx), __fmul_rn(c0, __uint_as_float(mkey)));
+  }
 }
 
 __global__ void write_two_floats_kernel(float* a, float va, float* b, float vb) {
@@ -466,6 +541,7 @@ __global__ __launch_bounds__(kThreads) void int4_encode_flat_kernel(Int4Args a) 
 
 template <bool BF16, bool NT>
 struct Int4Enc {
+  static constexpr bool kTrack = false;
   const Int4Args* a;
   const Int4Params* p;
   __device__ U8 load(int64_t e0) const { return load8<BF16, NT>(a->x, e0); }
@@ -476,7 +552,8 @@ template <bool BF16, bool NT>
 __global__ __launch_bounds__(kThreads) void int4_encode_tile_kernel(Int4Args a, int lg, int lt) {
   __shared__ __attribute__((aligned(16))) uint32_t lds[(1 << kInt4TileLg) + 32 * kTilePad];
   const Int4Params p = int4_block_params(a);
-  encode_tiles<1>(Int4Enc<BF16, NT>{&a, &p}, a.rows, a.cols, lg, lt, a.codes, a.codes_t, 0, lds);
+  uint32_t unused = 0;
+  encode_tiles<1>(Int4Enc<BF16, NT>{&a, &p}, a.rows, a.cols, lg, lt, a.codes, a.codes_t, 0, lds, unused);
 }
 
 // ------------------------------- launchers ---------------------------------
@@ -613,6 +690,60 @@ hipError_t launch_luq_quantize(const void* g, int bf16, int64_t rows, int64_t co
   a.alpha_out = alpha;
   a.max_out = maxabs;
   return bf16 ? luq_launch_t<true>(a, ns, a.nparts, st) : luq_launch_t<false>(a, ns, a.nparts, st);
+}
+
+template <bool BF16, bool NT>
+static int luq_hindsight_encode(const LuqArgs& a, int ns, hipStream_t st) {
+  if (a.codes_t) {
+    const TileShape t = tile_shape(a.rows, a.cols, kLuqTileLg);
+    if (ns == 1)
+      hipLaunchKernelGGL((luq_encode_tile_kernel<BF16, NT, 1, true>), dim3(t.blocks), dim3(kThreads), 0, st, a, t.lg,
+                         t.lt);
+    else
+      hipLaunchKernelGGL((luq_encode_tile_kernel<BF16, NT, 2, true>), dim3(t.blocks), dim3(kThreads), 0, st, a, t.lg,
+                         t.lt);
+    return t.blocks;
+  }
+  const int nb = encode_blocks_flat(a.n);
+  if (ns == 1)
+    hipLaunchKernelGGL((luq_encode_flat_kernel<BF16, NT, 1, true>), dim3(nb), dim3(kThreads), 0, st, a);
+  else
+    hipLaunchKernelGGL((luq_encode_flat_kernel<BF16, NT, 2, true>), dim3(nb), dim3(kThreads), 0, st, a);
+  return nb;
+}
+
+hipError_t launch_luq_quantize_hindsight(const void* g, int bf16, int64_t rows, int64_t cols, int R,
+                                         uint64_t seed, uint32_t counter, int ns, float eta, uint8_t* codes,
+                                         uint8_t* codes_t, float* state, float* alpha, float* maxabs, void* ws,
+                                         hipStream_t st) {
+  const int64_t n = rows * cols;
+  LuqArgs a;
+  a.g = g;
+  a.rows = rows;
+  a.cols = cols;
+  a.n = n;
+  a.R = R;
+  a.k0 = (uint32_t)seed;
+  a.k1 = (uint32_t)(seed >> 32);
+  a.counter = counter;
+  a.partial = nullptr;
+  a.nparts = 0;
+  a.codes = codes;
+  a.codes_t = codes_t;
+  a.plane = (int64_t)plane_bytes(n);
+  a.alpha_out = alpha;
+  a.max_out = maxabs;
+  a.state = state;
+  a.part_out = static_cast<uint32_t*>(ws);
+  int nblocks = 0;
+  if (n > 0) {
+    const bool nt = stream_reads(n, bf16 != 0);
+    nblocks = bf16 ? (nt ? luq_hindsight_encode<true, true>(a, ns, st) : luq_hindsight_encode<true, false>(a, ns, st))
+                   : (nt ? luq_hindsight_encode<false, true>(a, ns, st) : luq_hindsight_encode<false, false>(a, ns, st));
+  }
+  hipLaunchKernelGGL(hindsight_fold_kernel, dim3(1), dim3(1024), 0, st, a.part_out, nblocks, state,
+                     1.0f - eta, eta, R, alpha, maxabs);  // c1 = fl32(1 - eta) (host float arithmetic)
+  return hipGetLastError();
 }
 
 template <bool BF16>

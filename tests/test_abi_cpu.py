@@ -32,7 +32,7 @@ def _declared():
 
 def test_every_declared_function_is_exported():
     names = _declared()
-    assert len(names) == 10, names
+    assert len(names) == 11, names
     for n in names:
         assert hasattr(LIB, n), n
     assert set(names) == set(luq.EXPORTS)
@@ -90,6 +90,28 @@ def _qg(**kw):
 ])
 def test_quantize_grad_validation(kw, status):
     assert _qg(**kw) == status
+    assert LIB.luq_last_error()
+
+
+def _hs(**kw):
+    a = dict(g=P, dt=0, rows=4, cols=8, R=4, seed=0, counter=0, ns=1, eta=0.1, codes=P2, codes_t=NUL,
+             state=P3, alpha=P3, maxabs=NUL, ws=P, ws_bytes=WS)
+    a.update(kw)
+    return LIB.luq_quantize_grad_hindsight(a["g"], a["dt"], a["rows"], a["cols"], a["R"], a["seed"],
+                                           a["counter"], a["ns"], a["eta"], a["codes"], a["codes_t"], a["state"],
+                                           a["alpha"], a["maxabs"], a["ws"], a["ws_bytes"], None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(dt=2), 3), (dict(rows=3, cols=7), 2), (dict(rows=12, cols=8, codes_t=P2), 2),
+    (dict(R=7), 4), (dict(ns=2, R=6), 4),
+    (dict(eta=-0.1), 4), (dict(eta=1.5), 4), (dict(eta=float("nan")), 4),
+    (dict(state=NUL), 1), (dict(alpha=NUL), 1), (dict(g=NUL), 1), (dict(codes=NUL, codes_t=NUL), 1),
+    (dict(ws=NUL), 5), (dict(ws_bytes=16), 5), (dict(g=PMIS), 6),
+    (dict(state=ctypes.c_void_p(0x10002)), 6),
+])
+def test_quantize_grad_hindsight_validation(kw, status):
+    assert _hs(**kw) == status
     assert LIB.luq_last_error()
 
 
