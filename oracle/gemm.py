@@ -1,7 +1,9 @@
-"""Backward and update GEMMs on 4-bit codes -- oracle.
+"""The three 4-bit GEMMs on codes -- oracle.
 
-Test infrastructure only.  Eq. backward and Eq. update of the paper:
+Test infrastructure only.  Eq. forward, Eq. backward and Eq. update of the
+paper:
 
+    z_l       = Q_INT(W_l) Q_INT(a_{l-1})   (fwd, here y = Q(x) Q(W)^T)
     g_{l-1}   = Q_INT(W^T) Q_FP(delta)      (dgrad, here dX = Q(g) Q(W))
     dC/dW_l   = Q_FP(delta) Q_INT(a^T)      (wgrad, here dW = Q(g)^T Q(a))
 
@@ -14,6 +16,8 @@ matrix multiply (every partial sum is an integer far below 2^53) and
 multiplies by the scales in float64.
 
 Layouts (row-major, two codes per byte along the row):
+  fwd:   X [M, K] (tokens x input features), W [N, K] (the [out, in]
+         weight); y [M, N].
   dgrad: G [M, K] (K = output features), W [K, N] (the [out, in] weight);
          dX [M, N].
   wgrad: G [T, Nout], A [T, Kin]; dW [Nout, Kin].
@@ -93,6 +97,21 @@ def gemm_wgrad_ref(g_planes, alpha, a_codes, a_scale, a_signed, T, Nout, Kin, ro
     X = _rows_int4(a_codes, ts, Kin, a_signed)         # [T', Kin]
     ref, absref = _matmul_exact(G.T, X)
     sc = _scale(alpha, n_s, a_scale)
+    return ref * sc, absref * abs(sc)
+
+
+def gemm_fwd_ref(x_codes, x_scale, x_signed, w_codes, w_scale, w_signed, M, N, K, rows=None):
+    """y[m, n] = (s_x s_W) sum_k q_x[m, k] q_W[n, k] (Appendix A.1: the
+    scales of the two INT4 tensors leave the sum, every MAC is on codes).
+
+    rows: optional subset of output rows (all rows if None).
+    Returns (ref, absref) as float64 arrays of shape (len(rows), N).
+    """
+    rows = np.arange(M) if rows is None else np.asarray(rows)
+    X = _rows_int4(x_codes, rows, K, x_signed)         # [len(rows), K]
+    Wm = _rows_int4(w_codes, np.arange(N), K, w_signed)  # [N, K]
+    ref, absref = _matmul_exact(X, Wm.T)
+    sc = float(x_scale) * float(w_scale)
     return ref * sc, absref * abs(sc)
 
 

@@ -4,6 +4,10 @@ The backward / update products are pinned by a pure-Python triple loop over
 codes decoded from the bit layout directly (not through the oracle's
 decoders), by the MF-BPROP worked example of Appendix A.8.1 (FP4 field 011
 times INT4 3 is 12), and by the linearity of SMP averaging (Section 5.1).
+The forward product (Eq. forward, Appendix A.1) is pinned by the same kind
+of triple loop, by closed forms on constant codes, and by the round-to-
+nearest error bound: |Q(x)_k - x_k| <= s_x / 2 and |Q(w)_k - w_k| <= s_W / 2
+bound |y - x W^T| per output.
 """
 import numpy as np
 import pytest
@@ -11,7 +15,7 @@ import pytest
 import synth
 from oracle.luq import luq_quantize
 from oracle.int4 import int4_quantize
-from oracle.gemm import gemm_dgrad_ref, gemm_wgrad_ref
+from oracle.gemm import gemm_dgrad_ref, gemm_wgrad_ref, gemm_fwd_ref
 
 
 def _nib(codes, i):
@@ -104,3 +108,65 @@ def test_smp_gemm_is_mean_of_single_plane_gemms():
     p0, _ = gemm_dgrad_ref(planes[0], alpha, wc, ws, True, M, N, K)
     p1, _ = gemm_dgrad_ref(planes[1], alpha, wc, ws, True, M, N, K)
     assert np.allclose(both, 0.5 * (p0 + p1), rtol=1e-15, atol=0)
+
+
+def _loop_fwd(xc, xs, xsig, wc, ws, wsig, M, N, K):
+    out = np.zeros((M, N))
+    for m in range(M):
+        for n in range(N):
+            acc = 0
+            for k in range(K):
+                acc += _int4_val(_nib(xc, m * K + k), xsig) * _int4_val(_nib(wc, n * K + k), wsig)
+            out[m, n] = acc * float(xs) * float(ws)
+    return out
+
+
+@pytest.mark.parametrize("xsig,wsig", [(True, True), (False, True), (True, False), (False, False)])
+def test_fwd_matches_triple_loop(xsig, wsig):
+    M, N, K = 5, 7, 10
+    x = synth.normal((M, K), 1.0, [43, 1])
+    w = synth.normal((N, K), 0.5, [43, 2])
+    xc, xs = int4_quantize(x if xsig else np.abs(x), is_signed=xsig)
+    wc, ws = int4_quantize(w if wsig else np.abs(w), is_signed=wsig)
+    ref, absref = gemm_fwd_ref(xc, xs, xsig, wc, ws, wsig, M, N, K)
+    assert np.array_equal(ref, _loop_fwd(xc, xs, xsig, wc, ws, wsig, M, N, K))
+    assert np.all(absref >= np.abs(ref))
+    sub, _ = gemm_fwd_ref(xc, xs, xsig, wc, ws, wsig, M, N, K, rows=[4, 0])
+    assert np.array_equal(sub, ref[[4, 0]])
+
+
+def test_fwd_closed_forms():
+    K = 6
+    # every code 7 (signed) / 15 (unsigned): y = 49 K s_x s_W and 105 K s_x s_W
+    x7 = np.full((2 * K + 1) // 2, 0x77, np.uint8)
+    ref, _ = gemm_fwd_ref(x7, np.float32(0.5), True, x7, np.float32(0.25), True, 1, 1, K)
+    assert ref[0, 0] == 49 * K * 0.125
+    xf = np.full(K // 2, 0xFF, np.uint8)
+    ref, _ = gemm_fwd_ref(xf, np.float32(1), False, x7, np.float32(1), True, 1, 1, K)
+    assert ref[0, 0] == 105 * K
+    # the signed code 0xF is -1, unsigned 15
+    ref, _ = gemm_fwd_ref(xf, np.float32(1), True, x7, np.float32(1), True, 1, 1, K)
+    assert ref[0, 0] == -7 * K
+    # a ReLU-like row against alternating +-7 weights cancels pairwise
+    alt = np.full(K // 2, 0x97, np.uint8)   # codes 7, -7, 7, -7, ...
+    ref, _ = gemm_fwd_ref(xf, np.float32(1), False, alt, np.float32(1), True, 1, 1, K)
+    assert ref[0, 0] == 0
+
+
+@pytest.mark.parametrize("xsig", [True, False])
+def test_fwd_within_rounding_error_of_the_float_product(xsig):
+    M, N, K = 24, 16, 96
+    x = synth.normal((M, K), 1.0, [44, 1])
+    if not xsig:
+        x = np.maximum(x, 0)
+    w = synth.normal((N, K), 0.05, [44, 2])
+    xc, xs = int4_quantize(x, is_signed=xsig)
+    wc, ws = int4_quantize(w, is_signed=True)
+    ref, _ = gemm_fwd_ref(xc, xs, xsig, wc, ws, True, M, N, K)
+    exact = x.astype(np.float64) @ w.astype(np.float64).T
+    dx, dw = float(xs) / 2 * (1 + 1e-6), float(ws) / 2 * (1 + 1e-6)
+    bound = (np.abs(x) @ np.full((K, N), dw) + np.full((M, K), dx) @ np.abs(w).T.astype(np.float64)
+             + K * dx * dw)
+    assert np.all(np.abs(ref - exact) <= bound)
+    # and the bound is not vacuous: the product is far from zero on average
+    assert np.mean(np.abs(ref - exact)) < 0.25 * np.mean(np.abs(exact))

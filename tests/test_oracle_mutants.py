@@ -137,3 +137,55 @@ def test_transposed_operand_is_caught():
     good, _ = gemm_dgrad_ref(planes, alpha, wc, ws, True, M, N, K)
     bad, _ = gemm_dgrad_ref(planes, alpha, wt, ws, True, M, N, K)
     assert not np.allclose(good, bad)
+
+
+def _fwd_pin_fails():
+    """The forward pins (rounding bound against the float product, and the
+    closed form 49 K s_x s_W) against the current oracle.gemm."""
+    import oracle.gemm as G
+    fails = []
+    M, N, K = 12, 10, 64
+    x = synth.normal((M, K), 1.0, [51, 1])
+    w = synth.normal((N, K), 0.1, [51, 2])
+    xc, xs = int4_quantize(x, is_signed=True)
+    wc, ws = int4_quantize(w, is_signed=True)
+    ref, _ = G.gemm_fwd_ref(xc, xs, True, wc, ws, True, M, N, K)
+    exact = x.astype(np.float64) @ w.astype(np.float64).T
+    dx, dw = float(xs) / 2 * (1 + 1e-6), float(ws) / 2 * (1 + 1e-6)
+    bound = np.abs(x) @ np.full((K, N), dw) + np.full((M, K), dx) @ np.abs(w).T.astype(np.float64) + K * dx * dw
+    if not np.all(np.abs(ref - exact) <= bound):
+        fails.append("bound")
+    x7 = np.full(K // 2, 0x77, np.uint8)
+    r7, _ = G.gemm_fwd_ref(x7, np.float32(0.5), True, x7, np.float32(0.25), True, 1, 1, K)
+    if r7[0, 0] != 49 * K * 0.125:
+        fails.append("closed")
+    # triple loop over nibbles read from the bytes directly
+    m, n, k = 3, 4, 6
+    xb, wb = xc[: m * k // 2], wc[: n * k // 2]
+    nib = lambda c, i: (int(c[i // 2]) >> (4 * (i & 1))) & 15
+    val = lambda v: v - 16 if v >= 8 else v
+    loop = [[sum(val(nib(xb, a * k + t)) * val(nib(wb, b * k + t)) for t in range(k)) * float(xs) * float(ws)
+             for b in range(n)] for a in range(m)]
+    small, _ = G.gemm_fwd_ref(xb, xs, True, wb, ws, True, m, n, k)
+    if not np.array_equal(small, np.array(loop)):
+        fails.append("loop")
+    return fails
+
+
+def test_fwd_mutants_are_caught(monkeypatch):
+    import oracle.gemm as G
+    assert _fwd_pin_fails() == []
+    good_rows = G._rows_int4
+    # lost sign extension: signed codes decoded as unsigned
+    monkeypatch.setattr(G, "_rows_int4", lambda c, r, n, signed: good_rows(c, r, n, False))
+    assert _fwd_pin_fails()
+    monkeypatch.setattr(G, "_rows_int4", good_rows)
+    # reduction index reversed on one operand
+    good_mm = G._matmul_exact
+    monkeypatch.setattr(G, "_matmul_exact", lambda A, B: good_mm(A, B[::-1]))
+    assert "loop" in _fwd_pin_fails()
+    monkeypatch.setattr(G, "_matmul_exact", good_mm)
+    # the weight scale dropped
+    good_ref = G.gemm_fwd_ref
+    monkeypatch.setattr(G, "gemm_fwd_ref", lambda xc, xs, xsig, wc, ws, *a, **k: good_ref(xc, xs, xsig, wc, 1.0, *a, **k))
+    assert "closed" in _fwd_pin_fails()
