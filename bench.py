@@ -1,7 +1,7 @@
 """Benchmark of the LUQ 4-bit backward hot path on one MI355X.
 
     python bench.py [--gpus 1] [--steps K] [--warmup W]
-                    [--workload resnet|mlp|mlp_smp|small|luq_sweep]
+                    [--workload resnet|mlp|mlp_smp|mlp_fwd|small|luq_sweep]
 
 A step is one pass of the whole hot path over one batch of synthetic input,
 inputs resident in HBM:
@@ -16,6 +16,10 @@ measured step time, in percent.  Per-kernel GB/s and TOPS are listed too.
 `roofline` describes the dominant kernel, timed with HIP events on the
 stream it runs on; `cpu_baseline` times the CPU oracle on a bounded sample
 of the same workload.
+
+`--workload mlp_fwd` measures the forward pass of the same MLP layer instead:
+INT4 of the activations and of the weight (row-major codes) and the forward
+GEMM y = Q(x) Q(W)^T (Eq. forward).
 
 `--workload luq_sweep` measures the LUQ quantizer alone on 1-D gradients of
 2^20..2^30 elements (fp32 and bf16, lognormal magnitudes exp(N(-10, 3)),
@@ -36,6 +40,7 @@ sys.path.insert(0, ROOT)
 HBM_PEAK = 8.0e12      # bytes/s
 I8_PEAK = 5.0e15       # int8 dense ops/s
 METRIC = "LUQ quantize GB/s + 4-bit bwd GEMM TFLOP/s (as % of roofline), 1 MI355X"
+METRIC_FWD = "INT4 quantize GB/s + 4-bit fwd GEMM TFLOP/s (as % of roofline), 1 MI355X"
 
 
 def parse():
@@ -43,7 +48,7 @@ def parse():
     p.add_argument("--gpus", type=int, default=1)
     p.add_argument("--steps", type=int, default=20)
     p.add_argument("--warmup", type=int, default=5)
-    p.add_argument("--workload", default="resnet", choices=["resnet", "mlp", "mlp_smp", "small", "luq_sweep"])
+    p.add_argument("--workload", default="resnet", choices=["resnet", "mlp", "mlp_smp", "mlp_fwd", "small", "luq_sweep"])
     p.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     p.add_argument("--sweep-log2", default=None,
                    help="comma-separated log2 sizes for luq_sweep (default: 20,22,24,26..30)")
@@ -144,6 +149,34 @@ def build_mlp(L, torch, dev, ns=1, T=None, D=None, F=None, d=None):
                     dx=dx, dw=dw)
     cfg = {"workload": "transformer_mlp_bwd" + ("_smp2" if ns == 2 else ""), "tokens": T, "d_model": D,
            "hidden": F, "grad": "lognormal(-14,3) bf16", "R": 4, "n_samples": ns}
+    return stages, cfg, d
+
+
+def build_mlp_fwd(L, torch, dev, T=None, D=None, F=None, d=None):
+    """Forward of the MLP up-projection: y [T, F] = Q(x) Q(W)^T, x [T, D], W [F, D]."""
+    import synth
+    T = T or synth.MLP["T"]
+    D = D or synth.MLP["D"]
+    F = F or synth.MLP["F"]
+    d = dict(d) if d is not None else synth.mlp(T=T, D=D, F=F)
+    x = torch.from_numpy(d["x"].view("int16")).to(dev).view(torch.bfloat16)
+    w = torch.from_numpy(d["W"]).to(dev)
+    u8 = lambda n: torch.empty(int(n), dtype=torch.uint8, device=dev)
+    f32 = lambda *s: torch.empty(*s, dtype=torch.float32, device=dev)
+    xc, sx, wc, sw, y = u8(T * D // 2), f32(1), u8(F * D // 2), f32(1), f32(T, F)
+    wsx = u8(L.workspace_size(L.OP_INT4_QUANTIZE, T * D))
+    wsw = u8(L.workspace_size(L.OP_INT4_QUANTIZE, F * D))
+    wsf = u8(max(L.workspace_size(L.OP_GEMM_FWD, T, F, D), 1))
+    n_x, n_w = T * D, F * D
+    stages = [
+        Stage("int4_quantize(x)", lambda: L.int4_quantize(x, True, 0.0, xc, False, sx, wsx), 2 * 2 * n_x + n_x / 2),
+        Stage("int4_quantize(W)", lambda: L.int4_quantize(w, True, 0.0, wc, False, sw, wsw), 2 * 4 * n_w + n_w / 2),
+        Stage("int4_gemm_fwd", lambda: L.int4_gemm_fwd(xc, sx, True, wc, sw, True, T, F, D, y, wsf),
+              T * D / 2 + F * D / 2 + 4 * T * F, 2.0 * T * D * F),
+    ]
+    d["dev"] = dict(x=x, w=w, xc=xc, sx=sx, wc=wc, sw=sw, y=y)
+    cfg = {"workload": "transformer_mlp_fwd", "tokens": T, "d_model": D, "hidden": F,
+           "gemm_fwd_MNK": [T, F, D], "x": "N(0,1) bf16", "W": "N(0,0.02^2) fp32"}
     return stages, cfg, d
 
 
@@ -326,6 +359,25 @@ def cpu_baseline(workload, d):
             reps += 1
         sample = f"the whole step, {reps} times (last: " + ", ".join(parts) + ")"
         parts.clear()
+    elif workload == "mlp_fwd":
+        # INT4 on 2^20 elements and the forward GEMM on 64 token rows, repeated
+        # until at least 10 s of CPU work
+        n = 1 << 20
+        x = d["x"].reshape(-1)[:n]
+        F, D = d["W"].shape
+        rows = 64
+        xc, sx = oint4.int4_quantize(d["x"][:rows], dtype="bf16")
+        wc, ws = oint4.int4_quantize(d["W"], is_signed=True)             # [F, D] = [N, K]
+        reps = 0
+        while t_cpu < 10.0:
+            parts.clear()
+            timed("int4 2^20 bf16", lambda: oint4.int4_quantize(x, dtype="bf16"), 2 * 2 * n + n / 2)
+            timed(f"fwd {rows} rows", lambda: ogemm.gemm_fwd_ref(xc, sx, True, wc, ws, True, rows, F, D),
+                  rows * D / 2 + 4 * rows * F, 2.0 * rows * D * F)
+            reps += 1
+        sample = (f"INT4 on 2^20 elements, the forward GEMM on {rows} token rows, {reps} times (last: "
+                  + ", ".join(parts) + ")")
+        parts.clear()
     else:
         # LUQ and INT4 on 2^20 elements and dX on 64 token rows, repeated until
         # at least 10 s of CPU work
@@ -355,7 +407,8 @@ def cpu_baseline(workload, d):
 
 
 PROFILES = os.path.join(ROOT, "profiles")
-KERNEL_SOURCES = {"luq_gemm_dgrad": "gemm.hip", "luq_gemm_wgrad": "gemm.hip",
+KERNEL_SOURCES = {"luq_gemm_dgrad": "gemm_kernel.hpp", "luq_gemm_wgrad": "gemm_kernel.hpp",
+                  "int4_gemm_fwd": "gemm_kernel.hpp",
                   "luq_quantize_grad": "quant.hip", "int4_im2col3x3_t": "im2col.hip"}
 
 
@@ -412,6 +465,8 @@ def main():
         return
     if args.workload == "resnet":
         stages, cfg, d = build_resnet(L, torch, dev)
+    elif args.workload == "mlp_fwd":
+        stages, cfg, d = build_mlp_fwd(L, torch, dev)
     elif args.workload == "small":
         stages, cfg, d = build_mlp(L, torch, dev, 1, T=256, D=512, F=512)
         cfg["workload"] = "linear_256x512x512_bwd"
@@ -437,14 +492,15 @@ def main():
     roof["algorithmic_bytes"] = dom.bytes
     roof["launch_us"] = round(t * 1e6, 2)
     out = {
-        "metric": METRIC, "value": round(100.0 * roof_total / step_s, 2), "unit": "% of roofline",
+        "metric": METRIC_FWD if args.workload == "mlp_fwd" else METRIC,
+        "value": round(100.0 * roof_total / step_s, 2), "unit": "% of roofline",
         "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(step_s * 1e3, 4),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "i8",
         "data": "synthetic", "config": cfg, "roofline": roof, "kernels": kernels,
         "roofline_step_us": round(roof_total * 1e6, 2),
     }
     if not args.no_cpu:
-        out["cpu_baseline"] = cpu_baseline("resnet" if args.workload == "resnet" else "mlp", d)
+        out["cpu_baseline"] = cpu_baseline(args.workload if args.workload in ("resnet", "mlp_fwd") else "mlp", d)
     print(json.dumps(out), flush=True)
 
 

@@ -47,7 +47,7 @@
 extern "C" {
 #endif
 
-#define LUQ_ABI_VERSION 2
+#define LUQ_ABI_VERSION 3
 
 typedef int luq_status;
 enum {
@@ -68,7 +68,8 @@ enum {
   LUQ_OP_QUANTIZE_GRAD = 0, /* d0 = number of elements                     */
   LUQ_OP_INT4_QUANTIZE = 1, /* d0 = number of elements                     */
   LUQ_OP_GEMM_DGRAD = 2,    /* d0 = M, d1 = N, d2 = K                        */
-  LUQ_OP_GEMM_WGRAD = 3     /* d0 = T, d1 = Nout, d2 = Kin                   */
+  LUQ_OP_GEMM_WGRAD = 3,    /* d0 = T, d1 = Nout, d2 = Kin                   */
+  LUQ_OP_GEMM_FWD = 4       /* d0 = M, d1 = N, d2 = K                        */
 };
 
 /* ABI version of the loaded library (LUQ_ABI_VERSION of its build). */
@@ -224,6 +225,31 @@ luq_status luq_gemm_wgrad(const uint8_t* g_codes_t, const float* alpha, int n_sa
                           const uint8_t* a_codes_t, const float* a_scale, int a_signed, int64_t T,
                           int64_t Nout, int64_t Kin, float* dw, void* ws, size_t ws_bytes,
                           void* stream);
+
+/*
+ * int4_gemm_fwd -- the forward GEMM of Eq. forward on INT4 codes
+ * (Appendix A.1: every MAC on codes, the two scales applied once):
+ *   y[m][n] = x_scale * w_scale * sum_k cx[m][k] * cw[n][k]
+ * i.e. y = Q(x) Q(W)^T for activations x [M tokens][K in-features] and the
+ * weight W [N out][K in] in its natural layout; both are the row-major
+ * codes output of int4_quantize, so neither is transposed.  Integer MACs
+ * accumulate exactly in int32; reductions longer than the int32-exact
+ * length are split and the partial sums combined exactly in a fixed order.
+ *
+ *  x_codes    [M][K] INT4 codes; x_scale 1 float (device); x_signed 0/1
+ *             (unsigned for non-negative activations such as ReLU outputs).
+ *  w_codes    [N][K] INT4 codes; w_scale 1 float (device); w_signed 0/1.
+ *  M, N >= 1 and below 2^30; K >= 32 and a multiple of 32.
+ *  y          out: [M][N] fp32, row-major.
+ *  ws         workspace of luq_workspace_size(LUQ_OP_GEMM_FWD, M, N, K)
+ *             (0 bytes, NULL allowed, unless the reduction is split).
+ *  Errors: LUQ_ERR_NULL, LUQ_ERR_SHAPE, LUQ_ERR_WORKSPACE, LUQ_ERR_ALIGN
+ *  (code operands and ws 16-byte aligned; y and scales 4-byte aligned),
+ *  LUQ_ERR_HIP; nothing is enqueued on error.
+ */
+luq_status int4_gemm_fwd(const uint8_t* x_codes, const float* x_scale, int x_signed,
+                         const uint8_t* w_codes, const float* w_scale, int w_signed, int64_t M,
+                         int64_t N, int64_t K, float* y, void* ws, size_t ws_bytes, void* stream);
 
 /*
  * int4_im2col3x3_t -- lowering of a 3x3 / stride 1 / zero-pad 1 convolution

@@ -18,12 +18,12 @@ LIB_PATH = os.path.join(_HERE, "libluq.so")
 
 LUQ_OK = 0
 LUQ_F32, LUQ_BF16 = 0, 1
-OP_QUANTIZE_GRAD, OP_INT4_QUANTIZE, OP_GEMM_DGRAD, OP_GEMM_WGRAD = 0, 1, 2, 3
+OP_QUANTIZE_GRAD, OP_INT4_QUANTIZE, OP_GEMM_DGRAD, OP_GEMM_WGRAD, OP_GEMM_FWD = 0, 1, 2, 3, 4
 
 EXPORTS = (
     "luq_abi_version", "luq_status_string", "luq_last_error", "luq_plane_bytes",
     "luq_workspace_size", "luq_quantize_grad", "luq_quantize_grad_hindsight", "int4_quantize",
-    "luq_gemm_dgrad", "luq_gemm_wgrad", "int4_im2col3x3_t",
+    "luq_gemm_dgrad", "luq_gemm_wgrad", "int4_gemm_fwd", "int4_im2col3x3_t",
 )
 
 
@@ -58,6 +58,8 @@ def _load():
     lib.luq_gemm_dgrad.argtypes = [vp, vp, i32, vp, vp, i32, i64, i64, i64, vp, vp, sz, vp]
     lib.luq_gemm_wgrad.restype = i32
     lib.luq_gemm_wgrad.argtypes = [vp, vp, i32, vp, vp, i32, i64, i64, i64, vp, vp, sz, vp]
+    lib.int4_gemm_fwd.restype = i32
+    lib.int4_gemm_fwd.argtypes = [vp, vp, i32, vp, vp, i32, i64, i64, i64, vp, vp, sz, vp]
     lib.int4_im2col3x3_t.restype = i32
     lib.int4_im2col3x3_t.argtypes = [vp, i64, i64, i64, i64, vp, vp]
     return lib
@@ -211,6 +213,18 @@ def luq_gemm_wgrad(g_codes_t, alpha, a_codes_t, a_scale, a_signed, T, Nout, Kin,
                             1 if a_signed else 0, T, Nout, Kin, _ptr(dw), _ptr(ws), ws.numel(), _stream(dev))
     _check(st, "luq_gemm_wgrad")
     return dw
+
+
+def int4_gemm_fwd(x_codes, x_scale, x_signed, w_codes, w_scale, w_signed, M, N, K, y=None, ws=None):
+    """y [M, N] = Q(x) Q(W)^T from x codes [M, K] and W codes [N, K] (row-major)."""
+    dev = x_codes.device
+    y = torch.empty(M, N, dtype=torch.float32, device=dev) if y is None else y
+    wsb = workspace_size(OP_GEMM_FWD, M, N, K)
+    ws = _bytes(wsb, dev) if ws is None else ws
+    st = LIB.int4_gemm_fwd(_ptr(x_codes), _ptr(x_scale), 1 if x_signed else 0, _ptr(w_codes), _ptr(w_scale),
+                           1 if w_signed else 0, M, N, K, _ptr(y), _ptr(ws), ws.numel(), _stream(dev))
+    _check(st, "int4_gemm_fwd")
+    return y
 
 
 def int4_im2col3x3_t(act_codes, B, H, W, C, col_t=None):

@@ -69,6 +69,8 @@ size_t luq_workspace_size(int op, int64_t d0, int64_t d1, int64_t d2) {
       return (d0 > 0 && d1 > 0 && d2 > 0) ? luq::gemm_workspace_bytes(d0, d1, d2, 1) : 0;
     case LUQ_OP_GEMM_WGRAD:
       return (d0 > 0 && d1 > 0 && d2 > 0) ? luq::gemm_workspace_bytes(d1, d2, d0, 1) : 0;
+    case LUQ_OP_GEMM_FWD:
+      return (d0 > 0 && d1 > 0 && d2 > 0) ? luq::gemm_fwd_workspace_bytes(d0, d1, d2) : 0;
     default:
       return 0;
   }
@@ -162,23 +164,38 @@ luq_status int4_quantize(const void* x, luq_dtype dt, int64_t rows, int64_t cols
                                               static_cast<hipStream_t>(stream)));
 }
 
-static luq_status gemm_common(const char* name, const uint8_t* A, const float* alpha, int ns,
-                              const uint8_t* B, const float* bscale, int b_signed, int64_t M,
-                              int64_t N, int64_t K, float* C, void* ws, size_t ws_bytes,
-                              void* stream) {
+// Checks shared by the three GEMMs; need = the workspace the call requires.
+static luq_status gemm_checks(const char* name, const uint8_t* A, const float* alpha, const uint8_t* B,
+                              const float* bscale, int64_t M, int64_t N, int64_t K, const float* C, size_t need,
+                              const void* ws, size_t ws_bytes) {
   if (!A || !alpha || !B || !bscale || !C) return fail(LUQ_ERR_NULL, "%s: NULL operand", name);
-  if (ns != 1 && ns != 2) return fail(LUQ_ERR_PARAM, "%s: n_samples must be 1 or 2", name);
+  if (need && (!ws || ws_bytes < need)) return fail(LUQ_ERR_WORKSPACE, "%s: workspace too small", name);
+  if (!aligned16(A) || !aligned16(B) || !aligned16(ws) || !aligned4(C) || !aligned4(alpha) ||
+      !aligned4(bscale))
+    return fail(LUQ_ERR_ALIGN, "%s: code operands and ws must be 16-byte aligned", name);
+  return LUQ_OK;
+}
+
+static luq_status gemm_shape(const char* name, int64_t M, int64_t N, int64_t K) {
   if (M < 1 || N < 1 || K < 32 || (K & 31))
     return fail(LUQ_ERR_SHAPE, "%s: need M, N >= 1 and K a positive multiple of 32", name);
   if (mul_overflows(M, N) || mul_overflows(M, K) || mul_overflows(N, K))
     return fail(LUQ_ERR_SHAPE, "%s: size overflows", name);
   if (M > INT32_MAX / 2 || N > INT32_MAX / 2)
     return fail(LUQ_ERR_SHAPE, "%s: M and N must be below 2^30", name);
-  const size_t need = luq::gemm_workspace_bytes(M, N, K, ns);
-  if (need && (!ws || ws_bytes < need)) return fail(LUQ_ERR_WORKSPACE, "%s: workspace too small", name);
-  if (!aligned16(A) || !aligned16(B) || !aligned16(ws) || !aligned4(C) || !aligned4(alpha) ||
-      !aligned4(bscale))
-    return fail(LUQ_ERR_ALIGN, "%s: code operands and ws must be 16-byte aligned", name);
+  return LUQ_OK;
+}
+
+static luq_status gemm_common(const char* name, const uint8_t* A, const float* alpha, int ns,
+                              const uint8_t* B, const float* bscale, int b_signed, int64_t M,
+                              int64_t N, int64_t K, float* C, void* ws, size_t ws_bytes,
+                              void* stream) {
+  if (!A || !alpha || !B || !bscale || !C) return fail(LUQ_ERR_NULL, "%s: NULL operand", name);
+  if (ns != 1 && ns != 2) return fail(LUQ_ERR_PARAM, "%s: n_samples must be 1 or 2", name);
+  luq_status st = gemm_shape(name, M, N, K);
+  if (st != LUQ_OK) return st;
+  st = gemm_checks(name, A, alpha, B, bscale, M, N, K, C, luq::gemm_workspace_bytes(M, N, K, ns), ws, ws_bytes);
+  if (st != LUQ_OK) return st;
   return hip_status(luq::launch_gemm_luq_int4(A, (int64_t)luq::plane_bytes(M * K), ns, alpha, B,
                                               bscale, b_signed ? 1 : 0, M, N, K, C, ws, ws_bytes,
                                               static_cast<hipStream_t>(stream)));
@@ -200,6 +217,21 @@ luq_status luq_gemm_wgrad(const uint8_t* g_codes_t, const float* alpha, int n_sa
   g_last_error[0] = 0;
   return gemm_common("luq_gemm_wgrad", g_codes_t, alpha, n_samples, a_codes_t, a_scale, a_signed,
                      Nout, Kin, T, dw, ws, ws_bytes, stream);
+}
+
+luq_status int4_gemm_fwd(const uint8_t* x_codes, const float* x_scale, int x_signed, const uint8_t* w_codes,
+                         const float* w_scale, int w_signed, int64_t M, int64_t N, int64_t K, float* y, void* ws,
+                         size_t ws_bytes, void* stream) {
+  const char* fn = "int4_gemm_fwd";
+  g_last_error[0] = 0;
+  if (!x_codes || !x_scale || !w_codes || !w_scale || !y) return fail(LUQ_ERR_NULL, "%s: NULL operand", fn);
+  luq_status st = gemm_shape(fn, M, N, K);
+  if (st != LUQ_OK) return st;
+  st = gemm_checks(fn, x_codes, x_scale, w_codes, w_scale, M, N, K, y, luq::gemm_fwd_workspace_bytes(M, N, K), ws,
+                   ws_bytes);
+  if (st != LUQ_OK) return st;
+  return hip_status(luq::launch_gemm_int4_fwd(x_codes, x_scale, x_signed ? 1 : 0, w_codes, w_scale,
+                                              w_signed ? 1 : 0, M, N, K, y, ws, static_cast<hipStream_t>(stream)));
 }
 
 luq_status int4_im2col3x3_t(const uint8_t* act_codes, int64_t B, int64_t H, int64_t W, int64_t C,

@@ -1,514 +1,21 @@
-// 4-bit backward / update GEMMs on INT8 MFMA (gfx950).
-//
-//   C[m][n] = (alpha / ns) * s_B * sum_k A[m][k] * B[n][k]
-//
-// A holds LUQ codes (Section 4 of the paper; ns SMP planes, Section 5.1), B
-// INT4 codes (Section 3.3).  Both operands are K-major nibble matrices; the
-// quantizers write whichever layout (row-major or transposed) a GEMM needs,
-// so the GEMM never transposes.
-//
-// Carrier: v_mfma_i32_32x32x32_i8 with exact int32 accumulation.  Codes are
-// expanded from nibbles to int8 once per workgroup tile, on the way from
-// global memory into LDS:
-//   LUQ  : a byte LUT (v_perm_b32) maps the exponent field e to 2^(e-1) (or
-//          0), then bytes whose sign bit is set are negated with a SWAR
-//          xor/add.  Two SMP planes are expanded to excess-64 bytes and
-//          summed with one word add (|sum| <= 64, no carries).
-//   INT4 : the nibble is moved to the top of its byte, giving 16*q (signed,
-//          two's complement) or 8*q (unsigned) with no further work; the
-//          extra power of two is removed exactly in the epilogue.
-// The even-k nibbles of a word land in one int8 word and the odd-k nibbles
-// in the next.  Both operands use the same order, so the contraction over
-// k is unchanged.
-//
-// The per-tensor scales are applied once to the int32 sums (Appendix A.1):
-//   C = fl32( fl32(acc) * fl32( fl32(alpha / ns) * s_B ) * 2^-4|2^-3 ).
-// Long reductions are split along K into chunks whose int32 sums cannot
-// overflow; chunk sums are added in int64 in a fixed order.
-#include "luq_device.hpp"
-#include "luq_launch.hpp"
+// 4-bit backward and update GEMMs (Eq. backward, Eq. update): A = LUQ codes
+// of the neural gradient (n SMP planes), B = INT4 codes; the tile kernel is in
+// gemm_kernel.hpp.
+#include "gemm_kernel.hpp"
 
 namespace luq {
 
-typedef int v4i __attribute__((ext_vector_type(4)));
-typedef int v16i __attribute__((ext_vector_type(16)));
-typedef unsigned v4u __attribute__((ext_vector_type(4)));
-
-// Word 3 of a raw buffer descriptor on gfx9 (32-bit data, no swizzle).
-constexpr int kBufferFlags = 0x00020000;
-// A buffer offset beyond any operand's range: such loads return zeros.
-constexpr int kOutOfRange = 0x7FFFFFF0;
-
-constexpr int kGemmThreads = 256;
-constexpr int kKAlign = 128;            // k-chunk granularity of a split
-constexpr int64_t kMaxExactK = 1 << 18;  // |A| <= 64, |B| <= 120: 2^18 * 7680 < 2^31
-
-// ---- nibble -> int8 expansion ------------------------------------------------
-
-__device__ __forceinline__ void expand_luq(uint32_t x, uint32_t& lo, uint32_t& hi) {
-  // bytes 0..7 of the table: 0, 1, 2, 4, 8, 16, 32, 64 (indexed by field e)
-  const uint32_t t_lo = 0x04020100u, t_hi = 0x40201008u;
-  const uint32_t m_lo = __builtin_amdgcn_perm(t_hi, t_lo, x & 0x07070707u);
-  const uint32_t m_hi = __builtin_amdgcn_perm(t_hi, t_lo, (x >> 4) & 0x07070707u);
-  // selector bytes 12 (sign clear) or 13 (sign set): v_perm_b32 turns them
-  // into 0x00 / 0xFF, a byte mask of the negative elements
-  const uint32_t q_lo = ((x >> 3) & 0x01010101u) | 0x0C0C0C0Cu;
-  const uint32_t q_hi = ((x >> 7) & 0x01010101u) | 0x0C0C0C0Cu;
-  const uint32_t k_lo = __builtin_amdgcn_perm(0u, 0u, q_lo), k_hi = __builtin_amdgcn_perm(0u, 0u, q_hi);
-  // negation = (m ^ 0xFF) + 1, which never carries out of a byte because
-  // m >= 1 wherever the sign is set
-  lo = (m_lo ^ k_lo) + (q_lo & 0x01010101u);
-  hi = (m_hi ^ k_hi) + (q_hi & 0x01010101u);
-}
-
-// SMP operand (two LUQ planes, R <= 5 so every value is in [-32, 32]): each
-// plane is expanded to excess-64 bytes u = 64 + v (a LUT of 64 + 2^(e-1),
-// and 128 - that for negative codes, as (P ^ 0x7F) + 1), so that the byte
-// sum u0 + u1 = 128 + v0 + v1 lies in [64, 192] and one word add carries
-// nothing across bytes; flipping bit 7 then gives v0 + v1 in two's
-// complement.
-__device__ __forceinline__ void expand_luq_excess64(uint32_t x, uint32_t& lo, uint32_t& hi) {
-  // bytes 0..7: 64 + {0, 1, 2, 4, 8, 16, 32, 64}
-  const uint32_t t_lo = 0x44424140u, t_hi = 0x80605048u;
-  const uint32_t p_lo = __builtin_amdgcn_perm(t_hi, t_lo, x & 0x07070707u);
-  const uint32_t p_hi = __builtin_amdgcn_perm(t_hi, t_lo, (x >> 4) & 0x07070707u);
-  const uint32_t s_lo = (x >> 3) & 0x01010101u, s_hi = (x >> 7) & 0x01010101u;
-  lo = (p_lo ^ ((s_lo << 7) - s_lo)) + s_lo;
-  hi = (p_hi ^ ((s_hi << 7) - s_hi)) + s_hi;
-}
-
-template <bool SIGNED>
-__device__ __forceinline__ void expand_int4(uint32_t x, uint32_t& lo, uint32_t& hi) {
-  if constexpr (SIGNED) {
-    lo = (x << 4) & 0xF0F0F0F0u;  // 16 * q
-    hi = x & 0xF0F0F0F0u;
-  } else {
-    lo = (x << 3) & 0x78787878u;  // 8 * q
-    hi = (x >> 1) & 0x78787878u;
-  }
-}
-
-struct GemmArgs {
-  const uint8_t* A;
-  int64_t a_plane;
-  const uint8_t* B;
-  int64_t M, N, K;
-  const float* alpha;
-  const float* bscale;
-  float* C;
-  int32_t* partial;   // split-K chunk sums [splits][M][N], or null
-  int64_t k_chunk;    // k per split (multiple of kKAlign)
-  int tiles_m, tiles_n;
-  int vec;            // rows of C (or partial) are 16-byte aligned: vector stores
-};
-
-// Block -> output tile.  Blocks are dispatched round-robin over the 8 XCDs
-// (each with its own L2), so when the tile count allows, consecutive runs of
-// tiles are given to one XCD; within that run tiles are visited in groups of
-// 8 tile-rows so that the A rows and B rows in flight are shared.
-__device__ __forceinline__ void tile_coords(int bid, int ntm, int ntn, int& tm, int& tn) {
-  const int total = ntm * ntn;
-  int L = bid;
-  if ((total & 7) == 0) L = (bid & 7) * (total >> 3) + (bid >> 3);
-  constexpr int G = 8;
-  const int per_group = G * ntn;
-  const int first_m = (L / per_group) * G;
-  const int gsize = min(ntm - first_m, G);
-  const int in_group = L - (L / per_group) * per_group;
-  tm = first_m + in_group % gsize;
-  tn = in_group / gsize;
-}
-
-// ---- the tile kernel ----------------------------------------------------------
-//
-// 256 threads = 2 x 2 waves; a wave owns a (BM/2) x (BN/2) block of C as
-// (BM/64) x (BN/64) tiles of the 32x32 MFMA.  Per k-stage of BK (64 or 128):
-//   - the packed tile for stage t+2 is loaded into registers,
-//   - stage t is multiplied out of LDS buffer t%2,
-//   - stage t+1 (loaded one iteration earlier) is expanded into LDS buffer
-//     (t+1)%2,
-// all in one block of straight-line code, with the expansion and loads cut
-// into one piece per 32-deep k-step and placed after that k-step's MFMAs, so
-// the VALU work issues between MFMAs.  The MFMA takes the B fragment as its
-// first operand, so each lane ends up with 4 consecutive columns of one C row.
-//
-// FULLK: K is a multiple of kKAlign, so every stage of a split lies inside
-// the operands' rows and no chunk needs a per-lane range check; stages past
-// the end of the split are then never multiplied.  Otherwise chunks past
-// the split's end read as zeros and the loop may multiply one zero stage.
-// The 64-deep variant keeps three waves per SIMD.
-template <int BM, int BN, int BK, int NS, bool BSIGNED, bool FULLK>
-__global__ __launch_bounds__(kGemmThreads, BK == 64 ? 3 : 1) void gemm_luq_int4_kernel(GemmArgs a) {
-  static_assert(BM % 64 == 0 && BN % 64 == 0, "wave tiles are multiples of 32");
-  static_assert(BK == 64 || BK == 128, "k per stage");
-  constexpr int kBK = BK;
-  constexpr int kPitch = BK + 16;                      // LDS row pitch in bytes
-  constexpr int KC = BK / 32;                          // 16-byte chunks per row and stage
-  constexpr int TM = BM / 64, TN = BN / 64;            // 32x32 MFMA tiles per wave
-  constexpr int ACH = BM * KC / kGemmThreads;          // 16-byte A chunks per thread and stage
-  constexpr int BCH = BN * KC / kGemmThreads;
-  static_assert(ACH >= 1 && BCH >= 1, "tile too small for the block");
-  constexpr int STAGE = (BM + BN) * kPitch;            // bytes of one LDS stage
-  __shared__ __attribute__((aligned(16))) uint8_t lds[2 * STAGE];
-
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm = wave >> 1, wn = wave & 1;
-  int tm, tn;
-  tile_coords(blockIdx.x, a.tiles_m, a.tiles_n, tm, tn);
-  const int64_t m0 = (int64_t)tm * BM, n0 = (int64_t)tn * BN;
-  const int64_t kbeg = (int64_t)blockIdx.y * a.k_chunk;
-  const int64_t kend = min(kbeg + a.k_chunk, a.K);
-  const int nkt = (int)((kend - kbeg + kBK - 1) / kBK);
-  const int64_t ld = a.K >> 1;  // bytes per operand row
-
-  // Operands are read through buffer descriptors whose range is the operand
-  // itself: rows past M (or N) fall outside the range, and a chunk past the
-  // end of this split's k range is given an offset outside it, so both read
-  // as zeros without a branch.
-  __amdgpu_buffer_rsrc_t rsa[NS];
-#pragma unroll
-  for (int s = 0; s < NS; ++s)
-    rsa[s] = __builtin_amdgcn_make_buffer_rsrc((void*)(a.A + s * a.a_plane), (short)0,
-                                               (int)(a.M * ld), kBufferFlags);
-  const __amdgpu_buffer_rsrc_t rsb =
-      __builtin_amdgcn_make_buffer_rsrc((void*)a.B, (short)0, (int)(a.N * ld), kBufferFlags);
-  int offa[ACH], kca[ACH], offb[BCH], kcb[BCH];
-#pragma unroll
-  for (int i = 0; i < ACH; ++i) {
-    const int c = tid + i * kGemmThreads, row = c / KC, kc = c % KC;
-    kca[i] = kc * 32;
-    offa[i] = (int)((m0 + row) * ld + (kbeg >> 1) + kc * 16);
-  }
-#pragma unroll
-  for (int i = 0; i < BCH; ++i) {
-    const int c = tid + i * kGemmThreads, row = c / KC, kc = c % KC;
-    kcb[i] = kc * 32;
-    offb[i] = (int)((n0 + row) * ld + (kbeg >> 1) + kc * 16);
-  }
-
-  struct Regs {
-    v4u a[NS][ACH];
-    v4u b[BCH];
-  };
-  // Work of one stage is split into KS pieces, one per 32-deep k-step: piece
-  // kk covers the A and B chunks i with i % KS == kk.
-  constexpr int KS = kBK / 32;
-  auto load_piece = [&](Regs& r, int t, int kk) {
-    const int64_t k0 = kbeg + (int64_t)t * kBK;
-#pragma unroll
-    for (int i = 0; i < ACH; ++i) {
-      if (i % KS != kk) continue;
-      const int off = FULLK || (k0 + kca[i]) < kend ? offa[i] + t * (kBK / 2) : kOutOfRange;
-#pragma unroll
-      for (int s = 0; s < NS; ++s) r.a[s][i] = __builtin_amdgcn_raw_buffer_load_b128(rsa[s], off, 0, 0);
-    }
-#pragma unroll
-    for (int i = 0; i < BCH; ++i) {
-      if (i % KS != kk) continue;
-      const int off = FULLK || (k0 + kcb[i]) < kend ? offb[i] + t * (kBK / 2) : kOutOfRange;
-      r.b[i] = __builtin_amdgcn_raw_buffer_load_b128(rsb, off, 0, 0);
-    }
-  };
-  auto expand_piece = [&](const Regs& r, int buf, int kk) {
-    uint8_t* As = lds + buf * STAGE;
-    uint8_t* Bs = As + BM * kPitch;
-#pragma unroll
-    for (int i = 0; i < ACH; ++i) {
-      if (i % KS != kk) continue;
-      const int c = tid + i * kGemmThreads, row = c / KC, kc = c % KC;
-      uint32_t w[8];
-      const uint32_t x0[4] = {r.a[0][i][0], r.a[0][i][1], r.a[0][i][2], r.a[0][i][3]};
-      if constexpr (NS == 1) {
-#pragma unroll
-        for (int d = 0; d < 4; ++d) expand_luq(x0[d], w[2 * d], w[2 * d + 1]);
-      } else {
-        const uint32_t x1[4] = {r.a[1][i][0], r.a[1][i][1], r.a[1][i][2], r.a[1][i][3]};
-#pragma unroll
-        for (int d = 0; d < 4; ++d) {
-          uint32_t l0, h0, l1, h1;
-          expand_luq_excess64(x0[d], l0, h0);
-          expand_luq_excess64(x1[d], l1, h1);
-          w[2 * d] = (l0 + l1) ^ 0x80808080u;
-          w[2 * d + 1] = (h0 + h1) ^ 0x80808080u;
-        }
-      }
-      uint4* dst = reinterpret_cast<uint4*>(As + row * kPitch + kc * 32);
-      dst[0] = make_uint4(w[0], w[1], w[2], w[3]);
-      dst[1] = make_uint4(w[4], w[5], w[6], w[7]);
-    }
-#pragma unroll
-    for (int i = 0; i < BCH; ++i) {
-      if (i % KS != kk) continue;
-      const int c = tid + i * kGemmThreads, row = c / KC, kc = c % KC;
-      uint32_t w[8];
-      const uint32_t x0[4] = {r.b[i][0], r.b[i][1], r.b[i][2], r.b[i][3]};
-#pragma unroll
-      for (int d = 0; d < 4; ++d) expand_int4<BSIGNED>(x0[d], w[2 * d], w[2 * d + 1]);
-      uint4* dst = reinterpret_cast<uint4*>(Bs + row * kPitch + kc * 32);
-      dst[0] = make_uint4(w[0], w[1], w[2], w[3]);
-      dst[1] = make_uint4(w[4], w[5], w[6], w[7]);
-    }
-  };
-
-  v16i acc[TM][TN];
-#pragma unroll
-  for (int i = 0; i < TM; ++i)
-#pragma unroll
-    for (int j = 0; j < TN; ++j) acc[i][j] = v16i{};
-
-  // 32x32x32 MFMA operands: lane l supplies row l%32 and 16 consecutive k
-  // (positions 16*(l/32) .. +15 of the 32-k step) of its fragment.
-  struct Frags {
-    v4i a[TM], b[TN];
-  };
-  auto read_frags = [&](int buf, int kk, Frags& f) {
-    const uint8_t* As = lds + buf * STAGE;
-    const uint8_t* as = As + (wm * (BM / 2) + (lane & 31)) * kPitch + (lane >> 5) * 16 + kk * 32;
-    const uint8_t* bs = As + BM * kPitch + (wn * (BN / 2) + (lane & 31)) * kPitch + (lane >> 5) * 16 + kk * 32;
-#pragma unroll
-    for (int i = 0; i < TM; ++i) f.a[i] = *reinterpret_cast<const v4i*>(as + i * 32 * kPitch);
-#pragma unroll
-    for (int j = 0; j < TN; ++j) f.b[j] = *reinterpret_cast<const v4i*>(bs + j * 32 * kPitch);
-  };
-  auto mfmas = [&](const Frags& f) {
-#pragma unroll
-    for (int i = 0; i < TM; ++i)
-#pragma unroll
-      for (int j = 0; j < TN; ++j)
-        acc[i][j] = __builtin_amdgcn_mfma_i32_32x32x32_i8(f.b[j], f.a[i], acc[i][j], 0, 0, 0);
-  };
-
-  // One pipeline step, straight-line code between barriers: for each k-step
-  // of stage `cb` (in LDS), the fragments of the next k-step are read ahead,
-  // the MFMAs of this k-step issue, and one piece of the next stage (the
-  // registers `r`) is expanded into the other buffer, after which that
-  // piece's registers are reloaded from stage `tload` into `rl`.  Source
-  // order interleaves the expansion work with the MFMAs.
-  auto step = [&](int cb, const Regs& r, Regs& rl, int tload) {
-    Frags f[2];
-    read_frags(cb, 0, f[0]);
-#pragma unroll
-    for (int kk = 0; kk < KS; ++kk) {
-      if (kk + 1 < KS) read_frags(cb, kk + 1, f[(kk + 1) & 1]);
-      mfmas(f[kk & 1]);
-      expand_piece(r, cb ^ 1, kk);
-      load_piece(rl, tload, kk);
-    }
-    __syncthreads();
-  };
-
-  Regs r0, r1;
-#pragma unroll
-  for (int kk = 0; kk < KS; ++kk) load_piece(r0, 0, kk);
-#pragma unroll
-  for (int kk = 0; kk < KS; ++kk) load_piece(r1, 1, kk);
-#pragma unroll
-  for (int kk = 0; kk < KS; ++kk) expand_piece(r0, 0, kk);
-  __syncthreads();
-#pragma unroll
-  for (int kk = 0; kk < KS; ++kk) load_piece(r0, 2, kk);
-  int t = 0;
-  for (; t + 2 <= nkt; t += 2) {
-    step(0, r1, r1, t + 3);   // multiply t, expand t+1 (r1), then reuse r1 for t+3
-    step(1, r0, r0, t + 4);   // multiply t+1, expand t+2 (r0), then reuse r0 for t+4
-  }
-  // an odd stage count leaves stage t in buffer 0 (with FULLK the stage
-  // expanded beside it may hold another split's codes; it is not multiplied)
-  if (t < nkt) step(0, r1, r1, t + 3);
-
-  // Epilogue through LDS.  In MFMA tile (i, j), lane l holds row l%32 and, in
-  // registers 4q..4q+3, the 4 consecutive columns 8q + 4*(l/32) + 0..3 (the
-  // swapped operands).  Each wave stages 32 rows of its block at a time as a
-  // row-major slab in its own part of the (now idle) stage buffers, then
-  // stores whole row segments: WN/4 consecutive lanes cover one row of the
-  // wave's block, so a store instruction writes 64*16/WN-row runs of
-  // contiguous 16-byte chunks.  C gets the scaled fp32 values, the split-K
-  // workspace the raw int32 sums.
-  constexpr int WM = BM / 2, WN = BN / 2;
-  constexpr int EP = WN + 4;      // slab row pitch in 32-bit words
-  constexpr int LPR = WN / 4;     // lanes per row in the store phase
-  constexpr int RPI = 64 / LPR;   // rows per store instruction (lanes past RPI * LPR idle)
-  static_assert(4 * 32 * EP * 4 <= 2 * STAGE, "epilogue slabs fit in the stage buffers");
-  static_assert(WM % 32 == 0 && LPR <= 64 && 32 % RPI == 0, "slab shape");
-  uint32_t* E = reinterpret_cast<uint32_t*>(lds) + wave * 32 * EP;
-  const bool part = a.partial != nullptr;
-  const float sc = part ? 0.0f
-                        : __fmul_rn(__fmul_rn(*a.alpha, 1.0f / NS), *a.bscale) * (BSIGNED ? 0x1p-4f : 0x1p-3f);
-  uint32_t* out = part ? reinterpret_cast<uint32_t*>(a.partial + (int64_t)blockIdx.y * a.M * a.N)
-                       : reinterpret_cast<uint32_t*>(a.C);
-  const int64_t rbase = m0 + wm * WM, cbase = n0 + wn * WN;
-  const int srow = lane / LPR, scol = (lane % LPR) * 4;
-  const bool sact = lane < RPI * LPR;
-  __syncthreads();  // every wave is done with the stage buffers
-#pragma unroll
-  for (int i = 0; i < TM; ++i) {
-#pragma unroll
-    for (int j = 0; j < TN; ++j)
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        v4u v;
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int32_t x = acc[i][j][4 * q + r];
-          v[r] = part ? (uint32_t)x : __float_as_uint(__fmul_rn((float)x, sc));
-        }
-        *reinterpret_cast<v4u*>(E + (lane & 31) * EP + j * 32 + 8 * q + 4 * (lane >> 5)) = v;
-      }
-    __syncthreads();
-#pragma unroll
-    for (int rr = 0; rr < 32; rr += RPI) {
-      const int64_t row = rbase + i * 32 + rr + srow;
-      const int64_t col = cbase + scol;
-      if (sact && row < a.M) {
-        const v4u v = *reinterpret_cast<const v4u*>(E + (rr + srow) * EP + scol);
-        uint32_t* dst = out + row * a.N + col;
-        if (a.vec && col + 3 < a.N) {
-          *reinterpret_cast<v4u*>(dst) = v;
-        } else {
-#pragma unroll
-          for (int r = 0; r < 4; ++r)
-            if (col + r < a.N) dst[r] = v[r];
-        }
-      }
-    }
-    __syncthreads();  // the slab is rewritten by the next i
-  }
-}
-
-// Sums the split-K chunk sums in int64 and applies the scales.  A block owns
-// 64 consecutive outputs; its four waves add every fourth chunk (coalesced
-// 256-byte reads), then combine through LDS in a fixed order.
-template <int NS, bool BSIGNED>
-__global__ __launch_bounds__(256) void splitk_reduce_kernel(const int32_t* __restrict__ partial,
-                                                            int splits, int64_t MN,
-                                                            const float* alpha, const float* bscale,
-                                                            float* __restrict__ C) {
-  __shared__ int64_t part[4][64];
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int64_t i = (int64_t)blockIdx.x * 64 + lane;
-  int64_t s = 0;
-  if (i < MN) {
-    int p = wave;
-    for (; p + 12 < splits; p += 16) {
-      const int32_t v0 = partial[(int64_t)p * MN + i], v1 = partial[(int64_t)(p + 4) * MN + i];
-      const int32_t v2 = partial[(int64_t)(p + 8) * MN + i], v3 = partial[(int64_t)(p + 12) * MN + i];
-      s += (int64_t)v0 + v1 + v2 + v3;
-    }
-    for (; p < splits; p += 4) s += partial[(int64_t)p * MN + i];
-  }
-  part[wave][lane] = s;
-  __syncthreads();
-  if (wave == 0 && i < MN) {
-    const int64_t tot = part[0][lane] + part[1][lane] + part[2][lane] + part[3][lane];
-    const float sc = __fmul_rn(__fmul_rn(*alpha, 1.0f / NS), *bscale) * (BSIGNED ? 0x1p-4f : 0x1p-3f);
-    C[i] = __fmul_rn((float)tot, sc);
-  }
-}
-
-// ---- planning and launch ----------------------------------------------------------
-
-struct GemmPlan {
-  int bm, bn, bk;
-  int64_t tiles_m, tiles_n;
-  int splits;
-  int64_t k_chunk;
-};
-
-static GemmPlan plan_gemm(int64_t M, int64_t N, int64_t K) {
-  GemmPlan p;
-  auto tiles = [&](int bm, int bn) { return ((M + bm - 1) / bm) * ((N + bn - 1) / bn); };
-  // 256x256 tiles halve the expansion and LDS work per MAC but run one wave
-  // per SIMD; they pay off only for long reductions.  Short reductions (the
-  // conv dX with K = 64) are bound by the fp32 output and prefer the 128x128
-  // tile, which keeps two workgroups per CU.
-  if (K >= 1024 && tiles(256, 256) >= 256) {
-    p.bm = 256;
-    p.bn = 256;
-  } else if (M <= 64 && N >= 192 && K >= 65536) {
-    // few output rows and a long reduction (the conv dW: 64 x 576 x 200704):
-    // wide tiles so that the A rows are re-read for fewer column tiles
-    p.bm = 64;
-    p.bn = 192;
-  } else if (tiles(128, 128) >= 128) {
-    p.bm = 128;
-    p.bn = 128;
-  } else {
-    p.bm = 64;
-    p.bn = 64;
-  }
-  // a reduction of at most 64 fits one 64-deep stage: half the LDS, so more
-  // workgroups per CU overlap their loads with other tiles' output stores
-  p.bk = (K <= 64 && p.bm == 128) ? 64 : 128;
-  p.tiles_m = (M + p.bm - 1) / p.bm;
-  p.tiles_n = (N + p.bn - 1) / p.bn;
-  const int64_t nt = p.tiles_m * p.tiles_n;
-  const int64_t ktiles = (K + kKAlign - 1) / kKAlign;
-  int64_t splits = 1;
-  // too few tiles to fill 256 CUs: split the reduction (>= 8 k-stages each);
-  // the wide tiles aim at one workgroup per CU, since every split adds
-  // M x N partial sums to write and read back
-  if (nt < 256) {
-    const int64_t target = p.bn == 192 ? 256 : 512;
-    splits = (target + nt - 1) / nt;
-    const int64_t max_by_len = ktiles / 8 > 0 ? ktiles / 8 : 1;
-    if (splits > max_by_len) splits = max_by_len;
-  }
-  // int32-exact chunk length
-  const int64_t min_splits = (K + kMaxExactK - 1) / kMaxExactK;
-  if (splits < min_splits) splits = min_splits;
-  if (splits < 1) splits = 1;
-  const int64_t chunk_tiles = (ktiles + splits - 1) / splits;
-  p.k_chunk = chunk_tiles * kKAlign;
-  p.splits = (int)((ktiles + chunk_tiles - 1) / chunk_tiles);
-  return p;
-}
-
 size_t gemm_workspace_bytes(int64_t M, int64_t N, int64_t K, int /*ns*/) {
-  const GemmPlan p = plan_gemm(M, N, K);
+  const GemmPlan p = plan_gemm(M, N, K, kMaxExactK);
   if (p.splits <= 1) return 0;
   return (size_t)p.splits * (size_t)M * (size_t)N * sizeof(int32_t);
-}
-
-template <int BM, int BN, int BK, int NS, bool BSIGNED>
-static void launch_tile(const GemmArgs& a, dim3 grid, hipStream_t st) {
-  if (a.K % kKAlign == 0)
-    hipLaunchKernelGGL((gemm_luq_int4_kernel<BM, BN, BK, NS, BSIGNED, true>), grid, dim3(kGemmThreads), 0, st, a);
-  else
-    hipLaunchKernelGGL((gemm_luq_int4_kernel<BM, BN, BK, NS, BSIGNED, false>), grid, dim3(kGemmThreads), 0, st, a);
-}
-
-template <int NS, bool BSIGNED>
-static hipError_t gemm_launch_t(const GemmArgs& a0, const GemmPlan& p, hipStream_t st) {
-  GemmArgs a = a0;
-  a.tiles_m = (int)p.tiles_m;
-  a.tiles_n = (int)p.tiles_n;
-  a.k_chunk = p.k_chunk;
-  const dim3 grid((unsigned)(p.tiles_m * p.tiles_n), (unsigned)p.splits);
-  // 16-byte stores need 16-byte aligned rows
-  a.vec = (a.N % 4) == 0 && (((uintptr_t)(a.partial ? (void*)a.partial : (void*)a.C)) & 15) == 0;
-  if (p.bm == 256)
-    launch_tile<256, 256, 128, NS, BSIGNED>(a, grid, st);
-  else if (p.bm == 128 && p.bk == 64)
-    launch_tile<128, 128, 64, NS, BSIGNED>(a, grid, st);
-  else if (p.bm == 128)
-    launch_tile<128, 128, 128, NS, BSIGNED>(a, grid, st);
-  else if (p.bn == 192)
-    launch_tile<64, 192, 128, NS, BSIGNED>(a, grid, st);
-  else
-    launch_tile<64, 64, 128, NS, BSIGNED>(a, grid, st);
-  if (p.splits > 1) {
-    const int64_t MN = a.M * a.N;
-    hipLaunchKernelGGL((splitk_reduce_kernel<NS, BSIGNED>), dim3((unsigned)((MN + 63) / 64)), dim3(256), 0, st,
-                       a.partial, p.splits, MN, a.alpha, a.bscale, a.C);
-  }
-  return hipGetLastError();
 }
 
 hipError_t launch_gemm_luq_int4(const uint8_t* A, int64_t a_plane, int ns, const float* alpha,
                                 const uint8_t* B, const float* bscale, int b_signed, int64_t M,
                                 int64_t N, int64_t K, float* C, void* ws, size_t /*ws_bytes*/,
                                 hipStream_t st) {
-  const GemmPlan p = plan_gemm(M, N, K);
+  const GemmPlan p = plan_gemm(M, N, K, kMaxExactK);
   GemmArgs a;
   a.A = A;
   a.a_plane = a_plane;
@@ -521,8 +28,8 @@ hipError_t launch_gemm_luq_int4(const uint8_t* A, int64_t a_plane, int ns, const
   a.C = C;
   a.partial = p.splits > 1 ? static_cast<int32_t*>(ws) : nullptr;
   if (ns == 1)
-    return b_signed ? gemm_launch_t<1, true>(a, p, st) : gemm_launch_t<1, false>(a, p, st);
-  return b_signed ? gemm_launch_t<2, true>(a, p, st) : gemm_launch_t<2, false>(a, p, st);
+    return b_signed ? gemm_launch_t<kAcLuq, 1, true>(a, p, st) : gemm_launch_t<kAcLuq, 1, false>(a, p, st);
+  return b_signed ? gemm_launch_t<kAcLuq, 2, true>(a, p, st) : gemm_launch_t<kAcLuq, 2, false>(a, p, st);
 }
 
 }  // namespace luq

@@ -38,6 +38,12 @@ hipError_t launch_gemm_luq_int4(const uint8_t* A, int64_t a_plane, int ns, const
                                 int64_t N, int64_t K, float* C, void* ws, size_t ws_bytes,
                                 hipStream_t st);
 
+// y[m][n] = x_scale * w_scale * sum_k X[m][k] * W[n][k], INT4 codes, K-major.
+size_t gemm_fwd_workspace_bytes(int64_t M, int64_t N, int64_t K);
+hipError_t launch_gemm_int4_fwd(const uint8_t* X, const float* x_scale, int x_signed, const uint8_t* W,
+                                const float* w_scale, int w_signed, int64_t M, int64_t N, int64_t K, float* Y,
+                                void* ws, hipStream_t st);
+
 hipError_t launch_im2col3x3_t(const uint8_t* act, int64_t B, int64_t H, int64_t W, int64_t C,
                               uint8_t* col_t, hipStream_t st);
 

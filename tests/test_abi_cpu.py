@@ -32,7 +32,7 @@ def _declared():
 
 def test_every_declared_function_is_exported():
     names = _declared()
-    assert len(names) == 11, names
+    assert len(names) == 12, names
     for n in names:
         assert hasattr(LIB, n), n
     assert set(names) == set(luq.EXPORTS)
@@ -57,6 +57,11 @@ def test_plane_and_workspace_sizes():
     # a long, thin reduction is split along K and needs partial sums
     assert luq.workspace_size(luq.OP_GEMM_WGRAD, 200704, 64, 576) > 0
     assert luq.workspace_size(luq.OP_GEMM_DGRAD, 8192, 4096, 16384) == 0
+    # the forward product of INT4 x INT4 (|A|, |B| <= 120 after expansion)
+    # is int32-exact only up to K = 2^17: a longer reduction is split
+    assert luq.workspace_size(luq.OP_GEMM_FWD, 8192, 4096, 1 << 18) > 0
+    assert luq.workspace_size(luq.OP_GEMM_DGRAD, 8192, 4096, 1 << 18) == 0
+    assert luq.workspace_size(luq.OP_GEMM_FWD, 8192, 16384, 4096) == 0
     assert luq.workspace_size(99, 1, 1, 1) == 0
 
 
@@ -155,6 +160,24 @@ def test_wgrad_validation():
     assert LIB.luq_gemm_wgrad(*args, 40, 64, 64, P, P, WS, None) == 2          # T not a multiple of 32
     assert LIB.luq_gemm_wgrad(*args, 200704, 64, 576, P, NUL, 0, None) == 5    # split-K needs ws
     assert LIB.luq_gemm_wgrad(NUL, P3, 1, P2, P3, 0, 64, 8, 8, P, P, WS, None) == 1
+
+
+def _fw(**kw):
+    a = dict(x=P, xs=P3, xsig=1, w=P2, ws_=P3, wsig=1, M=64, N=64, K=64, y=P, ws=P, wsb=WS)
+    a.update(kw)
+    return LIB.int4_gemm_fwd(a["x"], a["xs"], a["xsig"], a["w"], a["ws_"], a["wsig"], a["M"], a["N"], a["K"],
+                             a["y"], a["ws"], a["wsb"], None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(x=NUL), 1), (dict(xs=NUL), 1), (dict(w=NUL), 1), (dict(ws_=NUL), 1), (dict(y=NUL), 1),
+    (dict(M=0), 2), (dict(N=-1), 2), (dict(K=48), 2), (dict(K=16), 2), (dict(N=2**31), 2),
+    (dict(x=PMIS), 6), (dict(w=PMIS), 6), (dict(y=ctypes.c_void_p(0x10002)), 6),
+    (dict(M=8192, N=4096, K=1 << 18, ws=NUL), 5),
+    (dict(M=8192, N=4096, K=1 << 18, wsb=1024), 5),
+])
+def test_fwd_validation(kw, status):
+    assert _fw(**kw) == status
 
 
 def test_im2col_validation():

@@ -231,6 +231,41 @@ def test_mlp_wgrad_sampled_rows(mlp, mlp_data):
     assert np.array_equal(dw, epilogue_replica(acc, alpha, ns, xs)), "mlp dW epilogue not bit-exact"
 
 
+@pytest.fixture(scope="module")
+def mlp_fwd(L, mlp_data):
+    import bench
+    stages, _, d = bench.build_mlp_fwd(L, torch, DEV, d={k: mlp_data[k] for k in ("g", "x", "W")})
+    _run(stages, "mlp fwd")
+    yield d["dev"]
+    d["dev"].clear()
+    torch.cuda.empty_cache()
+
+
+def test_mlp_fwd_int4_whole_tensors(mlp_fwd, mlp_data):
+    xc, xs = mlp_data["xq"]
+    wc, ws = mlp_data["wq"]
+    assert host(mlp_fwd["sx"])[0].tobytes() == np.float32(xs).tobytes()
+    assert host(mlp_fwd["sw"])[0].tobytes() == np.float32(ws).tobytes()
+    assert_codes_equal(host(mlp_fwd["xc"]), xc, "mlp fwd x codes")
+    assert_codes_equal(host(mlp_fwd["wc"]), wc, "mlp fwd W codes")
+
+
+def test_mlp_fwd_sampled_rows(mlp_fwd, mlp_data):
+    """y [8192, 16384] = Q(x) [8192, 4096] Q(W)^T [4096, 16384]: 8 rows."""
+    T, D = mlp_data["x"].shape
+    F = mlp_data["W"].shape[0]
+    xc, xs = mlp_data["xq"]
+    wc, ws = mlp_data["wq"]
+    rows = np.array([0, 1, 255, 256, 4100, 6001, 8190, 8191], dtype=np.int64)
+    y = host(mlp_fwd["y"])[rows]
+    ref, absref = ogemm.gemm_fwd_ref(xc, xs, True, wc, ws, True, T, F, D, rows=rows)
+    assert_gemm_close(y, ref, absref, "mlp fwd rows")
+    X = oint4.int4_decode_int(xc, T * D, True).reshape(T, D)[rows]
+    Wm = oint4.int4_decode_int(wc, F * D, True).reshape(F, D)
+    acc = (X.astype(np.float64) @ Wm.T.astype(np.float64)).astype(np.int64)
+    assert np.array_equal(y, epilogue_replica(acc, xs, 1, ws)), "mlp fwd epilogue not bit-exact"
+
+
 # --------------------------- 1-D quantizer sweep ----------------------------
 
 def _sweep_case(L, g, dtype, what):

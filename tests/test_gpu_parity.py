@@ -278,6 +278,66 @@ def test_gemm_long_reduction_exact_split(L):
     _wgrad_case(L, (1 << 18) + 4096, 8, 16, 1, signed=False, seed=13)
 
 
+def _fwd_case(L, M, N, K, xsig, wsig, seed, dtype=np.float32):
+    """y = Q(x) Q(W)^T: x [M, K] activations, W [N, K] weight; compares with the oracle."""
+    x = synth.normal((M, K), 1.0, [seed, 1])
+    if not xsig:
+        x = np.maximum(x, 0)
+    w = synth.normal((N, K), 0.05, [seed, 2])
+    if not wsig:
+        w = np.abs(w)
+    announce("fwd", M, N, K, xsig, wsig)
+    xc, _, sx = L.int4_quantize(to_dev(x), is_signed=xsig)
+    wc, _, sw = L.int4_quantize(to_dev(w), is_signed=wsig)
+    y = host(L.int4_gemm_fwd(xc, sx, xsig, wc, sw, wsig, M, N, K))
+    rxc, rsx = oint4.int4_quantize(x, is_signed=xsig)
+    rwc, rsw = oint4.int4_quantize(w, is_signed=wsig)
+    assert host(sx)[0] == rsx and host(sw)[0] == rsw
+    ref, absref = ogemm.gemm_fwd_ref(rxc, rsx, xsig, rwc, rsw, wsig, M, N, K)
+    assert_gemm_close(y, ref, absref, f"fwd {M}x{N}x{K}")
+    X = oint4.int4_decode_int(rxc, M * K, xsig).reshape(M, K)
+    Wq = oint4.int4_decode_int(rwc, N * K, wsig).reshape(N, K)
+    acc = (X.astype(np.float64) @ Wq.T.astype(np.float64)).astype(np.int64)
+    assert np.array_equal(y, epilogue_replica(acc, rsx, 1, rsw)), "fwd epilogue not bit-exact"
+
+
+# every tile configuration (64x64 with and without split-K, 128x128 with
+# BK 64 and 128, 256x256, 64x192) with ragged M, N and K tails
+@pytest.mark.parametrize("M,N,K", [(256, 512, 512), (300, 200, 160), (37, 8, 32), (129, 136, 1056),
+                                   (64, 64, 32768), (512, 384, 2048), (1500, 1400, 224), (4192, 4128, 288),
+                                   (2100, 1100, 64), (40, 200, 70048)])
+def test_fwd_parity(L, M, N, K):
+    _fwd_case(L, M, N, K, True, True, seed=M + 2 * N + K)
+
+
+@pytest.mark.parametrize("xsig,wsig", [(False, True), (True, False), (False, False)])
+@pytest.mark.parametrize("M,N,K", [(200, 96, 256), (2100, 2060, 1152)])
+def test_fwd_code_signedness(L, M, N, K, xsig, wsig):
+    _fwd_case(L, M, N, K, xsig, wsig, seed=11 + K)
+
+
+def test_fwd_long_reduction_exact_split(L):
+    """K beyond the int32-exact chunk of INT4 x INT4 (2^17): chunk sums are
+    combined in int64, every output still equals the exact epilogue."""
+    _fwd_case(L, 8, 24, (1 << 17) + 4096, True, True, seed=21)
+
+
+def test_fwd_extreme_codes(L):
+    """All codes at the end of the range: sums of 49 K (signed) and 225 K
+    (unsigned) at K = 2^17, the longest unsplit reduction (4096 x 4096
+    outputs fill the 256 x 256 tiles without a split), and the same with a
+    split reduction (4 x 8 outputs)."""
+    for (M, N), sig, byte, val in [((4096, 4096), True, 0x99, -7), ((4096, 4096), False, 0xFF, 15),
+                                   ((4, 8), True, 0x99, -7), ((4, 8), False, 0xFF, 15)]:
+        K = 1 << 17
+        announce("fwd extreme codes", M, N, K, sig)
+        xc = torch.full((M * K // 2,), byte, dtype=torch.uint8, device="cuda:0")
+        wc = torch.full((N * K // 2,), byte, dtype=torch.uint8, device="cuda:0")
+        one = torch.ones(1, dtype=torch.float32, device="cuda:0")
+        y = host(L.int4_gemm_fwd(xc, one, sig, wc, one, sig, M, N, K))
+        assert np.all(y == np.float32(val * val * K)), (sig, y[0, 0])
+
+
 # ------------------------------- im2col -------------------------------------
 
 # fast path (C and W multiples of 8) over several blocks and odd channel-group
