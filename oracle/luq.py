@@ -16,6 +16,11 @@ Test infrastructure only.  Follows Section 4 of the paper in its order:
 6. SMP (Section 5.1): n independent samples with the same alpha; their mean
    has 1/n of the variance.
 
+Power-of-two LUQ (Appendix, "Power-of-two LUQ"): alpha is replaced by
+alpha_PW2 = 2^ceil(log2 max|x|) / 2^R, so every level is a power of two and
+the top level is the least power of two at or above max|x| (nothing is
+clipped); steps 2-6 are unchanged.
+
 Readings of points the paper leaves open (each also listed in the design
 notes of the repository):
 
@@ -42,6 +47,7 @@ notes of the repository):
   odd element count leaves the last high nibble 0.
 """
 
+import math
 from fractions import Fraction
 
 import numpy as np
@@ -66,6 +72,18 @@ def to_float32(x, dtype="f32"):
 def luq_alpha(maxabs, R):
     """Eq. alpha: alpha = max|x| / 2^R, rounded to float32 (exact unless subnormal)."""
     return np.float32(float(maxabs) * 2.0 ** (-R))
+
+
+def luq_alpha_pw2(maxabs, R):
+    """Power-of-two alpha (Appendix, power-of-two LUQ): 2^ceil(log2 max|x|) / 2^R
+    as float32 -- exact, or 0 where 2^(ceil - R) is below half the smallest
+    float32 subnormal (it rounds to 0, as the plain alpha does there)."""
+    m = float(maxabs)
+    if not m > 0:
+        return np.float32(0.0)
+    mant, e = math.frexp(m)            # m = mant * 2^e, 0.5 <= mant < 1
+    c = e - 1 if mant == 0.5 else e    # ceil(log2 m)
+    return np.float32(math.ldexp(1.0, c - R))
 
 
 def luq_levels(alpha, R):
@@ -115,8 +133,8 @@ def luq_fields(a, alpha, R, j):
     return e.astype(np.uint8)
 
 
-def luq_quantize(x, dtype="f32", R=4, seed=0, counter=0, n_samples=1):
-    """Quantize a gradient tensor with LUQ.
+def luq_quantize(x, dtype="f32", R=4, seed=0, counter=0, n_samples=1, pw2=False):
+    """Quantize a gradient tensor with LUQ (with pw2: power-of-two LUQ).
 
     Returns (codes, alpha, maxabs): codes is uint8 of shape
     (n_samples, ceil(N/2)) -- one packed plane per SMP sample -- and alpha,
@@ -133,7 +151,7 @@ def luq_quantize(x, dtype="f32", R=4, seed=0, counter=0, n_samples=1):
         mx = np.float32(np.nan) if np.any(np.isnan(a)) else np.float32(np.inf)
         return codes, np.float32(np.nan), mx
     maxabs = np.float32(a.max())
-    alpha = luq_alpha(maxabs, R)
+    alpha = luq_alpha_pw2(maxabs, R) if pw2 else luq_alpha(maxabs, R)
     if alpha == 0:
         return codes, alpha, maxabs
     for s in range(n_samples):
@@ -159,7 +177,7 @@ def hindsight_update(maxabs, m_hat, eta):
         return np.float32(np.float32(c1 * np.float32(maxabs)) + np.float32(c0 * np.float32(m_hat)))
 
 
-def luq_quantize_hindsight(x, m_hat, dtype="f32", R=4, seed=0, counter=0, n_samples=1, eta=0.1):
+def luq_quantize_hindsight(x, m_hat, dtype="f32", R=4, seed=0, counter=0, n_samples=1, eta=0.1, pw2=False):
     """LUQ in one pass with the in-hindsight maximum (Section 4, "Reducing the
     data movement"; Appendix on hindsight).
 
@@ -169,7 +187,9 @@ def luq_quantize_hindsight(x, m_hat, dtype="f32", R=4, seed=0, counter=0, n_samp
     above alpha 2^R (the estimate may be below this tensor's maximum) take the
     top level with their sign, as does a NaN element; codes are otherwise
     those of ``luq_fields`` (Section 4).  A non-finite estimate gives alpha =
-    NaN and all codes 0, a zero estimate all codes 0.
+    NaN and all codes 0, a zero estimate all codes 0.  With pw2 the alpha of
+    the estimate is the power-of-two one (the combination of the appendix's
+    power-of-two LUQ with hindsight).
 
     Returns (codes, alpha, maxabs, m_next).
     """
@@ -177,7 +197,7 @@ def luq_quantize_hindsight(x, m_hat, dtype="f32", R=4, seed=0, counter=0, n_samp
     N = xf.size
     codes = np.zeros((n_samples, (N + 1) // 2), dtype=np.uint8)
     m = hindsight_estimate(m_hat)
-    alpha = np.float32(np.nan) if not np.isfinite(m) else luq_alpha(m, R)
+    alpha = np.float32(np.nan) if not np.isfinite(m) else (luq_alpha_pw2(m, R) if pw2 else luq_alpha(m, R))
     a = np.abs(xf.astype(np.float64))
     if N == 0:
         maxabs = np.float32(0.0)

@@ -189,3 +189,26 @@ def test_fwd_mutants_are_caught(monkeypatch):
     good_ref = G.gemm_fwd_ref
     monkeypatch.setattr(G, "gemm_fwd_ref", lambda xc, xs, xsig, wc, ws, *a, **k: good_ref(xc, xs, xsig, wc, 1.0, *a, **k))
     assert "closed" in _fwd_pin_fails()
+
+
+def test_pw2_floor_instead_of_ceil_is_caught(monkeypatch):
+    """alpha_PW2 with floor(log2 max) clips the maximum: the pin that the top
+    level is at or above max|x| rejects it, the real oracle passes it."""
+    from fractions import Fraction
+    import math
+
+    def top_at_or_above_max():
+        for m in [3.0, 1.5, 17.0, 1e-3, 123.456]:
+            x = np.array([m, -m / 3, m / 7], np.float32)
+            _, a, mx = L.luq_quantize(x, R=4, pw2=True)
+            if not Fraction(float(a)) * 16 >= Fraction(float(mx)):
+                return False
+        return True
+
+    assert top_at_or_above_max()
+
+    def floor_alpha(maxabs, R):
+        return np.float32(2.0 ** (math.floor(math.log2(float(maxabs))) - R))
+
+    monkeypatch.setattr(L, "luq_alpha_pw2", floor_alpha)
+    assert not top_at_or_above_max()
