@@ -26,7 +26,7 @@ GEMM y = Q(x) Q(W)^T (Eq. forward).
 random sign, 25% zeros; 0% and 50% zeros at 2^28): `value` is then the
 quantizer's mean fraction of the HBM roofline over the sizes >= 2^27, and
 `sweep` lists every size, with the single-pass in-hindsight variant
-(roofline N * s_in + N/2 bytes) beside it.
+(roofline N * s_in + N/2 bytes) and the power-of-two alpha beside it.
 """
 import argparse
 import json
@@ -219,6 +219,11 @@ def run_sweep(L, torch, steps, sizes=None):
         gr.replay()
         t = time_graph(torch, gr, max(3, steps // 4)) / per_graph
         alg = 2 * n * s_in + n / 2
+        # power-of-two alpha (same passes, same bytes)
+        fp = lambda: L.luq_quantize_grad(g, 4 | L.ALPHA_PW2, 0, 0, 1, codes, False, alpha, gmax, ws)
+        grp = capture(torch, [fp] * per_graph)
+        grp.replay()
+        tp = time_graph(torch, grp, max(3, steps // 4)) / per_graph
         # single pass with the in-hindsight maximum (the estimate starts at
         # this tensor's maximum, so every replay sees the same estimate)
         state = gmax.clone()
@@ -231,8 +236,9 @@ def run_sweep(L, torch, steps, sizes=None):
                      "GB/s": round(alg / t / 1e9, 1), "frac": round(alg / t / HBM_PEAK, 4),
                      "single_read_GB/s": round((n * s_in + n / 2) / t / 1e9, 1),
                      "hindsight_us": round(th * 1e6, 2), "hindsight_GB/s": round(alg1 / th / 1e9, 1),
-                     "hindsight_frac": round(alg1 / th / HBM_PEAK, 4)})
-        del g, codes, ws, gr, grh
+                     "hindsight_frac": round(alg1 / th / HBM_PEAK, 4),
+                     "pw2_us": round(tp * 1e6, 2), "pw2_frac": round(alg / tp / HBM_PEAK, 4)})
+        del g, codes, ws, gr, grh, grp
         torch.cuda.empty_cache()
     big = [r["frac"] for r in rows if r["log2_n"] >= min(27, max(sizes)) and r["zeros"] == 0.25]
     top = max((r for r in rows if r["zeros"] == 0.25 and r["dtype"] == "f32"), key=lambda r: r["log2_n"])

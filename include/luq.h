@@ -47,7 +47,7 @@
 extern "C" {
 #endif
 
-#define LUQ_ABI_VERSION 3
+#define LUQ_ABI_VERSION 4
 
 typedef int luq_status;
 enum {
@@ -62,6 +62,12 @@ enum {
 };
 
 typedef enum { LUQ_F32 = 0, LUQ_BF16 = 1 } luq_dtype;
+
+/* Or-ed into the R argument of the LUQ quantizers: power-of-two LUQ (the
+ * appendix on power-of-two LUQ), alpha = 2^ceil(log2 m) / 2^R instead of
+ * m / 2^R.  Every level is then a power of two and the top level is the
+ * least power of two at or above m, so the maximum is not clipped. */
+#define LUQ_ALPHA_PW2 0x100
 
 /* Operation ids for luq_workspace_size. */
 enum {
@@ -107,7 +113,9 @@ size_t luq_workspace_size(int op, int64_t d0, int64_t d1, int64_t d2);
  *  g        [rows][cols] row-major, dtype dt (LUQ_F32 or LUQ_BF16).
  *  rows, cols  >= 0.  For rows > 1, cols must be even.  When codes_t is
  *           requested, rows and cols must be multiples of 8.
- *  R        4, 5 or 6: levels alpha * 2^n for n = 0..R.
+ *  R        4, 5 or 6: levels alpha * 2^n for n = 0..R; or-ed with
+ *           LUQ_ALPHA_PW2 for the power-of-two alpha (alpha is then an
+ *           exact power of two, or 0 below the float32 subnormal range).
  *  seed, counter  Philox key and step counter; the codes are a pure
  *           function of (g, R, seed, counter, sample).
  *  n_samples  1 or 2 (SMP planes, Section 5.1).  2 requires R <= 5 so that
@@ -141,7 +149,9 @@ luq_status luq_quantize_grad(const void* g, luq_dtype dt, int64_t rows, int64_t 
  * tensor's maximum), and NaN elements, take the top code R + 1 with their
  * sign.  An estimate that is NaN or infinite gives alpha = NaN and all codes
  * 0; one that is 0 or negative gives alpha = 0 and all codes 0.  With
- * *state = max|g| the codes equal luq_quantize_grad's.
+ * *state = max|g| the codes equal luq_quantize_grad's.  R may carry
+ * LUQ_ALPHA_PW2: alpha is then the power-of-two alpha of the estimate (the
+ * appendix combines power-of-two LUQ with hindsight).
  *
  *  g, dt, rows, cols, R, seed, counter, n_samples, codes, codes_t
  *           as for luq_quantize_grad.

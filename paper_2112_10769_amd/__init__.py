@@ -18,6 +18,7 @@ LIB_PATH = os.path.join(_HERE, "libluq.so")
 
 LUQ_OK = 0
 LUQ_F32, LUQ_BF16 = 0, 1
+ALPHA_PW2 = 0x100  # or-ed into R: power-of-two alpha
 OP_QUANTIZE_GRAD, OP_INT4_QUANTIZE, OP_GEMM_DGRAD, OP_GEMM_WGRAD, OP_GEMM_FWD = 0, 1, 2, 3, 4
 
 EXPORTS = (
@@ -113,10 +114,11 @@ def _shape2d(x):
 
 
 def luq_quantize_grad(g, R=4, seed=0, counter=0, n_samples=1, codes=True, codes_t=False,
-                      alpha=None, maxabs=None, ws=None):
+                      alpha=None, maxabs=None, ws=None, pw2=False):
     """LUQ codes of g (2-D [rows, cols] or 1-D).  codes / codes_t: True to
-    allocate, a uint8 tensor to write into, or False.  Returns
-    (codes, codes_t, alpha, maxabs) with codes of shape [n_samples, plane]."""
+    allocate, a uint8 tensor to write into, or False; pw2 for the
+    power-of-two alpha.  Returns (codes, codes_t, alpha, maxabs) with codes of
+    shape [n_samples, plane]."""
     rows, cols = _shape2d(g)
     n = rows * cols
     dev = g.device
@@ -132,7 +134,7 @@ def luq_quantize_grad(g, R=4, seed=0, counter=0, n_samples=1, codes=True, codes_
     wsb = workspace_size(OP_QUANTIZE_GRAD, n)
     ws = _bytes(wsb, dev) if ws is None else ws
     g = g.contiguous()
-    st = LIB.luq_quantize_grad(_ptr(g) if n else None, _dtype(g), rows, cols, R,
+    st = LIB.luq_quantize_grad(_ptr(g) if n else None, _dtype(g), rows, cols, R | (ALPHA_PW2 if pw2 else 0),
                                seed & (2**64 - 1), counter & 0xFFFFFFFF, n_samples,
                                _ptr(codes), _ptr(codes_t), _ptr(alpha), _ptr(maxabs), _ptr(ws),
                                ws.numel(), _stream(dev))
@@ -141,10 +143,11 @@ def luq_quantize_grad(g, R=4, seed=0, counter=0, n_samples=1, codes=True, codes_
 
 
 def luq_quantize_grad_hindsight(g, state, R=4, seed=0, counter=0, n_samples=1, eta=0.1, codes=True,
-                                codes_t=False, alpha=None, maxabs=None, ws=None):
+                                codes_t=False, alpha=None, maxabs=None, ws=None, pw2=False):
     """Single-pass LUQ with the in-hindsight maximum: alpha from the estimate
     in `state` (a 1-element float32 device tensor, updated in place to the
-    next estimate).  Returns (codes, codes_t, alpha, maxabs)."""
+    next estimate); pw2 for the power-of-two alpha of the estimate.  Returns
+    (codes, codes_t, alpha, maxabs)."""
     rows, cols = _shape2d(g)
     n = rows * cols
     dev = g.device
@@ -160,7 +163,8 @@ def luq_quantize_grad_hindsight(g, state, R=4, seed=0, counter=0, n_samples=1, e
     wsb = workspace_size(OP_QUANTIZE_GRAD, n)
     ws = _bytes(wsb, dev) if ws is None else ws
     g = g.contiguous()
-    st = LIB.luq_quantize_grad_hindsight(_ptr(g) if n else None, _dtype(g), rows, cols, R,
+    st = LIB.luq_quantize_grad_hindsight(_ptr(g) if n else None, _dtype(g), rows, cols,
+                                         R | (ALPHA_PW2 if pw2 else 0),
                                          seed & (2**64 - 1), counter & 0xFFFFFFFF, n_samples, float(eta),
                                          _ptr(codes), _ptr(codes_t), _ptr(state), _ptr(alpha), _ptr(maxabs),
                                          _ptr(ws), ws.numel(), _stream(dev))

@@ -84,6 +84,8 @@ luq_status luq_quantize_grad(const void* g, luq_dtype dt, int64_t rows, int64_t 
   if (dt != LUQ_F32 && dt != LUQ_BF16) return fail(LUQ_ERR_DTYPE, "%s: dtype", "luq_quantize_grad");
   luq_status st = check_matrix(rows, cols, codes_t != nullptr, "luq_quantize_grad");
   if (st != LUQ_OK) return st;
+  const int pw2 = (R & LUQ_ALPHA_PW2) ? 1 : 0;
+  R &= ~LUQ_ALPHA_PW2;
   if (R < 4 || R > 6) return fail(LUQ_ERR_PARAM, "%s: R must be 4, 5 or 6", "luq_quantize_grad");
   if (n_samples != 1 && n_samples != 2)
     return fail(LUQ_ERR_PARAM, "%s: n_samples must be 1 or 2", "luq_quantize_grad");
@@ -102,7 +104,7 @@ luq_status luq_quantize_grad(const void* g, luq_dtype dt, int64_t rows, int64_t 
   }
   if (!aligned4(alpha) || !aligned4(maxabs))
     return fail(LUQ_ERR_ALIGN, "%s: alpha / maxabs misaligned", "luq_quantize_grad");
-  return hip_status(luq::launch_luq_quantize(g, dt == LUQ_BF16, rows, cols, R, seed, counter,
+  return hip_status(luq::launch_luq_quantize(g, dt == LUQ_BF16, rows, cols, R, pw2, seed, counter,
                                              n_samples, codes, codes_t, alpha, maxabs, ws,
                                              static_cast<hipStream_t>(stream)));
 }
@@ -116,6 +118,8 @@ luq_status luq_quantize_grad_hindsight(const void* g, luq_dtype dt, int64_t rows
   if (dt != LUQ_F32 && dt != LUQ_BF16) return fail(LUQ_ERR_DTYPE, "%s: dtype", fn);
   luq_status st = check_matrix(rows, cols, codes_t != nullptr, fn);
   if (st != LUQ_OK) return st;
+  const int pw2 = (R & LUQ_ALPHA_PW2) ? 1 : 0;
+  R &= ~LUQ_ALPHA_PW2;
   if (R < 4 || R > 6) return fail(LUQ_ERR_PARAM, "%s: R must be 4, 5 or 6", fn);
   if (n_samples != 1 && n_samples != 2) return fail(LUQ_ERR_PARAM, "%s: n_samples must be 1 or 2", fn);
   if (n_samples == 2 && R > 5) return fail(LUQ_ERR_PARAM, "%s: n_samples = 2 needs R <= 5", fn);
@@ -133,7 +137,7 @@ luq_status luq_quantize_grad_hindsight(const void* g, luq_dtype dt, int64_t rows
   }
   if (!aligned4(alpha) || !aligned4(maxabs) || !aligned4(state))
     return fail(LUQ_ERR_ALIGN, "%s: alpha / maxabs / state misaligned", fn);
-  return hip_status(luq::launch_luq_quantize_hindsight(g, dt == LUQ_BF16, rows, cols, R, seed, counter, n_samples,
+  return hip_status(luq::launch_luq_quantize_hindsight(g, dt == LUQ_BF16, rows, cols, R, pw2, seed, counter, n_samples,
                                                        eta, codes, codes_t, state, alpha, maxabs, ws,
                                                        static_cast<hipStream_t>(stream)));
 }

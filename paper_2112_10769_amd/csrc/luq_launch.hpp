@@ -16,12 +16,12 @@ inline size_t plane_bytes(int64_t n) {
 
 size_t quant_workspace_bytes(int64_t n);
 
-hipError_t launch_luq_quantize(const void* g, int bf16, int64_t rows, int64_t cols, int R,
+hipError_t launch_luq_quantize(const void* g, int bf16, int64_t rows, int64_t cols, int R, int pw2,
                                uint64_t seed, uint32_t counter, int ns, uint8_t* codes,
                                uint8_t* codes_t, float* alpha, float* maxabs, void* ws,
                                hipStream_t st);
 
-hipError_t launch_luq_quantize_hindsight(const void* g, int bf16, int64_t rows, int64_t cols, int R,
+hipError_t launch_luq_quantize_hindsight(const void* g, int bf16, int64_t rows, int64_t cols, int R, int pw2,
                                          uint64_t seed, uint32_t counter, int ns, float eta, uint8_t* codes,
                                          uint8_t* codes_t, float* state, float* alpha, float* maxabs, void* ws,
                                          hipStream_t st);

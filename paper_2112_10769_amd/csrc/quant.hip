@@ -197,18 +197,30 @@ __device__ __forceinline__ void encode_tiles(const Enc& enc, int64_t rows, int64
 struct LuqParams {
   float alpha_s;    // alpha * S
   float alpha16_s;  // alpha * S * 2^-16
-  float ltop_s;     // alpha * S * 2^R
   float S;          // 1 or 2^100
   uint32_t a_bits;  // bits of alpha_s
   uint32_t a16_bits;
-  uint32_t e_alpha;  // biased exponent of alpha_s
-  uint32_t m_alpha;  // mantissa field of alpha_s
   uint32_t top_field;
   bool zero;  // every code is 0 (alpha == 0, or non-finite input)
 };
 
-// Eq. alpha: alpha = fl32(m * 2^-R).  `alpha_out` gets the unscaled alpha.
-__device__ __forceinline__ LuqParams luq_params(uint32_t mbits, int R, float* alpha_out) {
+// Power-of-two alpha (Appendix, power-of-two LUQ): 2^(ceil(log2 m) - R) for
+// a finite m > 0, from the bits of m: the exponent of a normal m, or the
+// position of the top mantissa bit of a subnormal one, plus one unless m is
+// a power of two.  Below the float32 subnormal range it is 0 (half the
+// smallest subnormal rounds to 0 as well).
+__device__ __forceinline__ float pw2_alpha(uint32_t mbits, int R) {
+  if (mbits == 0) return 0.0f;
+  const uint32_t e = mbits >> 23, mant = mbits & 0x7FFFFFu;
+  const int c = e ? (int)e - 127 + (mant != 0) : (31 - __clz((int)mant)) - 149 + ((mant & (mant - 1)) != 0);
+  const int k = c - R;
+  if (k >= -126) return __uint_as_float((uint32_t)(k + 127) << 23);
+  return k >= -149 ? __uint_as_float(1u << (k + 149)) : 0.0f;
+}
+
+// Eq. alpha: alpha = fl32(m * 2^-R), or with pw2 the power-of-two alpha.
+// `alpha_out` gets the unscaled alpha.
+__device__ __forceinline__ LuqParams luq_params(uint32_t mbits, int R, bool pw2, float* alpha_out) {
   LuqParams p;
   const float m = __uint_as_float(mbits);
   float alpha;
@@ -216,18 +228,16 @@ __device__ __forceinline__ LuqParams luq_params(uint32_t mbits, int R, float* al
     alpha = __uint_as_float(0x7FC00000u);  // NaN
     p.zero = true;
   } else {
-    alpha = m * __uint_as_float((uint32_t)(127 - R) << 23);  // exact 2^-R scale, one rounding
+    alpha = pw2 ? pw2_alpha(mbits, R)
+                : m * __uint_as_float((uint32_t)(127 - R) << 23);  // exact 2^-R scale, one rounding
     p.zero = (alpha == 0.0f);
   }
   *alpha_out = alpha;
   p.S = (m < 0x1p-90f) ? 0x1p100f : 1.0f;
   p.alpha_s = alpha * p.S;
   p.alpha16_s = p.alpha_s * 0x1p-16f;
-  p.ltop_s = p.alpha_s * __uint_as_float((uint32_t)(127 + R) << 23);
   p.a_bits = __float_as_uint(p.alpha_s);
   p.a16_bits = __float_as_uint(p.alpha16_s);
-  p.e_alpha = p.a_bits >> 23;
-  p.m_alpha = p.a_bits & 0x7FFFFFu;
   p.top_field = (uint32_t)R + 1;
   return p;
 }
@@ -297,6 +307,7 @@ struct LuqArgs {
   const void* g;
   int64_t rows, cols, n;
   int R;
+  bool pw2;  // power-of-two alpha
   uint32_t k0, k1, counter;
   const uint32_t* partial;
   int nparts;
@@ -323,7 +334,7 @@ __device__ __forceinline__ LuqParams luq_block_params(const LuqArgs& a) {
   __shared__ uint32_t scratch[kThreads / kWave];
   const uint32_t mbits = HS ? estimate_key(*a.state) : reduce_partials(a.partial, a.nparts, scratch);
   float alpha;
-  const LuqParams p = luq_params(mbits, a.R, &alpha);
+  const LuqParams p = luq_params(mbits, a.R, a.pw2, &alpha);
   if (!HS && blockIdx.x == 0 && threadIdx.x == 0) {
     *a.alpha_out = alpha;
     if (a.max_out) *a.max_out = __uint_as_float(mbits);
@@ -437,13 +448,13 @@ __global__ __launch_bounds__(kThreads) void luq_encode_tile_kernel(LuqArgs a, in
 // with c1 = fl32(1 - eta), c0 = eta.
 __global__ __launch_bounds__(1024) void hindsight_fold_kernel(const uint32_t* __restrict__ part, int nparts,
                                                              float* state, float c1, float c0, int R,
-                                                             float* alpha_out, float* maxabs_out) {
+                                                             bool pw2, float* alpha_out, float* maxabs_out) {
   __shared__ uint32_t scratch[1024 / kWave];
   const uint32_t m = reduce_partials(part, nparts, scratch);
   if (threadIdx.x == 0) {
     const uint32_t mkey = estimate_key(*state);
     float alpha;
-    (void)luq_params(mkey, R, &alpha);
+    (void)luq_params(mkey, R, pw2, &alpha);
     const float mx = __uint_as_float(m);
     *alpha_out = alpha;
     if (maxabs_out) *maxabs_out = mx;
@@ -664,7 +675,7 @@ static hipError_t luq_launch_t(LuqArgs a, int ns, int nmax, hipStream_t st) {
   return hipGetLastError();
 }
 
-hipError_t launch_luq_quantize(const void* g, int bf16, int64_t rows, int64_t cols, int R,
+hipError_t launch_luq_quantize(const void* g, int bf16, int64_t rows, int64_t cols, int R, int pw2,
                                uint64_t seed, uint32_t counter, int ns, uint8_t* codes,
                                uint8_t* codes_t, float* alpha, float* maxabs, void* ws,
                                hipStream_t st) {
@@ -679,6 +690,7 @@ hipError_t launch_luq_quantize(const void* g, int bf16, int64_t rows, int64_t co
   a.cols = cols;
   a.n = n;
   a.R = R;
+  a.pw2 = pw2 != 0;
   a.k0 = (uint32_t)seed;
   a.k1 = (uint32_t)(seed >> 32);
   a.counter = counter;
@@ -712,7 +724,7 @@ static int luq_hindsight_encode(const LuqArgs& a, int ns, hipStream_t st) {
   return nb;
 }
 
-hipError_t launch_luq_quantize_hindsight(const void* g, int bf16, int64_t rows, int64_t cols, int R,
+hipError_t launch_luq_quantize_hindsight(const void* g, int bf16, int64_t rows, int64_t cols, int R, int pw2,
                                          uint64_t seed, uint32_t counter, int ns, float eta, uint8_t* codes,
                                          uint8_t* codes_t, float* state, float* alpha, float* maxabs, void* ws,
                                          hipStream_t st) {
@@ -723,6 +735,7 @@ hipError_t launch_luq_quantize_hindsight(const void* g, int bf16, int64_t rows, 
   a.cols = cols;
   a.n = n;
   a.R = R;
+  a.pw2 = pw2 != 0;
   a.k0 = (uint32_t)seed;
   a.k1 = (uint32_t)(seed >> 32);
   a.counter = counter;
@@ -742,7 +755,7 @@ hipError_t launch_luq_quantize_hindsight(const void* g, int bf16, int64_t rows, 
                    : (nt ? luq_hindsight_encode<false, true>(a, ns, st) : luq_hindsight_encode<false, false>(a, ns, st));
   }
   hipLaunchKernelGGL(hindsight_fold_kernel, dim3(1), dim3(1024), 0, st, a.part_out, nblocks, state,
-                     1.0f - eta, eta, R, alpha, maxabs);  // c1 = fl32(1 - eta) (host float arithmetic)
+                     1.0f - eta, eta, R, pw2 != 0, alpha, maxabs);  // c1 = fl32(1 - eta) (host float arithmetic)
   return hipGetLastError();
 }
 

@@ -82,9 +82,11 @@ def _qg(**kw):
     (dict(rows=16, cols=12, codes_t=P2), 2),
     (dict(rows=2**40, cols=2**40), 2),
     (dict(R=3), 4), (dict(R=7), 4),
+    (dict(R=3 | 0x100), 4), (dict(R=4 | 0x200), 4), (dict(R=0x105, ns=2, g=PMIS), 6),
     (dict(ns=3), 4), (dict(ns=0), 4),
-    (dict(ns=2, R=6), 4),
+    (dict(ns=2, R=6), 4), (dict(ns=2, R=6 | 0x100), 4),
     (dict(alpha=NUL), 1),
+    (dict(R=0x104, alpha=NUL), 1),
     (dict(g=NUL), 1),
     (dict(codes=NUL, codes_t=NUL), 1),
     (dict(ws=NUL), 5),
