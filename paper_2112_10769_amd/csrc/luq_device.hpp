@@ -52,6 +52,14 @@ struct U8 {
 
 typedef uint32_t v4u32 __attribute__((ext_vector_type(4)));
 
+// One code word at p (4-byte aligned); NT marks the store non-temporal (the
+// codes of a tensor too large for the last-level cache).
+template <bool NT>
+__device__ __forceinline__ void store_word(uint8_t* p, uint32_t v) {
+  if constexpr (NT) __builtin_nontemporal_store(v, reinterpret_cast<uint32_t*>(p));
+  else *reinterpret_cast<uint32_t*>(p) = v;
+}
+
 // 16 bytes at p; NT marks the load non-temporal (streaming data read once).
 template <bool NT>
 __device__ __forceinline__ v4u32 load16(const void* p) {
@@ -124,11 +132,21 @@ __device__ __forceinline__ uint32_t block_max_u32(uint32_t v, uint32_t* scratch)
   return m;
 }
 
-// Max of the per-block partial keys written by a max pass.
+// Max of the per-block partial keys written by a max pass.  Eight loads per
+// thread are in flight at once: indices past the end are clamped to the last
+// partial, which leaves the maximum unchanged and keeps every load in bounds
+// (a conditional load would make each one wait for the previous).
 __device__ __forceinline__ uint32_t reduce_partials(const uint32_t* partial, int nparts,
                                                     uint32_t* scratch) {
   uint32_t m = 0;
-  for (int i = threadIdx.x; i < nparts; i += blockDim.x) m = max(m, partial[i]);
+  const int step = blockDim.x;
+  for (int i0 = threadIdx.x; i0 < nparts; i0 += 8 * step) {
+    uint32_t v[8];
+#pragma unroll
+    for (int k = 0; k < 8; ++k) v[k] = partial[min(i0 + k * step, nparts - 1)];
+#pragma unroll
+    for (int k = 0; k < 8; ++k) m = max(m, v[k]);
+  }
   return block_max_u32(m, scratch);
 }
 

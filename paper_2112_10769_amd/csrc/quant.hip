@@ -89,15 +89,16 @@ __global__ __launch_bounds__(kThreads) void max_partial_kernel(const void* __res
   if (threadIdx.x == 0) partial[blockIdx.x] = r;
 }
 
-// Folds `nparts` (<= 16 * 1024) partial keys into one (one block): each
-// thread reads its 16 consecutive keys with independent loads.
+// Folds `nparts` (1 .. 16 * 1024) partial keys into one (one block): each
+// thread reads 16 keys with independent loads (indices past the end are
+// clamped to the last key, which leaves the maximum unchanged).
 __global__ __launch_bounds__(1024) void fold_partials_kernel(const uint32_t* __restrict__ partial, int nparts,
                                                             uint32_t* __restrict__ out) {
   __shared__ uint32_t scratch[1024 / kWave];
-  const int i0 = threadIdx.x * 16;
+  const int i0 = threadIdx.x;
   uint32_t v[16];
 #pragma unroll
-  for (int k = 0; k < 16; ++k) v[k] = i0 + k < nparts ? partial[i0 + k] : 0u;
+  for (int k = 0; k < 16; ++k) v[k] = partial[min(i0 + k * 1024, nparts - 1)];
   uint32_t m = 0;
 #pragma unroll
   for (int k = 0; k < 16; ++k) m = max(m, v[k]);
@@ -164,7 +165,7 @@ __device__ __forceinline__ void encode_tiles(const Enc& enc, int64_t rows, int64
 #pragma unroll
           for (int s = 0; s < NS; ++s) {
             w[s] = enc.word(v[u], (uint64_t)(e0[u] >> 3), s);
-            if (codes) *reinterpret_cast<uint32_t*>(codes + s * plane + (e0[u] >> 1)) = w[s];
+            if (codes) store_word<Enc::kNT>(codes + s * plane + (e0[u] >> 1), w[s]);
           }
         }
 #pragma unroll
@@ -185,7 +186,7 @@ __device__ __forceinline__ void encode_tiles(const Enc& enc, int64_t rows, int64
         transpose8x8_nibbles(w8);
         uint8_t* dst = codes_t + s * plane + (cg * 8) * (rows >> 1) + (row0 >> 1);
 #pragma unroll
-        for (int c = 0; c < 8; ++c) *reinterpret_cast<uint32_t*>(dst + c * (rows >> 1)) = w8[c];
+        for (int c = 0; c < 8; ++c) store_word<Enc::kNT>(dst + c * (rows >> 1), w8[c]);
       }
     }
     __syncthreads();
@@ -195,11 +196,10 @@ __device__ __forceinline__ void encode_tiles(const Enc& enc, int64_t rows, int64
 // ------------------------------- LUQ ---------------------------------------
 
 struct LuqParams {
-  float alpha_s;    // alpha * S
-  float alpha16_s;  // alpha * S * 2^-16
-  float S;          // 1 or 2^100
-  uint32_t a_bits;  // bits of alpha_s
-  uint32_t a16_bits;
+  float alpha_s;     // alpha * S
+  float S;           // 1 or 2^100
+  uint32_t a1_bits;  // bits of alpha_s / 2
+  uint32_t w16_bits;  // bits of alpha_s * 2^-17
   uint32_t top_field;
   bool zero;  // every code is 0 (alpha == 0, or non-finite input)
 };
@@ -219,7 +219,8 @@ __device__ __forceinline__ float pw2_alpha(uint32_t mbits, int R) {
 }
 
 // Eq. alpha: alpha = fl32(m * 2^-R), or with pw2 the power-of-two alpha.
-// `alpha_out` gets the unscaled alpha.
+// `alpha_out` gets the unscaled alpha.  alpha_s * 2^-17 is a normal float
+// (alpha_s >= 2^-96 unscaled, and tiny maxima are scaled by 2^100).
 __device__ __forceinline__ LuqParams luq_params(uint32_t mbits, int R, bool pw2, float* alpha_out) {
   LuqParams p;
   const float m = __uint_as_float(mbits);
@@ -235,47 +236,16 @@ __device__ __forceinline__ LuqParams luq_params(uint32_t mbits, int R, bool pw2,
   *alpha_out = alpha;
   p.S = (m < 0x1p-90f) ? 0x1p100f : 1.0f;
   p.alpha_s = alpha * p.S;
-  p.alpha16_s = p.alpha_s * 0x1p-16f;
-  p.a_bits = __float_as_uint(p.alpha_s);
-  p.a16_bits = __float_as_uint(p.alpha16_s);
+  p.a1_bits = __float_as_uint(p.alpha_s * 0.5f);
+  p.w16_bits = __float_as_uint(p.alpha_s * 0x1p-17f);
   p.top_field = (uint32_t)R + 1;
   return p;
 }
 
-// One element's 3-bit LUQ exponent field from its float32 bits and 16-bit
-// uniform.
-//
-// On scaled magnitudes (both normal once |x| >= alpha), the difference of the
-// float bit patterns D = bits(|x|) - bits(alpha) has D >> 23 equal to
-// floor(log2(|x| / alpha)): the exponent difference, less one when the
-// mantissa of |x| is below that of alpha (the borrow).  So n = D >> 23 is the
-// bin index, n < 0 is the underflow bin [0, alpha) and n = R the top level.
-// The bin width is w = alpha * 2^max(n, 0), built (times 2^-16) by adding
-// max(n, 0) to the exponent field of alpha * 2^-16; the lower level is w, or
-// 0 in the underflow bin, so lo - |x| = fma(w * 2^-16, 2^16 or 0, -|x|), which
-// is exact.  The field is max(n, -1) + 1 + up.  Unscaled, |x| <= max =
-// alpha * 2^R exactly, so n <= R and at n = R the offset d is 0 and `up` is
-// false: the field never exceeds R + 1.  Scaled, alpha may have been rounded
-// (subnormal alpha), and with an estimated maximum (CAP) magnitudes, Inf and
-// NaN may lie above the top level, so the field is capped at R + 1 (the top
-// code, with the element's sign).
-template <bool SCALED, bool CAP = false>
-__device__ __forceinline__ uint32_t luq_field(uint32_t b, uint32_t j, const LuqParams& p) {
-  const float mag = fabsf(__uint_as_float(b));
-  const float as = SCALED ? mag * p.S : mag;
-  const int32_t n = ((int32_t)__float_as_uint(as) - (int32_t)p.a_bits) >> 23;
-  const bool su = n < 0;
-  const float w16 = __uint_as_float(p.a16_bits + ((uint32_t)max(n, 0) << 23));
-  const float c = fmaf(w16, su ? 0.0f : 0x1p16f, -as);  // lo - |x|, exact
-  const bool up = fmaf((float)j, w16, c) < 0.0f;
-  const int32_t f = max(n, -1) + 1 + (int32_t)up;
-  return (uint32_t)(SCALED || CAP ? min(f, (int32_t)p.top_field) : f);
-}
-
-// Sign bits of 8 elements at the sign position of their nibbles (bit 4e+3):
-// the top bytes of the odd elements are gathered as they are (bit 7 of byte k
-// is element 2k+1's sign), those of the even elements are gathered and
-// rotated right by 4 bits.  Other bits are garbage and masked by the caller.
+// Sign bits of 8 words at the sign position of their nibbles (bit 4e+3):
+// the top bytes of the odd words are gathered as they are (bit 7 of byte k
+// is word 2k+1's sign), those of the even words are gathered and rotated
+// right by 4 bits.  Other bits are garbage and masked by the caller.
 __device__ __forceinline__ uint32_t gather_signs(const U8& v) {
   const uint32_t odd = __builtin_amdgcn_perm(v.v[3], v.v[1], 0x0C0C0703u) |
                        __builtin_amdgcn_perm(v.v[7], v.v[5], 0x07030C0Cu);
@@ -284,21 +254,65 @@ __device__ __forceinline__ uint32_t gather_signs(const U8& v) {
   return (odd & 0x80808080u) | (__builtin_amdgcn_alignbit(even, even, 4) & 0x08080808u);
 }
 
-// Codes of 8 consecutive elements (bits in v) for Philox block `blk`: the
-// exponent fields are packed first, then each sign bit is set where its field
-// is non-zero (zero is always +0).
+// [n >= 1] in one instruction (the compiler would otherwise emit a compare
+// and a select).
+__device__ __forceinline__ uint32_t med3_01(int32_t n) {
+  uint32_t r;
+  asm("v_med3_i32 %0, %1, 0, 1" : "=v"(r) : "v"(n));
+  return r;
+}
+
+// Codes of 8 consecutive elements (bits in v) for Philox block `blk`.
+//
+// Per element, on the magnitude a (scaled by S when SCALED; both a and alpha
+// normal once a >= alpha): the difference of the float bit patterns
+// bits(a) - bits(alpha / 2), shifted right by 23, is n1 = n + 1 with
+// n = floor(log2(a / alpha)) -- the exponent difference, less one when the
+// mantissa of a is below that of alpha (the borrow).  n1 <= 0 is the
+// underflow bin [0, alpha) (lower level 0), n1 >= 1 the bin
+// [alpha 2^n, alpha 2^(n+1)) (lower level = width = alpha 2^n), and the base
+// field is max(n1, 0).  With w16 = width * 2^-16 (alpha * 2^-17 with
+// max(n1, 1) added to its exponent) and jj = j + 2^16 [n1 >= 1], the exact
+// value jj * w16 - a equals (j * w - d * 2^16) * 2^-16 for the offset d of a
+// above the lower level; the fused multiply-add rounds it once, so its sign
+// is that of j * w - d * 2^16 and the value rounds up exactly when the sign
+// bit is set (a zero result is +0: no round-up).  The round-up bits are
+// gathered from the sign bits and added to the packed base fields.
+//
+// Unscaled, a <= max <= alpha * 2^R (equal for the plain alpha, which is
+// exact there), so n1 <= R + 1 and at n1 = R + 1 the offset is 0: the field
+// never exceeds R + 1.  Scaled, alpha may have been rounded (subnormal alpha), and
+// with an estimated maximum (CAP) magnitudes, Inf and NaN may lie above the
+// top level: there the base field is clamped to R + 1 and the round-up bit
+// of top-level elements is dropped (the top code, with the element's sign).
+// Each sign bit is then set where the field is non-zero (zero is always +0).
 template <bool SCALED, bool CAP = false>
 __device__ __forceinline__ uint32_t luq_word(const U8& v, uint64_t blk, uint32_t sample,
                                              uint32_t counter, uint32_t k0, uint32_t k1,
                                              const LuqParams& p) {
+  constexpr bool kClamp = SCALED || CAP;
   const U4 y = philox4x32_10(U4{(uint32_t)blk, (uint32_t)(blk >> 32), sample, counter}, k0, k1);
   const uint32_t w[4] = {y.x, y.y, y.z, y.w};
-  uint32_t fields = 0;
+  uint32_t base = 0;
+  U8 r;
 #pragma unroll
   for (int e = 0; e < 8; ++e) {
-    const uint32_t j = (e & 1) ? (w[e >> 1] >> 16) : (w[e >> 1] & 0xFFFFu);
-    fields |= luq_field<SCALED, CAP>(v.v[e], j, p) << (4 * e);
+    const uint32_t ab = SCALED ? __float_as_uint(fabsf(__uint_as_float(v.v[e])) * p.S) : (v.v[e] & 0x7FFFFFFFu);
+    const int32_t n1 = ((int32_t)ab - (int32_t)p.a1_bits) >> 23;
+    const int32_t f0 = kClamp ? min(max(n1, 0), (int32_t)p.top_field) : max(n1, 0);
+    const uint32_t ge = med3_01(n1);
+    const float w16 = __uint_as_float(p.w16_bits + ((uint32_t)max(n1, 1) << 23));
+    const uint32_t jj = (e & 1) ? __builtin_amdgcn_alignbit(ge, w[e >> 1], 16)
+                                : __builtin_amdgcn_perm(ge, w[e >> 1], 0x05040100u);
+    r.v[e] = __float_as_uint(fmaf((float)jj, w16, -__uint_as_float(ab)));
+    base |= (uint32_t)f0 << (4 * e);
   }
+  uint32_t up = (gather_signs(r) >> 3) & 0x11111111u;
+  if constexpr (kClamp) {
+    const uint32_t t = base ^ (0x11111111u * p.top_field);
+    up &= (t | (t >> 1) | (t >> 2));  // bit 4e set unless field e is the top one
+  }
+  const uint32_t fields = base + up;
   const uint32_t nz = (fields | (fields >> 1) | (fields >> 2)) & 0x11111111u;
   return fields | (gather_signs(v) & (nz << 3));
 }
@@ -350,17 +364,29 @@ __device__ __forceinline__ uint32_t luq_flat_body(const LuqArgs& a, const LuqPar
   const int64_t nfull = a.n >> 3;
   const int64_t stride = (int64_t)gridDim.x * kThreads;
   int64_t g = (int64_t)blockIdx.x * kThreads + threadIdx.x;
-  // two groups per trip: both loads are in flight before either is encoded
+  // four groups per trip (then two): every load of a trip is in flight before
+  // any of its groups is encoded
+  for (; g + 3 * stride < nfull; g += 4 * stride) {
+    U8 v[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) v[u] = load8<BF16, NT>(a.g, (g + u * stride) * 8);
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      if (HS) mx = max(mx, max_key8(v[u]));
+#pragma unroll
+      for (int s = 0; s < NS; ++s)
+        store_word<NT>(a.codes + s * a.plane + (g + u * stride) * 4, luq_word<SCALED, HS>(v[u], (uint64_t)(g + u * stride), s, a.counter, a.k0, a.k1, p));
+    }
+  }
   for (; g + stride < nfull; g += 2 * stride) {
     const U8 v0 = load8<BF16, NT>(a.g, g * 8);
     const U8 v1 = load8<BF16, NT>(a.g, (g + stride) * 8);
     if (HS) mx = max(mx, max(max_key8(v0), max_key8(v1)));
 #pragma unroll
     for (int s = 0; s < NS; ++s) {
-      *reinterpret_cast<uint32_t*>(a.codes + s * a.plane + g * 4) =
-          luq_word<SCALED, HS>(v0, (uint64_t)g, s, a.counter, a.k0, a.k1, p);
-      *reinterpret_cast<uint32_t*>(a.codes + s * a.plane + (g + stride) * 4) =
-          luq_word<SCALED, HS>(v1, (uint64_t)(g + stride), s, a.counter, a.k0, a.k1, p);
+      store_word<NT>(a.codes + s * a.plane + g * 4, luq_word<SCALED, HS>(v0, (uint64_t)g, s, a.counter, a.k0, a.k1, p));
+      store_word<NT>(a.codes + s * a.plane + (g + stride) * 4,
+                     luq_word<SCALED, HS>(v1, (uint64_t)(g + stride), s, a.counter, a.k0, a.k1, p));
     }
   }
   if (g < nfull) {
@@ -368,8 +394,7 @@ __device__ __forceinline__ uint32_t luq_flat_body(const LuqArgs& a, const LuqPar
     if (HS) mx = max(mx, max_key8(v));
 #pragma unroll
     for (int s = 0; s < NS; ++s)
-      *reinterpret_cast<uint32_t*>(a.codes + s * a.plane + g * 4) =
-          luq_word<SCALED, HS>(v, (uint64_t)g, s, a.counter, a.k0, a.k1, p);
+      store_word<NT>(a.codes + s * a.plane + g * 4, luq_word<SCALED, HS>(v, (uint64_t)g, s, a.counter, a.k0, a.k1, p));
   }
   if ((a.n & 7) && blockIdx.x == 0 && threadIdx.x == 0) {
     const U8 v = load8_tail<BF16>(a.g, nfull * 8, a.n);  // missing elements read +0
@@ -420,6 +445,7 @@ __global__ __launch_bounds__(kThreads) void luq_encode_flat_kernel(LuqArgs a) {
 template <bool BF16, bool NT, bool SCALED, bool HS = false>
 struct LuqEnc {
   static constexpr bool kTrack = HS;
+  static constexpr bool kNT = NT;
   const LuqArgs* a;
   const LuqParams* p;
   __device__ U8 load(int64_t e0) const { return load8<BF16, NT>(a->g, e0); }
@@ -544,7 +570,7 @@ __global__ __launch_bounds__(kThreads) void int4_encode_flat_kernel(Int4Args a) 
     const U8 v = full ? load8<BF16, NT>(a.x, g * 8) : load8_tail<BF16>(a.x, g * 8, a.n);
     const uint32_t word = p.zero ? 0u : int4_word(v, p);
     if (full)
-      *reinterpret_cast<uint32_t*>(a.codes + g * 4) = word;
+      store_word<NT>(a.codes + g * 4, word);
     else
       store_bytes(a.codes + g * 4, word, (int)((a.n - g * 8 + 1) >> 1));
   }
@@ -553,6 +579,7 @@ __global__ __launch_bounds__(kThreads) void int4_encode_flat_kernel(Int4Args a) 
 template <bool BF16, bool NT>
 struct Int4Enc {
   static constexpr bool kTrack = false;
+  static constexpr bool kNT = NT;
   const Int4Args* a;
   const Int4Params* p;
   __device__ U8 load(int64_t e0) const { return load8<BF16, NT>(a->x, e0); }
@@ -643,7 +670,8 @@ static const uint32_t* encode_partials(const uint32_t* partial, int nblocks, int
 }
 
 // Encode pass.  Its read is the tensor's second; it is non-temporal exactly
-// when the max pass's was (tensors too large to stay in the last-level cache).
+// when the max pass's was (tensors too large to stay in the last-level cache),
+// and so are its code stores then.
 static bool stream_reads(int64_t n, bool bf16) { return n * (bf16 ? 2 : 4) > kCacheBytes; }
 
 template <bool BF16, bool NT>
