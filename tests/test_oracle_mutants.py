@@ -212,3 +212,39 @@ def test_pw2_floor_instead_of_ceil_is_caught(monkeypatch):
 
     monkeypatch.setattr(L, "luq_alpha_pw2", floor_alpha)
     assert not top_at_or_above_max()
+
+
+def test_conv_dgrad_tap_mistakes_are_caught(monkeypatch):
+    """A gradient that reads the tap offsets with the wrong sign, or drops a
+    border tap, fails the adjoint pin against scipy's correlation."""
+    from scipy.signal import correlate2d
+    import oracle.conv as CV
+    from oracle.luq import luq_decode_int
+    from oracle.int4 import int4_decode_int
+    B, H, W, C, Cout = 1, 5, 6, 2, 3
+    g = synth.lognormal_grad((B * H * W, Cout), -4.0, 2.0, 0.3, [70, 1])
+    w = synth.normal((Cout, 9 * C), 1.0, [70, 2])
+    planes, alpha, _ = L.luq_quantize(g, R=4, seed=1)
+    wc, ws = int4_quantize(w, is_signed=True)
+
+    def adjoint_holds():
+        G = luq_decode_int(planes[0], B * H * W * Cout).reshape(B, H, W, Cout).astype(np.float64)
+        Wq = int4_decode_int(wc, Cout * 9 * C, True).reshape(Cout, 3, 3, C).astype(np.float64)
+        act = np.random.default_rng(3).integers(-7, 8, size=(B, H, W, C)).astype(np.float64)
+        z = np.zeros((B, H, W, Cout))
+        for o in range(Cout):
+            for c in range(C):
+                z[0, :, :, o] += correlate2d(act[0, :, :, c], Wq[o, :, :, c], mode="same")
+        dact, _ = CV.conv3x3_dgrad_ref(planes, np.float32(1), wc, np.float32(1), True, B, H, W, C, Cout)
+        return np.sum(z * G) == np.sum(act.reshape(-1, C) * dact)
+
+    assert adjoint_holds()
+    good = CV.conv3x3_dgrad_ref
+    src = open(CV.__file__).read()
+    bad_src = src.replace("ys, xs = y - kh + 1, x - kw + 1", "ys, xs = y + kh - 1, x + kw - 1")
+    assert bad_src != src
+    ns = {}
+    exec(compile(bad_src, CV.__file__, "exec"), CV.__dict__ | ns, ns)
+    monkeypatch.setattr(CV, "conv3x3_dgrad_ref", ns["conv3x3_dgrad_ref"])
+    assert not adjoint_holds()
+    monkeypatch.setattr(CV, "conv3x3_dgrad_ref", good)
