@@ -1,13 +1,17 @@
 """Benchmark of the LUQ 4-bit backward hot path on one MI355X.
 
     python bench.py [--gpus 1] [--steps K] [--warmup W]
-                    [--workload resnet|mlp|mlp_smp|mlp_fwd|small|luq_sweep]
+                    [--workload resnet|resnet_lowered|mlp|mlp_smp|mlp_fwd|small|luq_sweep]
 
 A step is one pass of the whole hot path over one batch of synthetic input,
 inputs resident in HBM:
   LUQ of the neural gradient (row-major codes for dX, transposed for dW),
   INT4 of the activations (+ 3x3 im2col on codes for the conv workload),
   INT4 of the weights (transposed codes), the dX GEMM and the dW GEMM.
+For the default conv workload (ResNet-50 3x3 conv, batch 64, 56x56, 64->64)
+the activation gradient is the implicit-GEMM convolution (dact [T, C]);
+`--workload resnet_lowered` runs the GEMM on the lowered layout instead
+(dcol [T, 9C], which a col2im would still have to fold).
 
 Prints one JSON line.  `value` is roofline-normalised throughput: the sum,
 over the step's kernels, of each kernel's roofline time (algorithmic HBM
@@ -48,7 +52,7 @@ def parse():
     p.add_argument("--gpus", type=int, default=1)
     p.add_argument("--steps", type=int, default=20)
     p.add_argument("--warmup", type=int, default=5)
-    p.add_argument("--workload", default="resnet", choices=["resnet", "mlp", "mlp_smp", "mlp_fwd", "small", "luq_sweep"])
+    p.add_argument("--workload", default="resnet", choices=["resnet", "resnet_lowered", "mlp", "mlp_smp", "mlp_fwd", "small", "luq_sweep"])
     p.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     p.add_argument("--sweep-log2", default=None,
                    help="comma-separated log2 sizes for luq_sweep (default: 20,22,24,26..30)")
@@ -68,7 +72,11 @@ class Stage:
         return "hbm" if self.bytes / HBM_PEAK >= self.ops / I8_PEAK else "mfma"
 
 
-def build_resnet(L, torch, dev):
+def build_resnet(L, torch, dev, lowered_dx=False):
+    """The 3x3 conv layer's backward.  The activation gradient comes from the
+    implicit-GEMM convolution kernel (dact [T, C], M = T, K = 9 * Cout, N = C),
+    or with lowered_dx from the GEMM on the lowered layout (dcol [T, 9 * C],
+    M = T, K = Cout, N = 9 * C; a col2im would still have to fold it)."""
     import synth
     p = synth.RESNET
     B, H, W, C, Co = p["B"], p["H"], p["W"], p["C"], p["Cout"]
@@ -83,7 +91,9 @@ def build_resnet(L, torch, dev):
     ac, sa = u8(T * C // 2), f32(1)
     colt = u8(Ki * T // 2)
     wct, sw = u8(Co * Ki // 2), f32(1)
-    dx, dw = f32(T, Ki), f32(Co, Ki)
+    dx = f32(T, Ki) if lowered_dx else None
+    dact = None if lowered_dx else f32(T, C)
+    dw = f32(Co, Ki)
     wsq = u8(L.workspace_size(L.OP_QUANTIZE_GRAD, T * Co))
     wsa = u8(L.workspace_size(L.OP_INT4_QUANTIZE, T * C))
     wsw = u8(L.workspace_size(L.OP_INT4_QUANTIZE, Co * Ki))
@@ -102,14 +112,27 @@ def build_resnet(L, torch, dev):
         # the last-level cache; the dX GEMM's 462 MB of output would evict them
         Stage("luq_gemm_wgrad", lambda: L.luq_gemm_wgrad(gct, alpha, colt, sa, False, T, Co, Ki, 1, dw, wsg),
               Co * T / 2 + Ki * T / 2 + 4 * Co * Ki, 2.0 * T * Ki * Co),
-        Stage("luq_gemm_dgrad", lambda: L.luq_gemm_dgrad(gc, alpha, wct, sw, True, T, Ki, Co, 1, dx, wsd),
-              T * Co / 2 + Ki * Co / 2 + 4 * T * Ki, 2.0 * T * Ki * Co),
     ]
+    if lowered_dx:
+        stages.append(Stage("luq_gemm_dgrad", lambda: L.luq_gemm_dgrad(gc, alpha, wct, sw, True, T, Ki, Co, 1, dx, wsd),
+                            T * Co / 2 + Ki * Co / 2 + 4 * T * Ki, 2.0 * T * Ki * Co))
+    else:
+        # g codes, W codes and dact once each
+        stages.append(Stage("luq_conv3x3_dgrad",
+                            lambda: L.luq_conv3x3_dgrad(gc, alpha, wct, sw, True, B, H, W, C, Co, 1, dact),
+                            T * Co / 2 + Ki * Co / 2 + 4 * T * C, 2.0 * T * C * Ki))
     d["dev"] = dict(g=g, act=act, w=w, gc=gc, gct=gct, alpha=alpha, gmax=gmax, ac=ac, sa=sa, colt=colt,
-                    wct=wct, sw=sw, dx=dx, dw=dw)
-    cfg = {"workload": "resnet50_conv3x3_bwd", "batch": B, "hw": [H, W], "cin": C, "cout": Co,
-           "gemm_dgrad_MNK": [T, Ki, Co], "gemm_wgrad_MNK": [Co, Ki, T], "grad": "lognormal(-12,2.5) fp32, 50% zeros",
-           "R": 4, "n_samples": 1}
+                    wct=wct, sw=sw, dw=dw)
+    if lowered_dx:
+        d["dev"]["dx"] = dx
+    else:
+        d["dev"]["dact"] = dact
+    cfg = {"workload": "resnet50_conv3x3_bwd_lowered_dx" if lowered_dx else "resnet50_conv3x3_bwd",
+           "batch": B, "hw": [H, W], "cin": C, "cout": Co,
+           "dx": ("GEMM on the lowered layout, dcol [T, 9C]" if lowered_dx else
+                  "implicit-GEMM convolution, dact [T, C]"),
+           "gemm_dgrad_MNK": [T, Ki, Co] if lowered_dx else [T, C, Ki], "gemm_wgrad_MNK": [Co, Ki, T],
+           "grad": "lognormal(-12,2.5) fp32, 50% zeros", "R": 4, "n_samples": 1}
     return stages, cfg, d
 
 
@@ -317,7 +340,7 @@ def cpu_baseline(workload, d):
     """The oracle on a bounded sample of the workload (10-30 s of CPU work)."""
     import numpy as np
     from threadpoolctl import threadpool_info
-    from oracle import luq as oluq, int4 as oint4, gemm as ogemm, im2col as oim2col
+    from oracle import luq as oluq, int4 as oint4, gemm as ogemm, im2col as oim2col, conv as oconv
     import synth
     t_roof, t_cpu, parts = 0.0, 0.0, []
 
@@ -330,7 +353,7 @@ def cpu_baseline(workload, d):
         t_roof += max(bytes_ / HBM_PEAK, ops / I8_PEAK)
         parts.append(f"{label} {dt:.2f}s")
 
-    if workload == "resnet":
+    if workload in ("resnet", "resnet_lowered"):
         # the whole step, repeated until at least 10 s of CPU work
         p = synth.RESNET
         B, H, W, C, Co = p["B"], p["H"], p["W"], p["C"], p["Cout"]
@@ -358,8 +381,13 @@ def cpu_baseline(workload, d):
             timed("im2col", col, n_a / 2 + K9 * T / 2)
             timed("int4(W)", wq, 2 * 4 * n_w + n_w / 2)
             gc, ga, _ = out["g"]
-            timed("dX", lambda: ogemm.gemm_dgrad_ref(gc, ga, out["w"][0], out["w"][1], True, T, K9, Co),
-                  T * Co / 2 + K9 * Co / 2 + 4 * T * K9, 2.0 * T * K9 * Co)
+            if workload == "resnet_lowered":
+                timed("dX", lambda: ogemm.gemm_dgrad_ref(gc, ga, out["w"][0], out["w"][1], True, T, K9, Co),
+                      T * Co / 2 + K9 * Co / 2 + 4 * T * K9, 2.0 * T * K9 * Co)
+            else:
+                timed("dact", lambda: oconv.conv3x3_dgrad_ref(gc, ga, out["w"][0], out["w"][1], True,
+                                                              B, H, W, C, Co),
+                      T * Co / 2 + K9 * Co / 2 + 4 * T * C, 2.0 * T * K9 * Co)
             timed("dW", lambda: ogemm.gemm_wgrad_ref(gc, ga, out["col"], out["a"][1], False, T, Co, K9),
                   Co * T / 2 + K9 * T / 2 + 4 * Co * K9, 2.0 * T * K9 * Co)
             reps += 1
@@ -414,6 +442,7 @@ def cpu_baseline(workload, d):
 
 PROFILES = os.path.join(ROOT, "profiles")
 KERNEL_SOURCES = {"luq_gemm_dgrad": "gemm_kernel.hpp", "luq_gemm_wgrad": "gemm_kernel.hpp",
+                  "luq_conv3x3_dgrad": "conv.hip",
                   "int4_gemm_fwd": "gemm_kernel.hpp",
                   "luq_quantize_grad": "quant.hip", "int4_im2col3x3_t": "im2col.hip"}
 
@@ -469,8 +498,8 @@ def main():
             out["cpu_baseline"] = cpu_sweep_baseline()
         print(json.dumps(out), flush=True)
         return
-    if args.workload == "resnet":
-        stages, cfg, d = build_resnet(L, torch, dev)
+    if args.workload in ("resnet", "resnet_lowered"):
+        stages, cfg, d = build_resnet(L, torch, dev, lowered_dx=args.workload == "resnet_lowered")
     elif args.workload == "mlp_fwd":
         stages, cfg, d = build_mlp_fwd(L, torch, dev)
     elif args.workload == "small":
@@ -506,7 +535,8 @@ def main():
         "roofline_step_us": round(roof_total * 1e6, 2),
     }
     if not args.no_cpu:
-        out["cpu_baseline"] = cpu_baseline(args.workload if args.workload in ("resnet", "mlp_fwd") else "mlp", d)
+        out["cpu_baseline"] = cpu_baseline(args.workload if args.workload in ("resnet", "resnet_lowered", "mlp_fwd")
+                                           else "mlp", d)
     print(json.dumps(out), flush=True)
 
 

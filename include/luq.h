@@ -47,7 +47,7 @@
 extern "C" {
 #endif
 
-#define LUQ_ABI_VERSION 4
+#define LUQ_ABI_VERSION 5
 
 typedef int luq_status;
 enum {
@@ -271,6 +271,37 @@ luq_status int4_gemm_fwd(const uint8_t* x_codes, const float* x_scale, int x_sig
  */
 luq_status int4_im2col3x3_t(const uint8_t* act_codes, int64_t B, int64_t H, int64_t W, int64_t C,
                             uint8_t* col_t, void* stream);
+
+/*
+ * luq_conv3x3_dgrad -- activation gradient of a 3x3 / stride 1 / zero-pad 1
+ * convolution on codes: Eq. backward applied to the lowered convolution and
+ * folded back onto the input pixels (the adjoint of the lowering), without
+ * forming the lowered [T][9*C] gradient:
+ *   dact[t][c] = (alpha / n_samples) * w_scale *
+ *                sum_{kh,kw} sum_o (sum_s cg_s[t'][o]) * cw[(kh*3 + kw)*C + c][o]
+ * for t = (b*H + y)*W + x and t' = (b*H + y + 1 - kh)*W + x + 1 - kw, terms
+ * whose t' lies off the image left out.  Every MAC is on codes and
+ * accumulates exactly in int32; the scales are applied once in fp32
+ * (Appendix A.1), as in luq_gemm_dgrad.
+ *
+ *  g_codes    n_samples planes of [T][Cout] LUQ codes of the output gradient
+ *             (NHWC pixels t, T = B*H*W; plane stride luq_plane_bytes(T*Cout)).
+ *  alpha      1 float (device), the LUQ alpha of g.
+ *  w_codes_t  [9*C][Cout] INT4 codes: the weight [Cout][3][3][C] (columns in
+ *             (kh, kw, c) order) in the transposed layout, i.e. the codes_t
+ *             output of int4_quantize on W [Cout][9*C]; w_scale 1 float
+ *             (device); w_signed 0/1.
+ *  B, H, W, C >= 0 (nothing is done when B*H*W or C is 0); W <= 256;
+ *             Cout a multiple of 32 in [32, 16384]; each code operand below
+ *             1 GiB.  n_samples 1 or 2 (codes from this library, R <= 5 for 2).
+ *  dact       out: [T][C] fp32, row-major (NHWC).
+ *  No workspace.  Errors: LUQ_ERR_SHAPE, LUQ_ERR_PARAM, LUQ_ERR_NULL,
+ *  LUQ_ERR_ALIGN (code operands 16-byte aligned, dact and scales 4-byte),
+ *  LUQ_ERR_HIP; nothing is enqueued on error.
+ */
+luq_status luq_conv3x3_dgrad(const uint8_t* g_codes, const float* alpha, int n_samples,
+                             const uint8_t* w_codes_t, const float* w_scale, int w_signed, int64_t B,
+                             int64_t H, int64_t W, int64_t C, int64_t Cout, float* dact, void* stream);
 
 #ifdef __cplusplus
 }

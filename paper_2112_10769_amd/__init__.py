@@ -24,7 +24,7 @@ OP_QUANTIZE_GRAD, OP_INT4_QUANTIZE, OP_GEMM_DGRAD, OP_GEMM_WGRAD, OP_GEMM_FWD = 
 EXPORTS = (
     "luq_abi_version", "luq_status_string", "luq_last_error", "luq_plane_bytes",
     "luq_workspace_size", "luq_quantize_grad", "luq_quantize_grad_hindsight", "int4_quantize",
-    "luq_gemm_dgrad", "luq_gemm_wgrad", "int4_gemm_fwd", "int4_im2col3x3_t",
+    "luq_gemm_dgrad", "luq_gemm_wgrad", "int4_gemm_fwd", "int4_im2col3x3_t", "luq_conv3x3_dgrad",
 )
 
 
@@ -63,6 +63,8 @@ def _load():
     lib.int4_gemm_fwd.argtypes = [vp, vp, i32, vp, vp, i32, i64, i64, i64, vp, vp, sz, vp]
     lib.int4_im2col3x3_t.restype = i32
     lib.int4_im2col3x3_t.argtypes = [vp, i64, i64, i64, i64, vp, vp]
+    lib.luq_conv3x3_dgrad.restype = i32
+    lib.luq_conv3x3_dgrad.argtypes = [vp, vp, i32, vp, vp, i32, i64, i64, i64, i64, i64, vp, vp]
     return lib
 
 
@@ -239,3 +241,14 @@ def int4_im2col3x3_t(act_codes, B, H, W, C, col_t=None):
     st = LIB.int4_im2col3x3_t(_ptr(act_codes), B, H, W, C, _ptr(col_t), _stream(dev))
     _check(st, "int4_im2col3x3_t")
     return col_t
+
+
+def luq_conv3x3_dgrad(g_codes, alpha, w_codes_t, w_scale, w_signed, B, H, W, C, Cout, n_samples=1, dact=None):
+    """Activation gradient [B*H*W, C] of a 3x3 / stride 1 / pad 1 convolution
+    from LUQ codes of g [B*H*W, Cout] and transposed weight codes [9*C, Cout]."""
+    dev = g_codes.device
+    dact = torch.empty(B * H * W, C, dtype=torch.float32, device=dev) if dact is None else dact
+    st = LIB.luq_conv3x3_dgrad(_ptr(g_codes), _ptr(alpha), n_samples, _ptr(w_codes_t), _ptr(w_scale),
+                               1 if w_signed else 0, B, H, W, C, Cout, _ptr(dact), _stream(dev))
+    _check(st, "luq_conv3x3_dgrad")
+    return dact

@@ -256,4 +256,30 @@ luq_status int4_im2col3x3_t(const uint8_t* act_codes, int64_t B, int64_t H, int6
                                             static_cast<hipStream_t>(stream)));
 }
 
+luq_status luq_conv3x3_dgrad(const uint8_t* g_codes, const float* alpha, int n_samples,
+                             const uint8_t* w_codes_t, const float* w_scale, int w_signed, int64_t B,
+                             int64_t H, int64_t W, int64_t C, int64_t Cout, float* dact, void* stream) {
+  const char* fn = "luq_conv3x3_dgrad";
+  g_last_error[0] = 0;
+  if (B < 0 || H < 0 || W < 0 || C < 0 || Cout < 0) return fail(LUQ_ERR_SHAPE, "%s: negative size", fn);
+  if (n_samples != 1 && n_samples != 2) return fail(LUQ_ERR_PARAM, "%s: n_samples must be 1 or 2", fn);
+  if (B > INT32_MAX || H > INT32_MAX || W > INT32_MAX || C > INT32_MAX || Cout > INT32_MAX ||
+      mul_overflows(B, H) || mul_overflows(B * H, W) || mul_overflows(B * H * W, Cout) ||
+      mul_overflows(9 * C, Cout))
+    return fail(LUQ_ERR_SHAPE, "%s: size overflows", fn);
+  const int64_t T = B * H * W;
+  if (T == 0 || C == 0) return LUQ_OK;
+  if (Cout < 32 || (Cout & 31) || Cout > 16384)
+    return fail(LUQ_ERR_SHAPE, "%s: Cout must be a multiple of 32 in [32, 16384]", fn);
+  if (W > luq::conv3x3_max_width()) return fail(LUQ_ERR_SHAPE, "%s: image width above 256", fn);
+  if (T * (Cout / 2) >= ((int64_t)1 << 30) || 9 * C * (Cout / 2) >= ((int64_t)1 << 30))
+    return fail(LUQ_ERR_SHAPE, "%s: operand above 1 GiB of codes", fn);
+  if (!g_codes || !alpha || !w_codes_t || !w_scale || !dact) return fail(LUQ_ERR_NULL, "%s: NULL operand", fn);
+  if (!aligned16(g_codes) || !aligned16(w_codes_t) || !aligned4(dact) || !aligned4(alpha) || !aligned4(w_scale))
+    return fail(LUQ_ERR_ALIGN, "%s: code operands must be 16-byte aligned, dact and scales 4-byte", fn);
+  return hip_status(luq::launch_conv3x3_dgrad(g_codes, (int64_t)luq::plane_bytes(T * Cout), n_samples, alpha,
+                                              w_codes_t, w_scale, w_signed ? 1 : 0, B, H, W, C, Cout, dact,
+                                              static_cast<hipStream_t>(stream)));
+}
+
 }  // extern "C"

@@ -44,6 +44,13 @@ hipError_t launch_gemm_int4_fwd(const uint8_t* X, const float* x_scale, int x_si
                                 const float* w_scale, int w_signed, int64_t M, int64_t N, int64_t K, float* Y,
                                 void* ws, hipStream_t st);
 
+// dact[t][c] of a 3x3 / stride 1 / pad 1 convolution from LUQ codes of g
+// [T][Cout] (ns planes) and INT4 codes of W transposed [9*C][Cout].
+int conv3x3_max_width();
+hipError_t launch_conv3x3_dgrad(const uint8_t* g, int64_t g_plane, int ns, const float* alpha, const uint8_t* w,
+                                const float* wscale, int w_signed, int64_t B, int64_t H, int64_t W, int64_t C,
+                                int64_t Cout, float* dact, hipStream_t st);
+
 hipError_t launch_im2col3x3_t(const uint8_t* act, int64_t B, int64_t H, int64_t W, int64_t C,
                               uint8_t* col_t, hipStream_t st);
 

@@ -32,7 +32,7 @@ def _declared():
 
 def test_every_declared_function_is_exported():
     names = _declared()
-    assert len(names) == 12, names
+    assert len(names) == 13, names
     for n in names:
         assert hasattr(LIB, n), n
     assert set(names) == set(luq.EXPORTS)
@@ -189,3 +189,22 @@ def test_im2col_validation():
     assert LIB.int4_im2col3x3_t(PMIS, 1, 2, 4, 2, P2, None) == 6
     assert LIB.int4_im2col3x3_t(P, -1, 2, 4, 2, P2, None) == 2
     assert LIB.int4_im2col3x3_t(P, 0, 2, 4, 2, P2, None) == 0       # empty: nothing to do
+
+
+def _cv(**kw):
+    a = dict(g=P, alpha=P3, ns=1, w=P2, ws_=P3, wsig=1, B=2, H=8, W=8, C=64, Co=64, out=P)
+    a.update(kw)
+    return LIB.luq_conv3x3_dgrad(a["g"], a["alpha"], a["ns"], a["w"], a["ws_"], a["wsig"], a["B"], a["H"],
+                                 a["W"], a["C"], a["Co"], a["out"], None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(g=NUL), 1), (dict(alpha=NUL), 1), (dict(w=NUL), 1), (dict(ws_=NUL), 1), (dict(out=NUL), 1),
+    (dict(ns=0), 4), (dict(ns=3), 4),
+    (dict(B=-1), 2), (dict(Co=48), 2), (dict(Co=0), 2), (dict(Co=16), 2), (dict(Co=32768), 2),
+    (dict(W=257), 2), (dict(B=4096, H=256, W=256, Co=64), 2),
+    (dict(g=PMIS), 6), (dict(w=PMIS), 6), (dict(out=ctypes.c_void_p(0x10002)), 6),
+    (dict(B=0), 0), (dict(C=0), 0), (dict(B=0, g=NUL, out=NUL), 0),
+])
+def test_conv_dgrad_validation(kw, status):
+    assert _cv(**kw) == status

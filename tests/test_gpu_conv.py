@@ -1,0 +1,142 @@
+"""GPU parity of the 3x3 convolution activation gradient (luq_conv3x3_dgrad)
+against the oracle (oracle/conv.py), through the C ABI.
+
+Inputs: seeded synthetic gradients, activations' weights and codes from the
+library's own quantizers (checked bit-exact against the oracle's on the way).
+Every output is compared within 1e-5 of sum_k |a_k b_k| of the float64
+result, and bit-for-bit with the fp32 epilogue fl32(fl32(acc) *
+fl32(fl32(alpha / n) * s_W)) applied to the exact integer sums.
+
+Shapes span: one and several 256-pixel tiles with a ragged tail, channel
+counts that are not multiples of 64 (or of 4: scalar stores), Cout with a
+half-filled 64-deep chunk and several chunks, images narrower than a tile
+row and wider than 64 pixels (the wide-halo kernel), width and height 1, SMP
+planes, unsigned weights, and the full ResNet-50 layer (batch 64, 56 x 56,
+64 -> 64) on every pixel.
+"""
+import numpy as np
+import pytest
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+import synth  # noqa: E402
+from oracle import luq as oluq, int4 as oint4  # noqa: E402
+from oracle.conv import conv3x3_dgrad_ref  # noqa: E402
+from gpu_util import (announce, to_dev, host, transpose_codes, assert_codes_equal,  # noqa: E402
+                      assert_gemm_close, epilogue_replica)
+
+
+@pytest.fixture(scope="module")
+def L():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_2112_10769_amd as lib
+    return lib
+
+
+def _int_sums(planes, wc, wsig, B, H, W, C, Cout, pixels=None):
+    """Exact integer sums: the oracle with unit scales, times the plane count."""
+    ns = 1 if np.asarray(planes).ndim == 1 else np.asarray(planes).shape[0]
+    s, _ = conv3x3_dgrad_ref(planes, np.float32(1), wc, np.float32(1), wsig, B, H, W, C, Cout, pixels=pixels)
+    return np.rint(s * ns).astype(np.int64)
+
+
+def _conv_case(L, B, H, W, C, Cout, ns=1, wsig=True, seed=0, zero_grad=False, use_codes_t=False):
+    T = B * H * W
+    g = synth.lognormal_grad((T, Cout), -12.0, 2.5, 0.5, [seed, 1])
+    if zero_grad:
+        g[:] = 0
+    w = synth.normal((Cout, 9 * C), float(np.sqrt(2.0 / (9 * C))), [seed, 2])
+    if not wsig:
+        w = np.abs(w)
+    announce("conv3x3_dgrad", dict(B=B, H=H, W=W, C=C, Cout=Cout, ns=ns, wsig=wsig, seed=seed))
+    gc, _, alpha, _ = L.luq_quantize_grad(to_dev(g), R=4, seed=seed, counter=5, n_samples=ns)
+    if use_codes_t:
+        _, wct, sw = L.int4_quantize(to_dev(w), is_signed=wsig, codes=False, codes_t=True)
+    else:
+        wcg, _, sw = L.int4_quantize(to_dev(w), is_signed=wsig)
+        wct = to_dev(transpose_codes(host(wcg), Cout, 9 * C))
+    dact = host(L.luq_conv3x3_dgrad(gc, alpha, wct, sw, wsig, B, H, W, C, Cout, n_samples=ns))
+    assert dact.shape == (T, C)
+
+    rc, ra, _ = oluq.luq_quantize(g, R=4, seed=seed, counter=5, n_samples=ns)
+    wc, wsr = oint4.int4_quantize(w, is_signed=wsig)
+    assert host(alpha)[0].tobytes() == np.float32(ra).tobytes()
+    assert host(sw)[0].tobytes() == np.float32(wsr).tobytes()
+    gch = host(gc)
+    for s in range(ns):
+        assert_codes_equal(gch[s], rc[s], f"g codes plane {s}")
+    assert_codes_equal(host(wct), transpose_codes(wc, Cout, 9 * C), "W codes_t")
+    planes = rc if ns > 1 else rc[0]
+    ref, absref = conv3x3_dgrad_ref(planes, ra, wc, wsr, wsig, B, H, W, C, Cout)
+    assert_gemm_close(dact, ref, absref, f"conv dact {B}x{H}x{W}x{C}<-{Cout}")
+    acc = _int_sums(planes, wc, wsig, B, H, W, C, Cout)
+    assert np.array_equal(dact, epilogue_replica(acc, ra, ns, wsr)), "conv dact epilogue not bit-exact"
+    return dact
+
+
+@pytest.mark.parametrize("B,H,W,C,Cout", [
+    (1, 4, 4, 64, 64),        # a single partial tile
+    (4, 14, 14, 64, 64),      # 784 pixels: three tiles and a 16-pixel tail
+    (2, 5, 7, 6, 32),         # C not a multiple of 4 (scalar stores), half chunk
+    (3, 9, 11, 96, 96),       # two channel tiles (second partial), 1.5 chunks
+    (2, 8, 8, 128, 256),      # four chunks, two full channel tiles
+    (1, 3, 100, 8, 64),       # wider than 64: the wide-halo kernel
+    (1, 2, 256, 4, 32),       # the widest image accepted
+    (3, 1, 37, 16, 64),       # height 1
+    (2, 45, 1, 16, 64),       # width 1
+])
+@pytest.mark.parametrize("ns", [1, 2])
+def test_conv_dgrad_parity(L, B, H, W, C, Cout, ns):
+    _conv_case(L, B, H, W, C, Cout, ns=ns, seed=B * 1000 + H * 100 + W + C + Cout)
+
+
+@pytest.mark.parametrize("B,H,W,C,Cout", [(2, 7, 9, 24, 64), (1, 6, 70, 8, 96)])
+def test_conv_dgrad_unsigned_weights(L, B, H, W, C, Cout):
+    _conv_case(L, B, H, W, C, Cout, wsig=False, seed=17)
+
+
+def test_conv_dgrad_weight_codes_from_transposed_quantizer(L):
+    """The weight's codes_t output of int4_quantize is the operand layout."""
+    _conv_case(L, 2, 12, 12, 64, 64, use_codes_t=True, seed=23)
+
+
+def test_conv_dgrad_all_zero_gradient(L):
+    dact = _conv_case(L, 1, 6, 6, 8, 32, zero_grad=True, seed=29)
+    assert not np.any(dact)
+
+
+def test_conv_dgrad_empty(L):
+    announce("conv3x3_dgrad empty")
+    gc = torch.zeros(256, dtype=torch.uint8, device="cuda")
+    a = torch.ones(1, dtype=torch.float32, device="cuda")
+    out = torch.full((1,), 7.0, device="cuda")
+    L.luq_conv3x3_dgrad(gc, a, gc, a, True, 0, 5, 5, 8, 32, dact=out)
+    L.luq_conv3x3_dgrad(gc, a, gc, a, True, 1, 5, 5, 0, 32, dact=out)
+    assert host(out)[0] == 7.0
+
+
+def test_conv_dgrad_resnet_layer_whole_output(L):
+    """The ResNet-50 layer (batch 64, 56 x 56, 64 -> 64) in the benchmark's
+    launch, every pixel against the oracle."""
+    import bench
+    announce("conv3x3_dgrad full ResNet layer")
+    stages, _, d = bench.build_resnet(L, torch, torch.device("cuda:0"))
+    for s in stages:
+        if s.name in ("luq_quantize_grad", "int4_quantize(W)", "luq_conv3x3_dgrad"):
+            announce("stage", s.name)
+            s.fn()
+    torch.cuda.synchronize()
+    p = synth.RESNET
+    B, H, W, C, Co = p["B"], p["H"], p["W"], p["C"], p["Cout"]
+    dv = d["dev"]
+    assert "dact" in dv, "the benchmark's conv workload computes the activation gradient"
+    dact = host(dv["dact"])
+    rc, ra, _ = oluq.luq_quantize(d["g"], R=4)
+    wc, wsr = oint4.int4_quantize(d["W"], is_signed=True)
+    assert_codes_equal(host(dv["gc"])[: rc[0].size], rc[0], "g codes")
+    ref, absref = conv3x3_dgrad_ref(rc[0], ra, wc, wsr, True, B, H, W, C, Co)
+    assert_gemm_close(dact, ref, absref, "resnet dact")
+    acc = _int_sums(rc[0], wc, True, B, H, W, C, Co)
+    assert np.array_equal(dact, epilogue_replica(acc, ra, 1, wsr)), "resnet dact epilogue not bit-exact"
