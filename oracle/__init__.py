@@ -12,7 +12,8 @@ Matrix Multiplications at Standard Formats" (Chmiel et al., arXiv 2112.10769):
                  (Section 4: stochastic underflow, Eq. StochasticPruning;
                  underflow threshold, Eq. alpha; logarithmic SR,
                  Eq. unbiasedFpQ; their composition X_q = Q_alpha(T_alpha(x)))
-                 and the multi-sample average of Section 5.1 (SMP).
+                 and the multi-sample average of Section 5.1 (SMP), as planes
+                 or as the per-element sum of the decoded samples.
 * ``int4``    -- uniform INT4 round-to-nearest quantizer for weights and
                  activations (Section 3.3 rounding rule; Appendix A.1 scale
                  alpha = Delta / (2^b - 1)).

@@ -247,6 +247,21 @@ def luq_decode_int(codes, n):
     return np.where(nib & 8, -mag, mag)
 
 
+def luq_smp_sum(planes, n):
+    """SMP operand (Section 5.1) as one integer per element: the sum over the
+    n_s sample planes of the signed multiples of alpha, so that the averaged
+    gradient is (alpha / n_s) * sum.  int8 array of length n; |sum| <= n_s *
+    2^R, which fits int8 for two samples with R <= 5."""
+    planes = np.asarray(planes, dtype=np.uint8)
+    if planes.ndim == 1:
+        planes = planes[None]
+    tot = np.zeros(n, dtype=np.int64)
+    for p in planes:
+        tot += luq_decode_int(p, n)
+    assert np.all(np.abs(tot) <= 127), "sum does not fit int8"
+    return tot.astype(np.int8)
+
+
 def luq_decode(codes, n, alpha):
     """Dequantized values (float64)."""
     return luq_decode_int(codes, n).astype(np.float64) * float(alpha)
