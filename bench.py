@@ -1,7 +1,7 @@
 """Benchmark of the LUQ 4-bit backward hot path on one MI355X.
 
     python bench.py [--gpus 1] [--steps K] [--warmup W]
-                    [--workload resnet|resnet_lowered|mlp|mlp_smp|mlp_fwd|small|luq_sweep]
+                    [--workload resnet|resnet_lowered|mlp|mlp_smp|mlp_smp_planes|mlp_fwd|small|luq_sweep]
 
 A step is one pass of the whole hot path over one batch of synthetic input,
 inputs resident in HBM:
@@ -12,6 +12,8 @@ For the default conv workload (ResNet-50 3x3 conv, batch 64, 56x56, 64->64)
 the activation gradient is the implicit-GEMM convolution (dact [T, C]);
 `--workload resnet_lowered` runs the GEMM on the lowered layout instead
 (dcol [T, 9C], which a col2im would still have to fold).
+`--workload mlp_smp` is the MLP layer with two SMP samples stored as int8
+sums (the bytes of two 4-bit planes); `mlp_smp_planes` keeps two planes.
 
 Prints one JSON line.  `value` is roofline-normalised throughput: the sum,
 over the step's kernels, of each kernel's roofline time (algorithmic HBM
@@ -52,7 +54,8 @@ def parse():
     p.add_argument("--gpus", type=int, default=1)
     p.add_argument("--steps", type=int, default=20)
     p.add_argument("--warmup", type=int, default=5)
-    p.add_argument("--workload", default="resnet", choices=["resnet", "resnet_lowered", "mlp", "mlp_smp", "mlp_fwd", "small", "luq_sweep"])
+    p.add_argument("--workload", default="resnet", choices=["resnet", "resnet_lowered", "mlp", "mlp_smp", "mlp_smp_planes", "mlp_fwd", "small",
+                            "luq_sweep"])
     p.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     p.add_argument("--sweep-log2", default=None,
                    help="comma-separated log2 sizes for luq_sweep (default: 20,22,24,26..30)")
@@ -137,6 +140,8 @@ def build_resnet(L, torch, dev, lowered_dx=False):
 
 
 def build_mlp(L, torch, dev, ns=1, T=None, D=None, F=None, d=None):
+    """Backward of the MLP up-projection.  ns: 1, 2 (two SMP sample planes) or
+    L.SMP_SUM | 2 (the two samples as int8 sums, same bytes as two planes)."""
     import synth
     T = T or synth.MLP["T"]
     D = D or synth.MLP["D"]
@@ -147,8 +152,10 @@ def build_mlp(L, torch, dev, ns=1, T=None, D=None, F=None, d=None):
     w = torch.from_numpy(d["W"]).to(dev)                              # [F, D]
     u8 = lambda n: torch.empty(int(n), dtype=torch.uint8, device=dev)
     f32 = lambda *s: torch.empty(*s, dtype=torch.float32, device=dev)
-    pb = L.plane_bytes(T * F)
-    gc, gct, alpha, gmax = u8(ns * pb), u8(ns * pb), f32(1), f32(1)
+    summed = bool(ns & L.SMP_SUM)
+    nsamp = ns & 0xF
+    gbytes = T * F if summed else nsamp * L.plane_bytes(T * F)
+    gc, gct, alpha, gmax = u8(gbytes), u8(gbytes), f32(1), f32(1)
     xct, sx = u8(T * D // 2), f32(1)
     wct, sw = u8(F * D // 2), f32(1)
     dx, dw = f32(T, D), f32(F, D)
@@ -160,18 +167,20 @@ def build_mlp(L, torch, dev, ns=1, T=None, D=None, F=None, d=None):
     n_g, n_x, n_w = T * F, T * D, F * D
     stages = [
         Stage("luq_quantize_grad", lambda: L.luq_quantize_grad(g, 4, 0, 0, ns, gc, gct, alpha, gmax, wsq),
-              2 * 2 * n_g + 2 * ns * n_g / 2),
+              2 * 2 * n_g + 2 * nsamp * n_g / 2),
         Stage("int4_quantize(x)", lambda: L.int4_quantize(x, True, 0.0, False, xct, sx, wsx), 2 * 2 * n_x + n_x / 2),
         Stage("int4_quantize(W)", lambda: L.int4_quantize(w, True, 0.0, False, wct, sw, wsw), 2 * 4 * n_w + n_w / 2),
         Stage("luq_gemm_dgrad", lambda: L.luq_gemm_dgrad(gc, alpha, wct, sw, True, T, D, F, ns, dx, wsd),
-              ns * T * F / 2 + D * F / 2 + 4 * T * D, 2.0 * T * D * F),
+              nsamp * T * F / 2 + D * F / 2 + 4 * T * D, 2.0 * T * D * F),
         Stage("luq_gemm_wgrad", lambda: L.luq_gemm_wgrad(gct, alpha, xct, sx, True, T, F, D, ns, dw, wsg),
-              ns * F * T / 2 + D * T / 2 + 4 * F * D, 2.0 * T * D * F),
+              nsamp * F * T / 2 + D * T / 2 + 4 * F * D, 2.0 * T * D * F),
     ]
     d["dev"] = dict(g=g, x=x, w=w, gc=gc, gct=gct, alpha=alpha, gmax=gmax, xct=xct, sx=sx, wct=wct, sw=sw,
                     dx=dx, dw=dw)
-    cfg = {"workload": "transformer_mlp_bwd" + ("_smp2" if ns == 2 else ""), "tokens": T, "d_model": D,
-           "hidden": F, "grad": "lognormal(-14,3) bf16", "R": 4, "n_samples": ns}
+    cfg = {"workload": "transformer_mlp_bwd" + ("_smp2" if nsamp == 2 else "") + ("_planes" if ns == 2 else ""),
+           "tokens": T, "d_model": D, "hidden": F, "grad": "lognormal(-14,3) bf16", "R": 4, "n_samples": nsamp}
+    if nsamp == 2:
+        cfg["smp_operand"] = "int8 sums of the two samples" if summed else "two 4-bit planes"
     return stages, cfg, d
 
 
@@ -506,7 +515,8 @@ def main():
         stages, cfg, d = build_mlp(L, torch, dev, 1, T=256, D=512, F=512)
         cfg["workload"] = "linear_256x512x512_bwd"
     else:
-        stages, cfg, d = build_mlp(L, torch, dev, 2 if args.workload == "mlp_smp" else 1)
+        ns = {"mlp_smp": L.SMP_SUM | 2, "mlp_smp_planes": 2}.get(args.workload, 1)
+        stages, cfg, d = build_mlp(L, torch, dev, ns)
     step_s, per = time_stages(torch, stages, args.steps, args.warmup)
     roof_total = sum(s.roofline_s() for s in stages)
     kernels = {}

@@ -69,6 +69,14 @@ typedef enum { LUQ_F32 = 0, LUQ_BF16 = 1 } luq_dtype;
  * least power of two at or above m, so the maximum is not clipped. */
 #define LUQ_ALPHA_PW2 0x100
 
+/* Or-ed into n_samples = 2 of the LUQ quantizers and the backward GEMMs
+ * (Section 5.1, SMP): the two samples are stored as one signed byte per
+ * element, the sum of their decoded values in units of alpha (the averaged
+ * gradient is alpha/2 times it), instead of two planes of codes.  It takes
+ * the bytes of the two planes and spares the GEMM the decoding; |sum| <= 64
+ * for R <= 5. */
+#define LUQ_SMP_SUM 0x10
+
 /* Operation ids for luq_workspace_size. */
 enum {
   LUQ_OP_QUANTIZE_GRAD = 0, /* d0 = number of elements                     */
@@ -118,12 +126,17 @@ size_t luq_workspace_size(int op, int64_t d0, int64_t d1, int64_t d2);
  *           exact power of two, or 0 below the float32 subnormal range).
  *  seed, counter  Philox key and step counter; the codes are a pure
  *           function of (g, R, seed, counter, sample).
- *  n_samples  1 or 2 (SMP planes, Section 5.1).  2 requires R <= 5 so that
- *           the sum of two decoded planes fits an int8 (|sum| <= 2^(R+1)).
+ *  n_samples  1 or 2 (SMP planes, Section 5.1), or LUQ_SMP_SUM | 2 (two
+ *           samples as int8 sums).  Two samples require R <= 5 so that the
+ *           sum of two decoded planes fits an int8 (|sum| <= 2^(R+1)).
  *  codes    out: n_samples planes of [rows][cols] codes (row stride
- *           ceil(cols/2) bytes), or NULL.
+ *           ceil(cols/2) bytes), or NULL.  With LUQ_SMP_SUM: one [rows][cols]
+ *           int8 matrix (row stride cols bytes), byte i the sum over the two
+ *           samples of the decoded code (0 or +-2^(e-1)).
  *  codes_t  out: n_samples planes of the transposed [cols][rows] codes (row
- *           stride rows/2 bytes), or NULL.  At least one of codes, codes_t.
+ *           stride rows/2 bytes), or NULL; with LUQ_SMP_SUM the transposed
+ *           [cols][rows] int8 sums (row stride rows bytes).  At least one of
+ *           codes, codes_t.
  *  alpha    out: 1 float.  0 when max|g| = 0 (all codes 0); NaN when g has
  *           a non-finite element (all codes 0).
  *  maxabs   out: 1 float, max|g| (non-finite when g is), or NULL.
@@ -203,14 +216,17 @@ luq_status int4_quantize(const void* x, luq_dtype dt, int64_t rows, int64_t cols
  * scales are applied once in fp32 (Appendix A.1).
  *
  *  g_codes    n_samples planes of [M][K] LUQ codes (plane stride
- *             luq_plane_bytes(M*K)).
+ *             luq_plane_bytes(M*K)); with n_samples = LUQ_SMP_SUM | 2 the
+ *             [M][K] int8 sums of two samples (luq_quantize_grad's output in
+ *             that format), scale alpha / 2.
  *  alpha      1 float (device), the LUQ alpha of g.
  *  w_codes_t  [N][K] INT4 codes; w_scale 1 float (device); w_signed 0/1.
- *  M, N >= 1; K >= 32 and a multiple of 32.  Reductions longer than the
- *             int32-exact length are split internally and the partial sums
- *             combined exactly, so any K is exact.  The codes must come from
- *             this library: with n_samples = 2 every field must be <= 6
- *             (R <= 5), which luq_quantize_grad enforces.
+ *  M, N >= 1; K >= 32 and a multiple of 32; each code operand below 2 GiB.
+ *             Reductions longer than the int32-exact length are split
+ *             internally and the partial sums combined exactly, so any K is
+ *             exact.  The codes must come from this library: with two samples
+ *             every field must be <= 6 (R <= 5), which luq_quantize_grad
+ *             enforces.
  *  dx         out: [M][N] fp32, row-major.
  *  ws         workspace of luq_workspace_size(LUQ_OP_GEMM_DGRAD, M, N, K).
  */
@@ -228,7 +244,10 @@ luq_status luq_gemm_dgrad(const uint8_t* g_codes, const float* alpha, int n_samp
  * Long reductions are split over T with exact int32 partial sums combined
  * in a fixed order, so the result does not depend on the split.
  *
- *  T >= 32 and a multiple of 32; Nout, Kin >= 1.
+ *  g_codes_t is n_samples planes of codes, or with n_samples =
+ *  LUQ_SMP_SUM | 2 the [Nout][T] int8 sums of two samples.
+ *  T >= 32 and a multiple of 32; Nout, Kin >= 1; each code operand below
+ *  2 GiB.
  *  ws  workspace of luq_workspace_size(LUQ_OP_GEMM_WGRAD, T, Nout, Kin).
  */
 luq_status luq_gemm_wgrad(const uint8_t* g_codes_t, const float* alpha, int n_samples,

@@ -19,6 +19,7 @@ LIB_PATH = os.path.join(_HERE, "libluq.so")
 LUQ_OK = 0
 LUQ_F32, LUQ_BF16 = 0, 1
 ALPHA_PW2 = 0x100  # or-ed into R: power-of-two alpha
+SMP_SUM = 0x10     # or-ed into n_samples = 2: the two samples as int8 sums
 OP_QUANTIZE_GRAD, OP_INT4_QUANTIZE, OP_GEMM_DGRAD, OP_GEMM_WGRAD, OP_GEMM_FWD = 0, 1, 2, 3, 4
 
 EXPORTS = (
@@ -115,20 +116,29 @@ def _shape2d(x):
     return x.shape[0], x.numel() // max(x.shape[0], 1)
 
 
+def _code_buffer(n, n_samples, dev):
+    """n_samples planes of codes, or with SMP_SUM one int8 byte per element."""
+    if not n:
+        return _bytes(1, dev)
+    if n_samples & SMP_SUM:
+        return torch.empty(n, dtype=torch.int8, device=dev)
+    return _bytes(n_samples * plane_bytes(n), dev).view(n_samples, -1)
+
+
 def luq_quantize_grad(g, R=4, seed=0, counter=0, n_samples=1, codes=True, codes_t=False,
                       alpha=None, maxabs=None, ws=None, pw2=False):
     """LUQ codes of g (2-D [rows, cols] or 1-D).  codes / codes_t: True to
     allocate, a uint8 tensor to write into, or False; pw2 for the
-    power-of-two alpha.  Returns (codes, codes_t, alpha, maxabs) with codes of
-    shape [n_samples, plane]."""
+    power-of-two alpha; n_samples = 2 | SMP_SUM for the summed samples.
+    Returns (codes, codes_t, alpha, maxabs) with codes of shape
+    [n_samples, plane] (an int8 vector of the sums with SMP_SUM)."""
     rows, cols = _shape2d(g)
     n = rows * cols
     dev = g.device
-    pb = plane_bytes(n)
     if codes is True:
-        codes = _bytes(n_samples * pb, dev).view(n_samples, -1) if n else _bytes(1, dev)
+        codes = _code_buffer(n, n_samples, dev)
     if codes_t is True:
-        codes_t = _bytes(n_samples * pb, dev).view(n_samples, -1) if n else _bytes(1, dev)
+        codes_t = _code_buffer(n, n_samples, dev)
     codes = codes if codes is not False else None
     codes_t = codes_t if codes_t is not False else None
     alpha = torch.empty(1, dtype=torch.float32, device=dev) if alpha is None else alpha
@@ -153,11 +163,10 @@ def luq_quantize_grad_hindsight(g, state, R=4, seed=0, counter=0, n_samples=1, e
     rows, cols = _shape2d(g)
     n = rows * cols
     dev = g.device
-    pb = plane_bytes(n)
     if codes is True:
-        codes = _bytes(n_samples * pb, dev).view(n_samples, -1) if n else _bytes(1, dev)
+        codes = _code_buffer(n, n_samples, dev)
     if codes_t is True:
-        codes_t = _bytes(n_samples * pb, dev).view(n_samples, -1) if n else _bytes(1, dev)
+        codes_t = _code_buffer(n, n_samples, dev)
     codes = codes if codes is not False else None
     codes_t = codes_t if codes_t is not False else None
     alpha = torch.empty(1, dtype=torch.float32, device=dev) if alpha is None else alpha

@@ -36,6 +36,15 @@ luq_status check_matrix(int64_t rows, int64_t cols, bool transposed, const char*
   return LUQ_OK;
 }
 
+// n_samples of the LUQ entry points: 1, 2, or LUQ_SMP_SUM | 2 (the two
+// samples stored as int8 sums); two samples need R <= 5.
+luq_status check_samples(int n_samples, int R, const char* name) {
+  if (n_samples != 1 && n_samples != 2 && n_samples != (LUQ_SMP_SUM | 2))
+    return fail(LUQ_ERR_PARAM, "%s: n_samples must be 1, 2 or LUQ_SMP_SUM | 2", name);
+  if (n_samples != 1 && R > 5) return fail(LUQ_ERR_PARAM, "%s: two samples need R <= 5", name);
+  return LUQ_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -87,10 +96,8 @@ luq_status luq_quantize_grad(const void* g, luq_dtype dt, int64_t rows, int64_t 
   const int pw2 = (R & LUQ_ALPHA_PW2) ? 1 : 0;
   R &= ~LUQ_ALPHA_PW2;
   if (R < 4 || R > 6) return fail(LUQ_ERR_PARAM, "%s: R must be 4, 5 or 6", "luq_quantize_grad");
-  if (n_samples != 1 && n_samples != 2)
-    return fail(LUQ_ERR_PARAM, "%s: n_samples must be 1 or 2", "luq_quantize_grad");
-  if (n_samples == 2 && R > 5)
-    return fail(LUQ_ERR_PARAM, "%s: n_samples = 2 needs R <= 5", "luq_quantize_grad");
+  st = check_samples(n_samples, R, "luq_quantize_grad");
+  if (st != LUQ_OK) return st;
   if (!alpha) return fail(LUQ_ERR_NULL, "%s: alpha is NULL", "luq_quantize_grad");
   const int64_t n = rows * cols;
   if (n > 0) {
@@ -121,8 +128,8 @@ luq_status luq_quantize_grad_hindsight(const void* g, luq_dtype dt, int64_t rows
   const int pw2 = (R & LUQ_ALPHA_PW2) ? 1 : 0;
   R &= ~LUQ_ALPHA_PW2;
   if (R < 4 || R > 6) return fail(LUQ_ERR_PARAM, "%s: R must be 4, 5 or 6", fn);
-  if (n_samples != 1 && n_samples != 2) return fail(LUQ_ERR_PARAM, "%s: n_samples must be 1 or 2", fn);
-  if (n_samples == 2 && R > 5) return fail(LUQ_ERR_PARAM, "%s: n_samples = 2 needs R <= 5", fn);
+  st = check_samples(n_samples, R, fn);
+  if (st != LUQ_OK) return st;
   if (!(eta >= 0.0f && eta <= 1.0f)) return fail(LUQ_ERR_PARAM, "%s: eta must be in [0, 1]", fn);
   if (!alpha) return fail(LUQ_ERR_NULL, "%s: alpha is NULL", fn);
   if (!state) return fail(LUQ_ERR_NULL, "%s: state is NULL", fn);
@@ -180,13 +187,20 @@ static luq_status gemm_checks(const char* name, const uint8_t* A, const float* a
   return LUQ_OK;
 }
 
-static luq_status gemm_shape(const char* name, int64_t M, int64_t N, int64_t K) {
+// a_bytes_per_k: 1 for an int8 A operand (summed SMP samples), else codes
+// (half a byte).  Code operands are addressed with 32-bit offsets, so each
+// must stay below 2 GiB with a tile's worth of rows to spare.
+static luq_status gemm_shape(const char* name, int64_t M, int64_t N, int64_t K, int a_bytes_per_k = 0) {
   if (M < 1 || N < 1 || K < 32 || (K & 31))
     return fail(LUQ_ERR_SHAPE, "%s: need M, N >= 1 and K a positive multiple of 32", name);
   if (mul_overflows(M, N) || mul_overflows(M, K) || mul_overflows(N, K))
     return fail(LUQ_ERR_SHAPE, "%s: size overflows", name);
   if (M > INT32_MAX / 2 || N > INT32_MAX / 2)
     return fail(LUQ_ERR_SHAPE, "%s: M and N must be below 2^30", name);
+  const int64_t lim = ((int64_t)1 << 31) - ((int64_t)1 << 20);
+  const int64_t a_bytes = a_bytes_per_k ? (M + 256) * K : (M + 256) * (K / 2);
+  if (a_bytes >= lim || (N + 256) * (K / 2) >= lim)
+    return fail(LUQ_ERR_SHAPE, "%s: a code operand reaches 2 GiB", name);
   return LUQ_OK;
 }
 
@@ -195,8 +209,9 @@ static luq_status gemm_common(const char* name, const uint8_t* A, const float* a
                               int64_t N, int64_t K, float* C, void* ws, size_t ws_bytes,
                               void* stream) {
   if (!A || !alpha || !B || !bscale || !C) return fail(LUQ_ERR_NULL, "%s: NULL operand", name);
-  if (ns != 1 && ns != 2) return fail(LUQ_ERR_PARAM, "%s: n_samples must be 1 or 2", name);
-  luq_status st = gemm_shape(name, M, N, K);
+  if (ns != 1 && ns != 2 && ns != (LUQ_SMP_SUM | 2))
+    return fail(LUQ_ERR_PARAM, "%s: n_samples must be 1, 2 or LUQ_SMP_SUM | 2", name);
+  luq_status st = gemm_shape(name, M, N, K, ns == (LUQ_SMP_SUM | 2) ? 1 : 0);
   if (st != LUQ_OK) return st;
   st = gemm_checks(name, A, alpha, B, bscale, M, N, K, C, luq::gemm_workspace_bytes(M, N, K, ns), ws, ws_bytes);
   if (st != LUQ_OK) return st;
@@ -262,7 +277,8 @@ luq_status luq_conv3x3_dgrad(const uint8_t* g_codes, const float* alpha, int n_s
   const char* fn = "luq_conv3x3_dgrad";
   g_last_error[0] = 0;
   if (B < 0 || H < 0 || W < 0 || C < 0 || Cout < 0) return fail(LUQ_ERR_SHAPE, "%s: negative size", fn);
-  if (n_samples != 1 && n_samples != 2) return fail(LUQ_ERR_PARAM, "%s: n_samples must be 1 or 2", fn);
+  if (n_samples != 1 && n_samples != 2)
+    return fail(LUQ_ERR_PARAM, "%s: n_samples must be 1 or 2 (sample planes)", fn);
   if (B > INT32_MAX || H > INT32_MAX || W > INT32_MAX || C > INT32_MAX || Cout > INT32_MAX ||
       mul_overflows(B, H) || mul_overflows(B * H, W) || mul_overflows(B * H * W, Cout) ||
       mul_overflows(9 * C, Cout))

@@ -1,6 +1,6 @@
 // 4-bit backward and update GEMMs (Eq. backward, Eq. update): A = LUQ codes
-// of the neural gradient (n SMP planes), B = INT4 codes; the tile kernel is in
-// gemm_kernel.hpp.
+// of the neural gradient (n SMP planes, or the int8 sums of two samples),
+// B = INT4 codes; the tile kernel is in gemm_kernel.hpp.
 #include "gemm_kernel.hpp"
 
 namespace luq {
@@ -29,6 +29,8 @@ hipError_t launch_gemm_luq_int4(const uint8_t* A, int64_t a_plane, int ns, const
   a.partial = p.splits > 1 ? static_cast<int32_t*>(ws) : nullptr;
   if (ns == 1)
     return b_signed ? gemm_launch_t<kAcLuq, 1, true>(a, p, st) : gemm_launch_t<kAcLuq, 1, false>(a, p, st);
+  if (ns == kSmpSum)
+    return b_signed ? gemm_launch_t<kAcSum2, 1, true>(a, p, st) : gemm_launch_t<kAcSum2, 1, false>(a, p, st);
   return b_signed ? gemm_launch_t<kAcLuq, 2, true>(a, p, st) : gemm_launch_t<kAcLuq, 2, false>(a, p, st);
 }
 

@@ -37,6 +37,7 @@ namespace luq {
 constexpr int kAcLuq = 0;     // LUQ codes, NS planes (Section 4, 5.1)
 constexpr int kAcInt4S = 1;   // signed INT4 codes (-7..7)
 constexpr int kAcInt4U = 2;   // unsigned INT4 codes (0..15)
+constexpr int kAcSum2 = 3;    // int8 sums of two LUQ samples (Section 5.1), one byte per k
 
 typedef int v4i __attribute__((ext_vector_type(4)));
 typedef int v16i __attribute__((ext_vector_type(16)));
@@ -134,7 +135,8 @@ __device__ __forceinline__ void tile_coords(int bid, int ntm, int ntn, int& tm, 
 // expansions (B: 2^-4 signed, 2^-3 unsigned; an INT4 A the same).
 template <int AC, int NS, bool BSIGNED>
 __device__ __forceinline__ float epilogue_scale(float alpha, float bscale) {
-  float sc = __fmul_rn(__fmul_rn(alpha, 1.0f / NS), bscale) * (BSIGNED ? 0x1p-4f : 0x1p-3f);
+  constexpr float kInvSamples = AC == kAcSum2 ? 0.5f : 1.0f / NS;
+  float sc = __fmul_rn(__fmul_rn(alpha, kInvSamples), bscale) * (BSIGNED ? 0x1p-4f : 0x1p-3f);
   if constexpr (AC == kAcInt4S) sc *= 0x1p-4f;
   if constexpr (AC == kAcInt4U) sc *= 0x1p-3f;
   return sc;
@@ -159,8 +161,10 @@ __device__ __forceinline__ float epilogue_scale(float alpha, float bscale) {
 // the split's end read as zeros and the loop may multiply one zero stage.
 // The 64-deep variant keeps three waves per SIMD.
 //
-// AC is the A operand's code type: LUQ (NS planes) or INT4 (the forward
-// product, NS = 1), expanded like B.
+// AC is the A operand's code type: LUQ (NS planes), INT4 (the forward
+// product, NS = 1), expanded like B, or the int8 sums of two LUQ samples
+// (NS = 1): 32 bytes per 32-deep chunk, whose bytes only need the even / odd
+// k split of the nibble expansions (two byte permutes per 8 values).
 template <int BM, int BN, int BK, int AC, int NS, bool BSIGNED, bool FULLK>
 __global__ __launch_bounds__(kGemmThreads, BK == 64 ? 3 : 1) void gemm_luq_int4_kernel(GemmArgs a) {
   static_assert(BM % 64 == 0 && BN % 64 == 0, "wave tiles are multiples of 32");
@@ -183,7 +187,10 @@ __global__ __launch_bounds__(kGemmThreads, BK == 64 ? 3 : 1) void gemm_luq_int4_
   const int64_t kbeg = (int64_t)blockIdx.y * a.k_chunk;
   const int64_t kend = min(kbeg + a.k_chunk, a.K);
   const int nkt = (int)((kend - kbeg + kBK - 1) / kBK);
-  const int64_t ld = a.K >> 1;  // bytes per operand row
+  constexpr bool kI8 = AC == kAcSum2;
+  constexpr int NA = kI8 ? 2 : NS;          // 16-byte A registers per chunk
+  const int64_t ld = a.K >> 1;              // bytes per B row (and per nibble A row)
+  const int64_t lda = kI8 ? a.K : ld;       // bytes per A row
 
   // Operands are read through buffer descriptors whose range is the operand
   // itself: rows past M (or N) fall outside the range, and a chunk past the
@@ -193,7 +200,7 @@ __global__ __launch_bounds__(kGemmThreads, BK == 64 ? 3 : 1) void gemm_luq_int4_
 #pragma unroll
   for (int s = 0; s < NS; ++s)
     rsa[s] = __builtin_amdgcn_make_buffer_rsrc((void*)(a.A + s * a.a_plane), (short)0,
-                                               (int)(a.M * ld), kBufferFlags);
+                                               (int)(a.M * lda), kBufferFlags);
   const __amdgpu_buffer_rsrc_t rsb =
       __builtin_amdgcn_make_buffer_rsrc((void*)a.B, (short)0, (int)(a.N * ld), kBufferFlags);
   int offa[ACH], kca[ACH], offb[BCH], kcb[BCH];
@@ -201,7 +208,7 @@ __global__ __launch_bounds__(kGemmThreads, BK == 64 ? 3 : 1) void gemm_luq_int4_
   for (int i = 0; i < ACH; ++i) {
     const int c = tid + i * kGemmThreads, row = c / KC, kc = c % KC;
     kca[i] = kc * 32;
-    offa[i] = (int)((m0 + row) * ld + (kbeg >> 1) + kc * 16);
+    offa[i] = kI8 ? (int)((m0 + row) * lda + kbeg + kc * 32) : (int)((m0 + row) * ld + (kbeg >> 1) + kc * 16);
   }
 #pragma unroll
   for (int i = 0; i < BCH; ++i) {
@@ -211,7 +218,7 @@ __global__ __launch_bounds__(kGemmThreads, BK == 64 ? 3 : 1) void gemm_luq_int4_
   }
 
   struct Regs {
-    v4u a[NS][ACH];
+    v4u a[NA][ACH];
     v4u b[BCH];
   };
   // Work of one stage is split into KS pieces, one per 32-deep k-step: piece
@@ -222,9 +229,16 @@ __global__ __launch_bounds__(kGemmThreads, BK == 64 ? 3 : 1) void gemm_luq_int4_
 #pragma unroll
     for (int i = 0; i < ACH; ++i) {
       if (i % KS != kk) continue;
-      const int off = FULLK || (k0 + kca[i]) < kend ? offa[i] + t * (kBK / 2) : kOutOfRange;
+      const bool in = FULLK || (k0 + kca[i]) < kend;
+      if constexpr (kI8) {
+        const int off = in ? offa[i] + t * kBK : kOutOfRange;
+        r.a[0][i] = __builtin_amdgcn_raw_buffer_load_b128(rsa[0], off, 0, 0);
+        r.a[1][i] = __builtin_amdgcn_raw_buffer_load_b128(rsa[0], in ? off + 16 : kOutOfRange, 0, 0);
+      } else {
+        const int off = in ? offa[i] + t * (kBK / 2) : kOutOfRange;
 #pragma unroll
-      for (int s = 0; s < NS; ++s) r.a[s][i] = __builtin_amdgcn_raw_buffer_load_b128(rsa[s], off, 0, 0);
+        for (int s = 0; s < NS; ++s) r.a[s][i] = __builtin_amdgcn_raw_buffer_load_b128(rsa[s], off, 0, 0);
+      }
     }
 #pragma unroll
     for (int i = 0; i < BCH; ++i) {
@@ -242,7 +256,15 @@ __global__ __launch_bounds__(kGemmThreads, BK == 64 ? 3 : 1) void gemm_luq_int4_
       const int c = tid + i * kGemmThreads, row = c / KC, kc = c % KC;
       uint32_t w[8];
       const uint32_t x0[4] = {r.a[0][i][0], r.a[0][i][1], r.a[0][i][2], r.a[0][i][3]};
-      if constexpr (AC != kAcLuq) {
+      if constexpr (kI8) {
+        // bytes of k = 8d .. 8d+7 are words 2d, 2d+1 of the 32-byte chunk
+        const uint32_t x[8] = {x0[0], x0[1], x0[2], x0[3], r.a[1][i][0], r.a[1][i][1], r.a[1][i][2], r.a[1][i][3]};
+#pragma unroll
+        for (int d = 0; d < 4; ++d) {
+          w[2 * d] = __builtin_amdgcn_perm(x[2 * d + 1], x[2 * d], 0x06040200u);      // k even
+          w[2 * d + 1] = __builtin_amdgcn_perm(x[2 * d + 1], x[2 * d], 0x07050301u);  // k odd
+        }
+      } else if constexpr (AC != kAcLuq) {
 #pragma unroll
         for (int d = 0; d < 4; ++d) expand_int4<AC == kAcInt4S>(x0[d], w[2 * d], w[2 * d + 1]);
       } else if constexpr (NS == 1) {

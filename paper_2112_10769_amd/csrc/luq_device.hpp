@@ -176,6 +176,64 @@ __device__ __forceinline__ void transpose8x8_nibbles(uint32_t (&r)[8]) {
   swap_fields(r[3], r[7], 16, 0x0000FFFFu);
 }
 
+// ---------------------------------------------------------------------------
+// SMP operand as bytes (Section 5.1: the average of two samples taken with
+// one alpha is alpha/2 times the sum of their decoded values).
+// ---------------------------------------------------------------------------
+
+// The 8 nibbles of x, one per byte in element order: lo = elements 0..3,
+// hi = elements 4..7.
+__device__ __forceinline__ void spread_nibbles(uint32_t x, uint32_t& lo, uint32_t& hi) {
+  const uint32_t t0 = __builtin_amdgcn_perm(x, x, 0x01010000u);  // bytes b0 b0 b1 b1
+  const uint32_t t1 = __builtin_amdgcn_perm(x, x, 0x03030202u);  // bytes b2 b2 b3 b3
+  lo = (t0 & 0x000F000Fu) | ((t0 >> 4) & 0x0F000F00u);
+  hi = (t1 & 0x000F000Fu) | ((t1 >> 4) & 0x0F000F00u);
+}
+
+// Sum of the decoded values of two LUQ codes per byte (one nibble per byte):
+// magnitudes 2^(e-1) from a byte LUT, added (<= 64 for fields <= 6, so no
+// carries), then negated where either code carries a sign (both samples of
+// an element have its sign; zero codes have none).
+__device__ __forceinline__ uint32_t smp_sum4(uint32_t n0, uint32_t n1) {
+  const uint32_t t_lo = 0x04020100u, t_hi = 0x40201008u;  // 0, 1, 2, 4, 8, 16, 32, 64
+  const uint32_t m = __builtin_amdgcn_perm(t_hi, t_lo, n0 & 0x07070707u) +
+                     __builtin_amdgcn_perm(t_hi, t_lo, n1 & 0x07070707u);
+  const uint32_t sg = ((n0 | n1) >> 3) & 0x01010101u;
+  return (m ^ ((sg << 8) - sg)) + sg;  // (m ^ 0xFF) + 1 in the negative bytes
+}
+
+// int8 sums of the 8 elements of two sample code words, in element order.
+__device__ __forceinline__ void smp_sum_bytes(uint32_t c0, uint32_t c1, uint32_t& lo, uint32_t& hi) {
+  uint32_t l0, h0, l1, h1;
+  spread_nibbles(c0, l0, h0);
+  spread_nibbles(c1, l1, h1);
+  lo = smp_sum4(l0, l1);
+  hi = smp_sum4(h0, h1);
+}
+
+// 4x4 transpose of bytes: r[i] holds row i (byte j = column j); c[j] gets
+// column j (byte i = row i).
+__device__ __forceinline__ void transpose4x4_bytes(const uint32_t (&r)[4], uint32_t (&c)[4]) {
+  const uint32_t t0 = __builtin_amdgcn_perm(r[1], r[0], 0x05010400u);  // r0c0 r1c0 r0c1 r1c1
+  const uint32_t t1 = __builtin_amdgcn_perm(r[1], r[0], 0x07030602u);  // r0c2 r1c2 r0c3 r1c3
+  const uint32_t t2 = __builtin_amdgcn_perm(r[3], r[2], 0x05010400u);
+  const uint32_t t3 = __builtin_amdgcn_perm(r[3], r[2], 0x07030602u);
+  c[0] = __builtin_amdgcn_perm(t2, t0, 0x05040100u);
+  c[1] = __builtin_amdgcn_perm(t2, t0, 0x07060302u);
+  c[2] = __builtin_amdgcn_perm(t3, t1, 0x05040100u);
+  c[3] = __builtin_amdgcn_perm(t3, t1, 0x07060302u);
+}
+
+typedef uint32_t v2u32 __attribute__((ext_vector_type(2)));
+
+// 8 bytes (lo, hi) at p (8-byte aligned).
+template <bool NT>
+__device__ __forceinline__ void store_word2(uint8_t* p, uint32_t lo, uint32_t hi) {
+  const v2u32 v = {lo, hi};
+  if constexpr (NT) __builtin_nontemporal_store(v, reinterpret_cast<v2u32*>(p));
+  else *reinterpret_cast<v2u32*>(p) = v;
+}
+
 // Stores the first `nbytes` (0..4) bytes of w at p (ragged tails).
 __device__ __forceinline__ void store_bytes(uint8_t* p, uint32_t w, int nbytes) {
   for (int i = 0; i < nbytes; ++i) p[i] = (uint8_t)(w >> (8 * i));

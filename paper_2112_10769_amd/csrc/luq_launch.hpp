@@ -8,6 +8,10 @@
 
 namespace luq {
 
+// Sample-count argument meaning two SMP samples stored as one int8 sum per
+// element (LUQ_SMP_SUM | 2 in the C ABI).
+constexpr int kSmpSum = 0x12;
+
 // ceil(n/2) rounded up to 256 bytes: the distance between SMP planes.
 inline size_t plane_bytes(int64_t n) {
   const size_t b = (size_t)((n + 1) / 2);

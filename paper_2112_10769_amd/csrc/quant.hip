@@ -126,10 +126,16 @@ __global__ __launch_bounds__(1024) void fold_partials_kernel(const uint32_t* __r
 constexpr int kLuqTileLg = 12, kInt4TileLg = 13;
 constexpr int kTilePad = 4;  // LDS words between column groups (keeps 16-byte alignment)
 
-template <int NS, typename Enc>
+//
+// SUM (two SMP samples stored as one int8 per element): the two code words
+// of an item become 8 bytes of sums (elements 0..3 in the first word), which
+// take the places of the two planes in LDS; phase B transposes 4x4 byte
+// blocks and stores 8 bytes (8 rows) per column.
+template <int NS, typename Enc, bool SUM = false>
 __device__ __forceinline__ void encode_tiles(const Enc& enc, int64_t rows, int64_t cols, int lg,
                                              int lt, uint8_t* codes, uint8_t* codes_t,
                                              int64_t plane, uint32_t* lds, uint32_t& mx) {
+  static_assert(!SUM || NS == 2, "the summed operand takes two samples");
   const int tw = 1 << lt, tg = 1 << lg, tr = tw >> lg, pitch = tr + kTilePad;
   const int64_t cgs = cols >> 3;
   const int64_t ntr = (rows + tr - 1) / tr, ntc = (cgs + tg - 1) / tg;
@@ -163,9 +169,17 @@ __device__ __forceinline__ void encode_tiles(const Enc& enc, int64_t rows, int64
         for (int s = 0; s < NS; ++s) w[s] = 0;
         if (ok[u]) {
 #pragma unroll
-          for (int s = 0; s < NS; ++s) {
-            w[s] = enc.word(v[u], (uint64_t)(e0[u] >> 3), s);
-            if (codes) store_word<Enc::kNT>(codes + s * plane + (e0[u] >> 1), w[s]);
+          for (int s = 0; s < NS; ++s) w[s] = enc.word(v[u], (uint64_t)(e0[u] >> 3), s);
+          if constexpr (SUM) {
+            uint32_t lo, hi;
+            smp_sum_bytes(w[0], w[1], lo, hi);
+            w[0] = lo;
+            w[1] = hi;
+            if (codes) store_word2<Enc::kNT>(codes + e0[u], lo, hi);
+          } else {
+#pragma unroll
+            for (int s = 0; s < NS; ++s)
+              if (codes) store_word<Enc::kNT>(codes + s * plane + (e0[u] >> 1), w[s]);
           }
         }
 #pragma unroll
@@ -178,6 +192,22 @@ __device__ __forceinline__ void encode_tiles(const Enc& enc, int64_t rows, int64
       const int rb = q & (rbs - 1), g = q / rbs;
       const int64_t row0 = r0 + rb * 8, cg = g0 + g;
       if (row0 >= rows || cg >= cgs) continue;
+      if constexpr (SUM) {
+        // lds plane 0: bytes of columns 0..3 of each row, plane 1: columns 4..7
+        uint8_t* dst = codes_t + (cg * 8) * rows + row0;
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+          const uint4* src = reinterpret_cast<const uint4*>(lds + (h * tg + g) * pitch + rb * 8);
+          const uint4 a = src[0], b = src[1];
+          const uint32_t ra[4] = {a.x, a.y, a.z, a.w}, rb4[4] = {b.x, b.y, b.z, b.w};
+          uint32_t ca[4], cb[4];
+          transpose4x4_bytes(ra, ca);   // rows 0..3
+          transpose4x4_bytes(rb4, cb);  // rows 4..7
+#pragma unroll
+          for (int c = 0; c < 4; ++c) store_word2<Enc::kNT>(dst + (h * 4 + c) * rows, ca[c], cb[c]);
+        }
+        continue;
+      }
 #pragma unroll
       for (int s = 0; s < NS; ++s) {
         const uint4* src = reinterpret_cast<const uint4*>(lds + (s * tg + g) * pitch + rb * 8);
@@ -356,9 +386,25 @@ __device__ __forceinline__ LuqParams luq_block_params(const LuqArgs& a) {
   return p;
 }
 
+// Codes of group g (elements 8g .. 8g+7): one word per sample plane, or with
+// SUM the 8 int8 sums of the two samples.
+template <bool NT, int NS, bool SUM, bool SCALED, bool HS>
+__device__ __forceinline__ void luq_emit_group(const LuqArgs& a, const LuqParams& p, const U8& v, int64_t g) {
+  if constexpr (SUM) {
+    uint32_t lo, hi;
+    smp_sum_bytes(luq_word<SCALED, HS>(v, (uint64_t)g, 0, a.counter, a.k0, a.k1, p),
+                  luq_word<SCALED, HS>(v, (uint64_t)g, 1, a.counter, a.k0, a.k1, p), lo, hi);
+    store_word2<NT>(a.codes + g * 8, lo, hi);
+  } else {
+#pragma unroll
+    for (int s = 0; s < NS; ++s)
+      store_word<NT>(a.codes + s * a.plane + g * 4, luq_word<SCALED, HS>(v, (uint64_t)g, s, a.counter, a.k0, a.k1, p));
+  }
+}
+
 // Flat row-major codes; groups of 8 elements along the flattened tensor.
 // With HS the fields are capped and the thread's max key is returned.
-template <bool BF16, bool NT, int NS, bool SCALED, bool HS = false>
+template <bool BF16, bool NT, int NS, bool SCALED, bool HS = false, bool SUM = false>
 __device__ __forceinline__ uint32_t luq_flat_body(const LuqArgs& a, const LuqParams& p) {
   uint32_t mx = 0;
   const int64_t nfull = a.n >> 3;
@@ -373,37 +419,37 @@ __device__ __forceinline__ uint32_t luq_flat_body(const LuqArgs& a, const LuqPar
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
       if (HS) mx = max(mx, max_key8(v[u]));
-#pragma unroll
-      for (int s = 0; s < NS; ++s)
-        store_word<NT>(a.codes + s * a.plane + (g + u * stride) * 4, luq_word<SCALED, HS>(v[u], (uint64_t)(g + u * stride), s, a.counter, a.k0, a.k1, p));
+      luq_emit_group<NT, NS, SUM, SCALED, HS>(a, p, v[u], g + u * stride);
     }
   }
   for (; g + stride < nfull; g += 2 * stride) {
     const U8 v0 = load8<BF16, NT>(a.g, g * 8);
     const U8 v1 = load8<BF16, NT>(a.g, (g + stride) * 8);
     if (HS) mx = max(mx, max(max_key8(v0), max_key8(v1)));
-#pragma unroll
-    for (int s = 0; s < NS; ++s) {
-      store_word<NT>(a.codes + s * a.plane + g * 4, luq_word<SCALED, HS>(v0, (uint64_t)g, s, a.counter, a.k0, a.k1, p));
-      store_word<NT>(a.codes + s * a.plane + (g + stride) * 4,
-                     luq_word<SCALED, HS>(v1, (uint64_t)(g + stride), s, a.counter, a.k0, a.k1, p));
-    }
+    luq_emit_group<NT, NS, SUM, SCALED, HS>(a, p, v0, g);
+    luq_emit_group<NT, NS, SUM, SCALED, HS>(a, p, v1, g + stride);
   }
   if (g < nfull) {
     const U8 v = load8<BF16, NT>(a.g, g * 8);
     if (HS) mx = max(mx, max_key8(v));
-#pragma unroll
-    for (int s = 0; s < NS; ++s)
-      store_word<NT>(a.codes + s * a.plane + g * 4, luq_word<SCALED, HS>(v, (uint64_t)g, s, a.counter, a.k0, a.k1, p));
+    luq_emit_group<NT, NS, SUM, SCALED, HS>(a, p, v, g);
   }
   if ((a.n & 7) && blockIdx.x == 0 && threadIdx.x == 0) {
     const U8 v = load8_tail<BF16>(a.g, nfull * 8, a.n);  // missing elements read +0
     if (HS) mx = max(mx, max_key8(v));
+    const int tail = (int)(a.n & 7);
+    if constexpr (SUM) {
+      uint32_t lo, hi;
+      smp_sum_bytes(luq_word<SCALED, HS>(v, (uint64_t)nfull, 0, a.counter, a.k0, a.k1, p),
+                    luq_word<SCALED, HS>(v, (uint64_t)nfull, 1, a.counter, a.k0, a.k1, p), lo, hi);
+      store_bytes(a.codes + nfull * 8, lo, min(tail, 4));
+      store_bytes(a.codes + nfull * 8 + 4, hi, max(tail - 4, 0));
+    } else {
 #pragma unroll
-    for (int s = 0; s < NS; ++s)
-      store_bytes(a.codes + s * a.plane + nfull * 4,
-                  luq_word<SCALED, HS>(v, (uint64_t)nfull, s, a.counter, a.k0, a.k1, p),
-                  (int)(((a.n & 7) + 1) >> 1));
+      for (int s = 0; s < NS; ++s)
+        store_bytes(a.codes + s * a.plane + nfull * 4,
+                    luq_word<SCALED, HS>(v, (uint64_t)nfull, s, a.counter, a.k0, a.k1, p), (tail + 1) >> 1);
+    }
   }
   return mx;
 }
@@ -427,18 +473,18 @@ __device__ __forceinline__ void write_block_max(uint32_t mx, uint32_t* part_out)
   if (threadIdx.x == 0) part_out[blockIdx.x] = m;
 }
 
-template <bool BF16, bool NT, int NS, bool HS = false>
+template <bool BF16, bool NT, int NS, bool HS = false, bool SUM = false>
 __global__ __launch_bounds__(kThreads) void luq_encode_flat_kernel(LuqArgs a) {
   const LuqParams p = luq_block_params<HS>(a);
-  if (p.zero) {  // alpha is 0 or NaN: every code is 0
-    const int64_t nbytes = (a.n + 1) >> 1;
+  if (p.zero) {  // alpha is 0 or NaN: every code (or sum) is 0
+    const int64_t nbytes = SUM ? a.n : (a.n + 1) >> 1;
     for (int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x; i < nbytes; i += (int64_t)gridDim.x * kThreads)
-      for (int s = 0; s < NS; ++s) a.codes[s * a.plane + i] = 0;
+      for (int s = 0; s < (SUM ? 1 : NS); ++s) a.codes[s * a.plane + i] = 0;
     if (HS) write_block_max(flat_max_only<BF16, NT>(a), a.part_out);
     return;
   }
-  const uint32_t mx = p.S != 1.0f ? luq_flat_body<BF16, NT, NS, true, HS>(a, p)
-                                  : luq_flat_body<BF16, NT, NS, false, HS>(a, p);
+  const uint32_t mx = p.S != 1.0f ? luq_flat_body<BF16, NT, NS, true, HS, SUM>(a, p)
+                                  : luq_flat_body<BF16, NT, NS, false, HS, SUM>(a, p);
   if (HS) write_block_max(mx, a.part_out);
 }
 
@@ -454,17 +500,17 @@ struct LuqEnc {
   }
 };
 
-template <bool BF16, bool NT, int NS, bool HS = false>
+template <bool BF16, bool NT, int NS, bool HS = false, bool SUM = false>
 __global__ __launch_bounds__(kThreads) void luq_encode_tile_kernel(LuqArgs a, int lg, int lt) {
   __shared__ __attribute__((aligned(16))) uint32_t lds[NS * ((1 << kLuqTileLg) + 32 * kTilePad)];
   const LuqParams p = luq_block_params<HS>(a);
   uint32_t mx = 0;
   if (p.S != 1.0f)
-    encode_tiles<NS>(LuqEnc<BF16, NT, true, HS>{&a, &p}, a.rows, a.cols, lg, lt, a.codes, a.codes_t, a.plane,
-                     lds, mx);
+    encode_tiles<NS, LuqEnc<BF16, NT, true, HS>, SUM>(LuqEnc<BF16, NT, true, HS>{&a, &p}, a.rows, a.cols, lg, lt,
+                                                      a.codes, a.codes_t, a.plane, lds, mx);
   else
-    encode_tiles<NS>(LuqEnc<BF16, NT, false, HS>{&a, &p}, a.rows, a.cols, lg, lt, a.codes, a.codes_t, a.plane,
-                     lds, mx);
+    encode_tiles<NS, LuqEnc<BF16, NT, false, HS>, SUM>(LuqEnc<BF16, NT, false, HS>{&a, &p}, a.rows, a.cols, lg, lt,
+                                                       a.codes, a.codes_t, a.plane, lds, mx);
   if (HS) write_block_max(mx, a.part_out);
 }
 
@@ -674,21 +720,30 @@ static const uint32_t* encode_partials(const uint32_t* partial, int nblocks, int
 // and so are its code stores then.
 static bool stream_reads(int64_t n, bool bf16) { return n * (bf16 ? 2 : 4) > kCacheBytes; }
 
-template <bool BF16, bool NT>
-static void luq_encode_launch(const LuqArgs& a, int ns, hipStream_t st) {
+// ns: 1 or 2 sample planes, or kSmpSum (two samples stored as int8 sums).
+template <bool BF16, bool NT, bool HS>
+static int luq_encode_launch(const LuqArgs& a, int ns, hipStream_t st) {
   if (a.codes_t) {
     const TileShape t = tile_shape(a.rows, a.cols, kLuqTileLg);
     if (ns == 1)
-      hipLaunchKernelGGL((luq_encode_tile_kernel<BF16, NT, 1>), dim3(t.blocks), dim3(kThreads), 0, st, a, t.lg, t.lt);
+      hipLaunchKernelGGL((luq_encode_tile_kernel<BF16, NT, 1, HS>), dim3(t.blocks), dim3(kThreads), 0, st, a, t.lg,
+                         t.lt);
+    else if (ns == 2)
+      hipLaunchKernelGGL((luq_encode_tile_kernel<BF16, NT, 2, HS>), dim3(t.blocks), dim3(kThreads), 0, st, a, t.lg,
+                         t.lt);
     else
-      hipLaunchKernelGGL((luq_encode_tile_kernel<BF16, NT, 2>), dim3(t.blocks), dim3(kThreads), 0, st, a, t.lg, t.lt);
-  } else {
-    const int nb = encode_blocks_flat(a.n);
-    if (ns == 1)
-      hipLaunchKernelGGL((luq_encode_flat_kernel<BF16, NT, 1>), dim3(nb), dim3(kThreads), 0, st, a);
-    else
-      hipLaunchKernelGGL((luq_encode_flat_kernel<BF16, NT, 2>), dim3(nb), dim3(kThreads), 0, st, a);
+      hipLaunchKernelGGL((luq_encode_tile_kernel<BF16, NT, 2, HS, true>), dim3(t.blocks), dim3(kThreads), 0, st, a,
+                         t.lg, t.lt);
+    return t.blocks;
   }
+  const int nb = encode_blocks_flat(a.n);
+  if (ns == 1)
+    hipLaunchKernelGGL((luq_encode_flat_kernel<BF16, NT, 1, HS>), dim3(nb), dim3(kThreads), 0, st, a);
+  else if (ns == 2)
+    hipLaunchKernelGGL((luq_encode_flat_kernel<BF16, NT, 2, HS>), dim3(nb), dim3(kThreads), 0, st, a);
+  else
+    hipLaunchKernelGGL((luq_encode_flat_kernel<BF16, NT, 2, HS, true>), dim3(nb), dim3(kThreads), 0, st, a);
+  return nb;
 }
 
 template <bool BF16>
@@ -697,9 +752,9 @@ static hipError_t luq_launch_t(LuqArgs a, int ns, int nmax, hipStream_t st) {
   launch_max_pass<BF16, 0>(a.g, a.n, nmax, ws, st);
   a.partial = encode_partials(ws, nmax, &a.nparts);
   if (stream_reads(a.n, BF16))
-    luq_encode_launch<BF16, true>(a, ns, st);
+    luq_encode_launch<BF16, true, false>(a, ns, st);
   else
-    luq_encode_launch<BF16, false>(a, ns, st);
+    luq_encode_launch<BF16, false, false>(a, ns, st);
   return hipGetLastError();
 }
 
@@ -732,26 +787,6 @@ hipError_t launch_luq_quantize(const void* g, int bf16, int64_t rows, int64_t co
   return bf16 ? luq_launch_t<true>(a, ns, a.nparts, st) : luq_launch_t<false>(a, ns, a.nparts, st);
 }
 
-template <bool BF16, bool NT>
-static int luq_hindsight_encode(const LuqArgs& a, int ns, hipStream_t st) {
-  if (a.codes_t) {
-    const TileShape t = tile_shape(a.rows, a.cols, kLuqTileLg);
-    if (ns == 1)
-      hipLaunchKernelGGL((luq_encode_tile_kernel<BF16, NT, 1, true>), dim3(t.blocks), dim3(kThreads), 0, st, a, t.lg,
-                         t.lt);
-    else
-      hipLaunchKernelGGL((luq_encode_tile_kernel<BF16, NT, 2, true>), dim3(t.blocks), dim3(kThreads), 0, st, a, t.lg,
-                         t.lt);
-    return t.blocks;
-  }
-  const int nb = encode_blocks_flat(a.n);
-  if (ns == 1)
-    hipLaunchKernelGGL((luq_encode_flat_kernel<BF16, NT, 1, true>), dim3(nb), dim3(kThreads), 0, st, a);
-  else
-    hipLaunchKernelGGL((luq_encode_flat_kernel<BF16, NT, 2, true>), dim3(nb), dim3(kThreads), 0, st, a);
-  return nb;
-}
-
 hipError_t launch_luq_quantize_hindsight(const void* g, int bf16, int64_t rows, int64_t cols, int R, int pw2,
                                          uint64_t seed, uint32_t counter, int ns, float eta, uint8_t* codes,
                                          uint8_t* codes_t, float* state, float* alpha, float* maxabs, void* ws,
@@ -779,8 +814,9 @@ hipError_t launch_luq_quantize_hindsight(const void* g, int bf16, int64_t rows, 
   int nblocks = 0;
   if (n > 0) {
     const bool nt = stream_reads(n, bf16 != 0);
-    nblocks = bf16 ? (nt ? luq_hindsight_encode<true, true>(a, ns, st) : luq_hindsight_encode<true, false>(a, ns, st))
-                   : (nt ? luq_hindsight_encode<false, true>(a, ns, st) : luq_hindsight_encode<false, false>(a, ns, st));
+    nblocks = bf16 ? (nt ? luq_encode_launch<true, true, true>(a, ns, st) : luq_encode_launch<true, false, true>(a, ns, st))
+                   : (nt ? luq_encode_launch<false, true, true>(a, ns, st)
+                         : luq_encode_launch<false, false, true>(a, ns, st));
   }
   hipLaunchKernelGGL(hindsight_fold_kernel, dim3(1), dim3(1024), 0, st, a.part_out, nblocks, state,
                      1.0f - eta, eta, R, pw2 != 0, alpha, maxabs);  // c1 = fl32(1 - eta) (host float arithmetic)

@@ -208,3 +208,21 @@ def _cv(**kw):
 ])
 def test_conv_dgrad_validation(kw, status):
     assert _cv(**kw) == status
+
+
+def test_smp_sum_sample_counts():
+    """n_samples accepts 1, 2 and LUQ_SMP_SUM | 2; two samples need R <= 5;
+    the convolution takes sample planes only."""
+    SUM2 = luq.SMP_SUM | 2
+    args = lambda ns, R: (P, 0, 8, 8, R, 0, 0, ns, P2, NUL, P3, NUL, P, WS, None)
+    assert LIB.luq_quantize_grad(*args(SUM2, 6)) == 4
+    assert LIB.luq_quantize_grad(*args(0x11, 4)) == 4
+    assert LIB.luq_quantize_grad(*args(0x10, 4)) == 4
+    assert LIB.luq_quantize_grad(*args(3, 4)) == 4
+    assert LIB.luq_quantize_grad(P, 0, 8, 8, 4, 0, 0, SUM2, NUL, NUL, P3, NUL, P, WS, None) == 1  # no output
+    assert _dg(ns=SUM2, g=NUL) == 1
+    assert _dg(ns=0x11) == 4
+    assert _dg(ns=SUM2, K=48) == 2
+    # an int8 operand of 2^31 bytes: M * K reaches the 32-bit offset limit
+    assert _dg(ns=SUM2, M=1 << 17, K=1 << 14) == 2
+    assert _cv(ns=SUM2) == 4

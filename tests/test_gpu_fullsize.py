@@ -147,13 +147,13 @@ def mlp_data():
     return d
 
 
-@pytest.fixture(scope="module", params=[1, 2], ids=["ns1", "smp2"])
+@pytest.fixture(scope="module", params=[1, 2, 0x12], ids=["ns1", "smp2", "smp2sum"])
 def mlp(L, mlp_data, request):
     import bench
     ns = request.param
     stages, _, d = bench.build_mlp(L, torch, DEV, ns=ns, d={k: mlp_data[k] for k in ("g", "x", "W")})
     _run(stages, f"mlp ns={ns}")
-    out = {"ns": ns, "dev": d["dev"]}
+    out = {"ns": ns & 0xF, "summed": bool(ns & L.SMP_SUM), "dev": d["dev"]}
     yield out
     d["dev"].clear()
     torch.cuda.empty_cache()
@@ -170,6 +170,14 @@ def test_mlp_luq_sampled_codes_and_layouts(mlp, mlp_data):
     pb = (n + 1) // 2
     pb_pad = (pb + 255) // 256 * 256
     gc, gct = host(dv["gc"]), host(dv["gct"])
+    if mlp["summed"]:
+        sums = gc[:n].view(np.int8)
+        for a, b in _sampled_ranges(n, 24, 4096, 100):
+            planes = np.stack([pack_nibbles(oluq.luq_nibbles_range(mlp_data["gf"].ravel()[a:b], a, alpha, 4, 0, 0, s))
+                               for s in range(2)])
+            assert np.array_equal(sums[a:b], oluq.luq_smp_sum(planes, b - a)), f"sums [{a}, {b})"
+        assert np.array_equal(gct[:n].view(np.int8).reshape(F, T), sums.reshape(T, F).T), "sums transposed layout"
+        return
     for s in range(ns):
         plane = unpack_nibbles(gc[s * pb_pad:s * pb_pad + pb], n)
         _valid_code_set(plane)
