@@ -1,11 +1,13 @@
-"""Pins for the convolution activation-gradient oracle (CPU).
+"""Pins for the convolution gradient oracles (CPU): activation gradient,
+weight gradient and the lowering (im2col) of the activations.
 
-Pinned by a pure-Python loop over the definition of the gradient of a 3x3,
+Pinned by pure-Python loops over the definitions of the gradients of a 3x3,
 stride 1, zero-padded convolution with codes decoded from the bits directly;
-by the adjoint identity <conv(a), g> = <a, dact> with the forward
-convolution computed by scipy's 2-D correlation (an independent library
-routine); and by the equality of the per-tap gather with the lowered GEMM
-(Eq. backward) folded back onto pixels.
+by the adjoint identities <conv(a), g> = <a, dact> and <dW, K> = <g, conv(a;
+K)> with the forward convolution computed by scipy's 2-D correlation (an
+independent library routine); by the equality of the per-tap sums with the
+lowered GEMMs (Eqs. backward and update); and the lowering by a direct
+gather with explicit bounds checks.
 """
 import numpy as np
 import pytest
@@ -104,3 +106,92 @@ def test_equals_lowered_gemm_folded_onto_pixels(ns, wsig):
     pix = [0, 7, T - 1, 31]
     sub, _ = conv3x3_dgrad_ref(planes, alpha, wc, ws, wsig, B, H, W, C, Cout, pixels=pix)
     assert np.array_equal(sub, ref[pix])
+
+
+# ----------------------------- weight gradient -----------------------------
+
+from oracle.conv import conv3x3_wgrad_ref  # noqa: E402
+from oracle.gemm import gemm_wgrad_ref  # noqa: E402
+from oracle.im2col import im2col3x3_codes  # noqa: E402
+
+
+def _wcase(B, H, W, C, Cout, ns, seed, asig):
+    g = synth.lognormal_grad((B * H * W, Cout), -4.0, 2.0, 0.3, [seed, 1])
+    a = synth.normal((B * H * W, C), 1.0, [seed, 2])
+    planes, alpha, _ = luq_quantize(g, R=4, seed=seed, counter=3, n_samples=ns)
+    ac, sa = int4_quantize(a if asig else np.abs(a), is_signed=asig)
+    return planes, alpha, ac, sa
+
+
+@pytest.mark.parametrize("ns,asig", [(1, False), (2, True)])
+def test_wgrad_matches_loop_over_the_definition(ns, asig):
+    B, H, W, C, Cout = 2, 3, 4, 2, 3
+    planes, alpha, ac, sa = _wcase(B, H, W, C, Cout, ns, 70, asig)
+    ref, absref = conv3x3_wgrad_ref(planes, alpha, ac, sa, asig, B, H, W, C, Cout)
+    want = np.zeros((Cout, 9 * C))
+    for o in range(Cout):
+        for kh in range(3):
+            for kw in range(3):
+                for c in range(C):
+                    acc = 0
+                    for b in range(B):
+                        for y in range(H):
+                            for x in range(W):
+                                ys, xs = y + kh - 1, x + kw - 1
+                                if not (0 <= ys < H and 0 <= xs < W):
+                                    continue
+                                t, ts = (b * H + y) * W + x, (b * H + ys) * W + xs
+                                gv = sum(_luq_val(_nib(p, t * Cout + o)) for p in planes)
+                                av = _int4_val(_nib(ac, ts * C + c), asig)
+                                acc += gv * av
+                    want[o, (kh * 3 + kw) * C + c] = acc * float(alpha) / ns * float(sa)
+    assert np.array_equal(ref, want)
+    assert np.all(absref >= np.abs(ref))
+
+
+@pytest.mark.parametrize("ns,asig", [(1, False), (2, True), (1, True)])
+def test_wgrad_equals_gemm_on_lowered_activations(ns, asig):
+    """Two formulations: the per-tap sum and Eq. update on the im2col lowering."""
+    B, H, W, C, Cout = 2, 5, 7, 4, 6
+    planes, alpha, ac, sa = _wcase(B, H, W, C, Cout, ns, 71, asig)
+    T = B * H * W
+    ref, absref = conv3x3_wgrad_ref(planes, alpha, ac, sa, asig, B, H, W, C, Cout)
+    col = im2col3x3_codes(ac, B, H, W, C)
+    low, lowabs = gemm_wgrad_ref(planes, alpha, col, sa, asig, T, Cout, 9 * C)
+    assert np.allclose(ref, low, rtol=1e-12, atol=0)
+    assert np.allclose(absref, lowabs, rtol=1e-12, atol=0)
+
+
+def test_wgrad_adjoint_of_scipy_correlation():
+    """<dW, K> = <g, conv(a; K)> on integer codes for a random integer kernel
+    K [Cout][3][3][C], the forward convolution by scipy.signal.correlate2d."""
+    B, H, W, C, Cout = 2, 6, 5, 3, 4
+    planes, alpha, ac, sa = _wcase(B, H, W, C, Cout, 1, 72, True)
+    G = luq_decode_int(planes[0], B * H * W * Cout).reshape(B, H, W, Cout).astype(np.float64)
+    A = int4_decode_int(ac, B * H * W * C, True).reshape(B, H, W, C).astype(np.float64)
+    K = np.random.default_rng(9).integers(-5, 6, size=(Cout, 3, 3, C)).astype(np.float64)
+    z = np.zeros((B, H, W, Cout))
+    for b in range(B):
+        for o in range(Cout):
+            for c in range(C):
+                z[b, :, :, o] += correlate2d(A[b, :, :, c], K[o, :, :, c], mode="same", fillvalue=0)
+    dW, _ = conv3x3_wgrad_ref(planes, np.float32(1), ac, np.float32(1), True, B, H, W, C, Cout)
+    assert np.sum(z * G) == np.sum(dW.reshape(Cout, 3, 3, C) * K)
+    # a flipped tap orientation breaks it
+    assert np.sum(z * G) != np.sum(np.flip(dW.reshape(Cout, 3, 3, C), axis=(1, 2)) * K)
+
+
+def test_im2col_lowering_against_padded_slices():
+    """The lowering oracle against a direct gather with explicit bounds checks."""
+    B, H, W, C = 2, 4, 5, 3
+    codes = np.random.default_rng(3).integers(0, 256, size=(B * H * W * C + 1) // 2, dtype=np.uint8)
+    col = im2col3x3_codes(codes, B, H, W, C)
+    for t in range(B * H * W):
+        b, rem = divmod(t, H * W)
+        y, x = divmod(rem, W)
+        for kh in range(3):
+            for kw in range(3):
+                for c in range(C):
+                    ys, xs = y + kh - 1, x + kw - 1
+                    want = _nib(codes, ((b * H + ys) * W + xs) * C + c) if (0 <= ys < H and 0 <= xs < W) else 0
+                    assert _nib(col, t * 9 * C + (kh * 3 + kw) * C + c) == want
