@@ -9,9 +9,10 @@ inputs resident in HBM:
   INT4 of the activations (+ 3x3 im2col on codes for the conv workload),
   INT4 of the weights (transposed codes), the dX GEMM and the dW GEMM.
 For the default conv workload (ResNet-50 3x3 conv, batch 64, 56x56, 64->64)
-the activation gradient is the implicit-GEMM convolution (dact [T, C]);
-`--workload resnet_lowered` runs the GEMM on the lowered layout instead
-(dcol [T, 9C], which a col2im would still have to fold).
+both gradients are implicit-GEMM convolutions on the codes (dact [T, C],
+dW [Cout, 9C]); `--workload resnet_lowered` lowers the activation codes by
+im2col and runs both as GEMMs on the lowered layout instead (dcol [T, 9C],
+which a col2im would still have to fold).
 `--workload mlp_smp` is the MLP layer with two SMP samples stored as int8
 sums (the bytes of two 4-bit planes); `mlp_smp_planes` keeps two planes.
 
@@ -75,11 +76,14 @@ class Stage:
         return "hbm" if self.bytes / HBM_PEAK >= self.ops / I8_PEAK else "mfma"
 
 
-def build_resnet(L, torch, dev, lowered_dx=False):
-    """The 3x3 conv layer's backward.  The activation gradient comes from the
-    implicit-GEMM convolution kernel (dact [T, C], M = T, K = 9 * Cout, N = C),
-    or with lowered_dx from the GEMM on the lowered layout (dcol [T, 9 * C],
-    M = T, K = Cout, N = 9 * C; a col2im would still have to fold it)."""
+def build_resnet(L, torch, dev, lowered=False):
+    """The 3x3 conv layer's backward.  By default both gradients come from the
+    implicit-GEMM convolution kernels: dact [T, C] (M = T, K = 9 * Cout,
+    N = C) and dW [Cout, 9C] (M = Cout, N = 9C, K = T) read the codes of g and
+    of the activations directly.  With lowered, the activation codes are
+    lowered by im2col (58 MB of column codes) and both gradients are GEMMs on
+    the lowered layout: dcol [T, 9C] (which a col2im would still have to
+    fold) and dW."""
     import synth
     p = synth.RESNET
     B, H, W, C, Co = p["B"], p["H"], p["W"], p["C"], p["Cout"]
@@ -91,50 +95,61 @@ def build_resnet(L, torch, dev, lowered_dx=False):
     u8 = lambda n: torch.empty(int(n), dtype=torch.uint8, device=dev)
     f32 = lambda *s: torch.empty(*s, dtype=torch.float32, device=dev)
     gc, gct, alpha, gmax = u8(L.plane_bytes(T * Co)), u8(L.plane_bytes(T * Co)), f32(1), f32(1)
-    ac, sa = u8(T * C // 2), f32(1)
-    colt = u8(Ki * T // 2)
+    ac, sa = u8(T * C // 2), f32(1)                                   # row-major (lowered) or transposed codes
     wct, sw = u8(Co * Ki // 2), f32(1)
-    dx = f32(T, Ki) if lowered_dx else None
-    dact = None if lowered_dx else f32(T, C)
     dw = f32(Co, Ki)
     wsq = u8(L.workspace_size(L.OP_QUANTIZE_GRAD, T * Co))
     wsa = u8(L.workspace_size(L.OP_INT4_QUANTIZE, T * C))
     wsw = u8(L.workspace_size(L.OP_INT4_QUANTIZE, Co * Ki))
-    wsd = u8(max(L.workspace_size(L.OP_GEMM_DGRAD, T, Ki, Co), 1))
-    wsg = u8(max(L.workspace_size(L.OP_GEMM_WGRAD, T, Co, Ki), 1))
     n_g, n_a, n_w = T * Co, T * C, Co * Ki
+    dv = dict(g=g, act=act, w=w, gc=gc, gct=gct, alpha=alpha, gmax=gmax, ac=ac, sa=sa, wct=wct, sw=sw, dw=dw)
     stages = [
         Stage("luq_quantize_grad", lambda: L.luq_quantize_grad(g, 4, 0, 0, 1, gc, gct, alpha, gmax, wsq),
               2 * 4 * n_g + 2 * n_g / 2),
-        Stage("int4_quantize(act)", lambda: L.int4_quantize(act, False, 0.0, ac, False, sa, wsa),
-              2 * 4 * n_a + n_a / 2),
-        Stage("int4_im2col3x3_t", lambda: L.int4_im2col3x3_t(ac, B, H, W, C, colt), n_a / 2 + Ki * T / 2),
-        Stage("int4_quantize(W)", lambda: L.int4_quantize(w, True, 0.0, False, wct, sw, wsw),
-              2 * 4 * n_w + n_w / 2),
-        # dW right after im2col, while its 58 MB of column codes may still be in
-        # the last-level cache; the dX GEMM's 462 MB of output would evict them
-        Stage("luq_gemm_wgrad", lambda: L.luq_gemm_wgrad(gct, alpha, colt, sa, False, T, Co, Ki, 1, dw, wsg),
-              Co * T / 2 + Ki * T / 2 + 4 * Co * Ki, 2.0 * T * Ki * Co),
     ]
-    if lowered_dx:
-        stages.append(Stage("luq_gemm_dgrad", lambda: L.luq_gemm_dgrad(gc, alpha, wct, sw, True, T, Ki, Co, 1, dx, wsd),
-                            T * Co / 2 + Ki * Co / 2 + 4 * T * Ki, 2.0 * T * Ki * Co))
+    if lowered:
+        colt = u8(Ki * T // 2)
+        dx = f32(T, Ki)
+        wsd = u8(max(L.workspace_size(L.OP_GEMM_DGRAD, T, Ki, Co), 1))
+        wsg = u8(max(L.workspace_size(L.OP_GEMM_WGRAD, T, Co, Ki), 1))
+        dv.update(colt=colt, dx=dx)
+        stages += [
+            Stage("int4_quantize(act)", lambda: L.int4_quantize(act, False, 0.0, ac, False, sa, wsa),
+                  2 * 4 * n_a + n_a / 2),
+            Stage("int4_im2col3x3_t", lambda: L.int4_im2col3x3_t(ac, B, H, W, C, colt), n_a / 2 + Ki * T / 2),
+            Stage("int4_quantize(W)", lambda: L.int4_quantize(w, True, 0.0, False, wct, sw, wsw),
+                  2 * 4 * n_w + n_w / 2),
+            # dW right after im2col, while its 58 MB of column codes may still be
+            # in the last-level cache; the dX GEMM's 462 MB of output would evict them
+            Stage("luq_gemm_wgrad", lambda: L.luq_gemm_wgrad(gct, alpha, colt, sa, False, T, Co, Ki, 1, dw, wsg),
+                  Co * T / 2 + Ki * T / 2 + 4 * Co * Ki, 2.0 * T * Ki * Co),
+            Stage("luq_gemm_dgrad", lambda: L.luq_gemm_dgrad(gc, alpha, wct, sw, True, T, Ki, Co, 1, dx, wsd),
+                  T * Co / 2 + Ki * Co / 2 + 4 * T * Ki, 2.0 * T * Ki * Co),
+        ]
     else:
-        # g codes, W codes and dact once each
-        stages.append(Stage("luq_conv3x3_dgrad",
-                            lambda: L.luq_conv3x3_dgrad(gc, alpha, wct, sw, True, B, H, W, C, Co, 1, dact),
-                            T * Co / 2 + Ki * Co / 2 + 4 * T * C, 2.0 * T * C * Ki))
-    d["dev"] = dict(g=g, act=act, w=w, gc=gc, gct=gct, alpha=alpha, gmax=gmax, ac=ac, sa=sa, colt=colt,
-                    wct=wct, sw=sw, dw=dw)
-    if lowered_dx:
-        d["dev"]["dx"] = dx
-    else:
-        d["dev"]["dact"] = dact
-    cfg = {"workload": "resnet50_conv3x3_bwd_lowered_dx" if lowered_dx else "resnet50_conv3x3_bwd",
+        dact = f32(T, C)
+        wsc = u8(max(L.workspace_size(L.OP_CONV_WGRAD, T, C, Co), 1))
+        dv.update(dact=dact)
+        stages += [
+            Stage("int4_quantize(act)", lambda: L.int4_quantize(act, False, 0.0, False, ac, sa, wsa),
+                  2 * 4 * n_a + n_a / 2),
+            Stage("int4_quantize(W)", lambda: L.int4_quantize(w, True, 0.0, False, wct, sw, wsw),
+                  2 * 4 * n_w + n_w / 2),
+            # g^T and activation codes once each
+            Stage("luq_conv3x3_wgrad",
+                  lambda: L.luq_conv3x3_wgrad(gct, alpha, ac, sa, False, B, H, W, C, Co, 1, dw, wsc),
+                  Co * T / 2 + C * T / 2 + 4 * Co * Ki, 2.0 * T * Ki * Co),
+            # g codes, W codes and dact once each
+            Stage("luq_conv3x3_dgrad",
+                  lambda: L.luq_conv3x3_dgrad(gc, alpha, wct, sw, True, B, H, W, C, Co, 1, dact),
+                  T * Co / 2 + Ki * Co / 2 + 4 * T * C, 2.0 * T * C * Ki),
+        ]
+    d["dev"] = dv
+    cfg = {"workload": "resnet50_conv3x3_bwd_lowered" if lowered else "resnet50_conv3x3_bwd",
            "batch": B, "hw": [H, W], "cin": C, "cout": Co,
-           "dx": ("GEMM on the lowered layout, dcol [T, 9C]" if lowered_dx else
-                  "implicit-GEMM convolution, dact [T, C]"),
-           "gemm_dgrad_MNK": [T, Ki, Co] if lowered_dx else [T, C, Ki], "gemm_wgrad_MNK": [Co, Ki, T],
+           "gradients": ("GEMMs on the im2col lowering: dcol [T, 9C] and dW" if lowered else
+                         "implicit-GEMM convolution: dact [T, C] and dW [Cout, 9C]"),
+           "gemm_dgrad_MNK": [T, Ki, Co] if lowered else [T, C, Ki], "gemm_wgrad_MNK": [Co, Ki, T],
            "grad": "lognormal(-12,2.5) fp32, 50% zeros", "R": 4, "n_samples": 1}
     return stages, cfg, d
 
@@ -387,18 +402,21 @@ def cpu_baseline(workload, d):
 
             timed("luq", luq, 2 * 4 * n_g + 2 * n_g / 2)
             timed("int4(act)", act, 2 * 4 * n_a + n_a / 2)
-            timed("im2col", col, n_a / 2 + K9 * T / 2)
             timed("int4(W)", wq, 2 * 4 * n_w + n_w / 2)
             gc, ga, _ = out["g"]
             if workload == "resnet_lowered":
+                timed("im2col", col, n_a / 2 + K9 * T / 2)
+                timed("dW", lambda: ogemm.gemm_wgrad_ref(gc, ga, out["col"], out["a"][1], False, T, Co, K9),
+                      Co * T / 2 + K9 * T / 2 + 4 * Co * K9, 2.0 * T * K9 * Co)
                 timed("dX", lambda: ogemm.gemm_dgrad_ref(gc, ga, out["w"][0], out["w"][1], True, T, K9, Co),
                       T * Co / 2 + K9 * Co / 2 + 4 * T * K9, 2.0 * T * K9 * Co)
             else:
+                timed("dW", lambda: oconv.conv3x3_wgrad_ref(gc, ga, out["a"][0], out["a"][1], False,
+                                                            B, H, W, C, Co),
+                      Co * T / 2 + C * T / 2 + 4 * Co * K9, 2.0 * T * K9 * Co)
                 timed("dact", lambda: oconv.conv3x3_dgrad_ref(gc, ga, out["w"][0], out["w"][1], True,
                                                               B, H, W, C, Co),
                       T * Co / 2 + K9 * Co / 2 + 4 * T * C, 2.0 * T * K9 * Co)
-            timed("dW", lambda: ogemm.gemm_wgrad_ref(gc, ga, out["col"], out["a"][1], False, T, Co, K9),
-                  Co * T / 2 + K9 * T / 2 + 4 * Co * K9, 2.0 * T * K9 * Co)
             reps += 1
         sample = f"the whole step, {reps} times (last: " + ", ".join(parts) + ")"
         parts.clear()
@@ -451,7 +469,7 @@ def cpu_baseline(workload, d):
 
 PROFILES = os.path.join(ROOT, "profiles")
 KERNEL_SOURCES = {"luq_gemm_dgrad": "gemm_kernel.hpp", "luq_gemm_wgrad": "gemm_kernel.hpp",
-                  "luq_conv3x3_dgrad": "conv.hip",
+                  "luq_conv3x3_dgrad": "conv.hip", "luq_conv3x3_wgrad": "conv.hip",
                   "int4_gemm_fwd": "gemm_kernel.hpp",
                   "luq_quantize_grad": "quant.hip", "int4_im2col3x3_t": "im2col.hip"}
 
@@ -508,7 +526,7 @@ def main():
         print(json.dumps(out), flush=True)
         return
     if args.workload in ("resnet", "resnet_lowered"):
-        stages, cfg, d = build_resnet(L, torch, dev, lowered_dx=args.workload == "resnet_lowered")
+        stages, cfg, d = build_resnet(L, torch, dev, lowered=args.workload == "resnet_lowered")
     elif args.workload == "mlp_fwd":
         stages, cfg, d = build_mlp_fwd(L, torch, dev)
     elif args.workload == "small":

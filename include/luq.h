@@ -47,7 +47,7 @@
 extern "C" {
 #endif
 
-#define LUQ_ABI_VERSION 5
+#define LUQ_ABI_VERSION 6
 
 typedef int luq_status;
 enum {
@@ -83,7 +83,8 @@ enum {
   LUQ_OP_INT4_QUANTIZE = 1, /* d0 = number of elements                     */
   LUQ_OP_GEMM_DGRAD = 2,    /* d0 = M, d1 = N, d2 = K                        */
   LUQ_OP_GEMM_WGRAD = 3,    /* d0 = T, d1 = Nout, d2 = Kin                   */
-  LUQ_OP_GEMM_FWD = 4       /* d0 = M, d1 = N, d2 = K                        */
+  LUQ_OP_GEMM_FWD = 4,      /* d0 = M, d1 = N, d2 = K                        */
+  LUQ_OP_CONV_WGRAD = 5     /* d0 = B*H*W, d1 = C, d2 = Cout                 */
 };
 
 /* ABI version of the loaded library (LUQ_ABI_VERSION of its build). */
@@ -321,6 +322,39 @@ luq_status int4_im2col3x3_t(const uint8_t* act_codes, int64_t B, int64_t H, int6
 luq_status luq_conv3x3_dgrad(const uint8_t* g_codes, const float* alpha, int n_samples,
                              const uint8_t* w_codes_t, const float* w_scale, int w_signed, int64_t B,
                              int64_t H, int64_t W, int64_t C, int64_t Cout, float* dact, void* stream);
+
+/*
+ * luq_conv3x3_wgrad -- weight gradient of a 3x3 / stride 1 / zero-pad 1
+ * convolution on codes: Eq. update applied to the lowered convolution,
+ * without forming the lowered [T][9*C] activations:
+ *   dw[o][(kh*3 + kw)*C + c] = (alpha / n_samples) * a_scale *
+ *                              sum_t (sum_s cg_s[t][o]) * ca[t'][c]
+ * for t = (b*H + y)*W + x and t' = (b*H + y + kh - 1)*W + x + kw - 1, terms
+ * whose t' lies off the image left out.  Equal to luq_gemm_wgrad on the
+ * int4_im2col3x3_t lowering of the activation codes.  Every MAC is on codes
+ * with exact int32 partial sums over pixel ranges, combined exactly in a
+ * fixed order; the scales are applied once in fp32 (Appendix A.1).
+ *
+ *  g_codes_t  n_samples planes of [Cout][T] LUQ codes of the output gradient
+ *             (the codes_t output of luq_quantize_grad on g [T][Cout]; plane
+ *             stride luq_plane_bytes(T*Cout)).
+ *  alpha      1 float (device), the LUQ alpha of g.
+ *  a_codes_t  [C][T] INT4 codes of the activations (NHWC pixels t; the
+ *             codes_t output of int4_quantize on act [T][C]); a_scale 1 float
+ *             (device); a_signed 0/1.
+ *  B, H, W >= 0 with T = B*H*W a positive multiple of 32 and W <= 256;
+ *             C, Cout >= 1; each code operand below 1 GiB.  n_samples 1 or 2
+ *             (sample planes).
+ *  dw         out: [Cout][9*C] fp32, columns in (kh, kw, c) order.
+ *  ws         workspace of luq_workspace_size(LUQ_OP_CONV_WGRAD, T, C, Cout).
+ *  Errors: LUQ_ERR_SHAPE, LUQ_ERR_PARAM, LUQ_ERR_NULL, LUQ_ERR_WORKSPACE,
+ *  LUQ_ERR_ALIGN (code operands and ws 16-byte aligned, dw and scales 4-byte),
+ *  LUQ_ERR_HIP; nothing is enqueued on error.
+ */
+luq_status luq_conv3x3_wgrad(const uint8_t* g_codes_t, const float* alpha, int n_samples,
+                             const uint8_t* a_codes_t, const float* a_scale, int a_signed, int64_t B,
+                             int64_t H, int64_t W, int64_t C, int64_t Cout, float* dw, void* ws,
+                             size_t ws_bytes, void* stream);
 
 #ifdef __cplusplus
 }

@@ -20,12 +20,13 @@ LUQ_OK = 0
 LUQ_F32, LUQ_BF16 = 0, 1
 ALPHA_PW2 = 0x100  # or-ed into R: power-of-two alpha
 SMP_SUM = 0x10     # or-ed into n_samples = 2: the two samples as int8 sums
-OP_QUANTIZE_GRAD, OP_INT4_QUANTIZE, OP_GEMM_DGRAD, OP_GEMM_WGRAD, OP_GEMM_FWD = 0, 1, 2, 3, 4
+OP_QUANTIZE_GRAD, OP_INT4_QUANTIZE, OP_GEMM_DGRAD, OP_GEMM_WGRAD, OP_GEMM_FWD, OP_CONV_WGRAD = 0, 1, 2, 3, 4, 5
 
 EXPORTS = (
     "luq_abi_version", "luq_status_string", "luq_last_error", "luq_plane_bytes",
     "luq_workspace_size", "luq_quantize_grad", "luq_quantize_grad_hindsight", "int4_quantize",
     "luq_gemm_dgrad", "luq_gemm_wgrad", "int4_gemm_fwd", "int4_im2col3x3_t", "luq_conv3x3_dgrad",
+    "luq_conv3x3_wgrad",
 )
 
 
@@ -66,6 +67,8 @@ def _load():
     lib.int4_im2col3x3_t.argtypes = [vp, i64, i64, i64, i64, vp, vp]
     lib.luq_conv3x3_dgrad.restype = i32
     lib.luq_conv3x3_dgrad.argtypes = [vp, vp, i32, vp, vp, i32, i64, i64, i64, i64, i64, vp, vp]
+    lib.luq_conv3x3_wgrad.restype = i32
+    lib.luq_conv3x3_wgrad.argtypes = [vp, vp, i32, vp, vp, i32, i64, i64, i64, i64, i64, vp, vp, sz, vp]
     return lib
 
 
@@ -261,3 +264,18 @@ def luq_conv3x3_dgrad(g_codes, alpha, w_codes_t, w_scale, w_signed, B, H, W, C, 
                                1 if w_signed else 0, B, H, W, C, Cout, _ptr(dact), _stream(dev))
     _check(st, "luq_conv3x3_dgrad")
     return dact
+
+
+def luq_conv3x3_wgrad(g_codes_t, alpha, a_codes_t, a_scale, a_signed, B, H, W, C, Cout, n_samples=1, dw=None,
+                      ws=None):
+    """Weight gradient [Cout, 9*C] of a 3x3 / stride 1 / pad 1 convolution from
+    transposed LUQ codes of g [Cout, B*H*W] and transposed activation codes
+    [C, B*H*W]."""
+    dev = g_codes_t.device
+    dw = torch.empty(Cout, 9 * C, dtype=torch.float32, device=dev) if dw is None else dw
+    wsb = workspace_size(OP_CONV_WGRAD, B * H * W, C, Cout)
+    ws = _bytes(wsb, dev) if ws is None else ws
+    st = LIB.luq_conv3x3_wgrad(_ptr(g_codes_t), _ptr(alpha), n_samples, _ptr(a_codes_t), _ptr(a_scale),
+                               1 if a_signed else 0, B, H, W, C, Cout, _ptr(dw), _ptr(ws), ws.numel(), _stream(dev))
+    _check(st, "luq_conv3x3_wgrad")
+    return dw

@@ -80,6 +80,11 @@ size_t luq_workspace_size(int op, int64_t d0, int64_t d1, int64_t d2) {
       return (d0 > 0 && d1 > 0 && d2 > 0) ? luq::gemm_workspace_bytes(d1, d2, d0, 1) : 0;
     case LUQ_OP_GEMM_FWD:
       return (d0 > 0 && d1 > 0 && d2 > 0) ? luq::gemm_fwd_workspace_bytes(d0, d1, d2) : 0;
+    case LUQ_OP_CONV_WGRAD:
+      return (d0 > 0 && d1 > 0 && d2 > 0 && d0 < ((int64_t)1 << 31) && d1 < ((int64_t)1 << 28) &&
+              d2 < ((int64_t)1 << 28))
+                 ? luq::conv3x3_wgrad_workspace_bytes(d0, d1, d2)
+                 : 0;
     default:
       return 0;
   }
@@ -295,6 +300,36 @@ luq_status luq_conv3x3_dgrad(const uint8_t* g_codes, const float* alpha, int n_s
     return fail(LUQ_ERR_ALIGN, "%s: code operands must be 16-byte aligned, dact and scales 4-byte", fn);
   return hip_status(luq::launch_conv3x3_dgrad(g_codes, (int64_t)luq::plane_bytes(T * Cout), n_samples, alpha,
                                               w_codes_t, w_scale, w_signed ? 1 : 0, B, H, W, C, Cout, dact,
+                                              static_cast<hipStream_t>(stream)));
+}
+
+luq_status luq_conv3x3_wgrad(const uint8_t* g_codes_t, const float* alpha, int n_samples,
+                             const uint8_t* a_codes_t, const float* a_scale, int a_signed, int64_t B,
+                             int64_t H, int64_t W, int64_t C, int64_t Cout, float* dw, void* ws,
+                             size_t ws_bytes, void* stream) {
+  const char* fn = "luq_conv3x3_wgrad";
+  g_last_error[0] = 0;
+  if (B < 0 || H < 0 || W < 0 || C < 1 || Cout < 1)
+    return fail(LUQ_ERR_SHAPE, "%s: need B, H, W >= 0 and C, Cout >= 1", fn);
+  if (n_samples != 1 && n_samples != 2)
+    return fail(LUQ_ERR_PARAM, "%s: n_samples must be 1 or 2 (sample planes)", fn);
+  if (B > INT32_MAX || H > INT32_MAX || W > INT32_MAX || C > INT32_MAX / 9 || Cout > INT32_MAX ||
+      mul_overflows(B, H) || mul_overflows(B * H, W) || mul_overflows(B * H * W, Cout) ||
+      mul_overflows(B * H * W, C) || mul_overflows(9 * C, Cout))
+    return fail(LUQ_ERR_SHAPE, "%s: size overflows", fn);
+  if (W > luq::conv3x3_max_width()) return fail(LUQ_ERR_SHAPE, "%s: image width above 256", fn);
+  const int64_t T = B * H * W;
+  if (T < 32 || (T & 31)) return fail(LUQ_ERR_SHAPE, "%s: B*H*W must be a positive multiple of 32", fn);
+  if (Cout * (T / 2) >= ((int64_t)1 << 30) || C * (T / 2) >= ((int64_t)1 << 30))
+    return fail(LUQ_ERR_SHAPE, "%s: operand above 1 GiB of codes", fn);
+  if (!g_codes_t || !alpha || !a_codes_t || !a_scale || !dw) return fail(LUQ_ERR_NULL, "%s: NULL operand", fn);
+  const size_t need = luq::conv3x3_wgrad_workspace_bytes(T, C, Cout);
+  if (need && (!ws || ws_bytes < need)) return fail(LUQ_ERR_WORKSPACE, "%s: workspace too small", fn);
+  if (!aligned16(g_codes_t) || !aligned16(a_codes_t) || !aligned16(ws) || !aligned4(dw) || !aligned4(alpha) ||
+      !aligned4(a_scale))
+    return fail(LUQ_ERR_ALIGN, "%s: code operands and ws must be 16-byte aligned, dw and scales 4-byte", fn);
+  return hip_status(luq::launch_conv3x3_wgrad(g_codes_t, (int64_t)luq::plane_bytes(T * Cout), n_samples, alpha,
+                                              a_codes_t, a_scale, a_signed ? 1 : 0, B, H, W, C, Cout, dw, ws,
                                               static_cast<hipStream_t>(stream)));
 }
 

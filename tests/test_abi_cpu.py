@@ -32,7 +32,7 @@ def _declared():
 
 def test_every_declared_function_is_exported():
     names = _declared()
-    assert len(names) == 13, names
+    assert len(names) == 14, names
     for n in names:
         assert hasattr(LIB, n), n
     assert set(names) == set(luq.EXPORTS)
@@ -226,3 +226,28 @@ def test_smp_sum_sample_counts():
     # an int8 operand of 2^31 bytes: M * K reaches the 32-bit offset limit
     assert _dg(ns=SUM2, M=1 << 17, K=1 << 14) == 2
     assert _cv(ns=SUM2) == 4
+
+
+def _cw(**kw):
+    a = dict(g=P, alpha=P3, ns=1, a=P2, as_=P3, asig=0, B=2, H=8, W=8, C=64, Co=64, dw=P, ws=P, wsb=WS << 6)
+    a.update(kw)
+    return LIB.luq_conv3x3_wgrad(a["g"], a["alpha"], a["ns"], a["a"], a["as_"], a["asig"], a["B"], a["H"], a["W"],
+                                 a["C"], a["Co"], a["dw"], a["ws"], a["wsb"], None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(g=NUL), 1), (dict(alpha=NUL), 1), (dict(a=NUL), 1), (dict(as_=NUL), 1), (dict(dw=NUL), 1),
+    (dict(ns=0), 4), (dict(ns=0x12), 4),
+    (dict(B=-1), 2), (dict(C=0), 2), (dict(Co=0), 2), (dict(B=0), 2), (dict(H=3, W=3), 2),
+    (dict(B=1 << 14, H=256, W=256), 2), (dict(B=1, H=32, W=257), 2),
+    (dict(g=PMIS), 6), (dict(a=PMIS), 6), (dict(dw=ctypes.c_void_p(0x10002)), 6),
+    (dict(B=64, H=56, W=56, ws=NUL), 5), (dict(B=64, H=56, W=56, wsb=1024), 5),
+    (dict(B=64, H=56, W=56, ws=PMIS), 6),
+])
+def test_conv_wgrad_validation(kw, status):
+    assert _cw(**kw) == status
+
+
+def test_conv_wgrad_workspace():
+    assert luq.workspace_size(luq.OP_CONV_WGRAD, 64 * 56 * 56, 64, 64) > 0
+    assert luq.workspace_size(luq.OP_CONV_WGRAD, 0, 64, 64) == 0

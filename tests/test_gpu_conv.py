@@ -140,3 +140,101 @@ def test_conv_dgrad_resnet_layer_whole_output(L):
     assert_gemm_close(dact, ref, absref, "resnet dact")
     acc = _int_sums(rc[0], wc, True, B, H, W, C, Co)
     assert np.array_equal(dact, epilogue_replica(acc, ra, 1, wsr)), "resnet dact epilogue not bit-exact"
+
+
+# ----------------------------- weight gradient -----------------------------
+
+from oracle.conv import conv3x3_wgrad_ref  # noqa: E402
+
+
+def _wgrad_case(L, B, H, W, C, Cout, ns=1, asig=False, seed=0):
+    T = B * H * W
+    g = synth.lognormal_grad((T, Cout), -12.0, 2.5, 0.5, [seed, 1])
+    a = synth.normal((T, C), 1.0, [seed, 2]) if asig else synth.half_normal((T, C), [seed, 2])
+    announce("conv3x3_wgrad", dict(B=B, H=H, W=W, C=C, Cout=Cout, ns=ns, asig=asig, seed=seed))
+    gd, ad = to_dev(g), to_dev(a)
+    if T % 8 == 0 and Cout % 8 == 0 and C % 8 == 0:
+        _, gct, alpha, _ = L.luq_quantize_grad(gd, R=4, seed=seed, counter=6, n_samples=ns, codes=False, codes_t=True)
+        _, act, sa = L.int4_quantize(ad, is_signed=asig, codes=False, codes_t=True)
+    else:  # row-major codes transposed on the host (the quantizers' codes_t needs multiples of 8)
+        gc, _, alpha, _ = L.luq_quantize_grad(gd, R=4, seed=seed, counter=6, n_samples=ns)
+        gch = host(gc)
+        gct = to_dev(np.stack([transpose_codes(gch[s], T, Cout) for s in range(ns)]).reshape(ns, -1))
+        ac, _, sa = L.int4_quantize(ad, is_signed=asig)
+        act = to_dev(transpose_codes(host(ac), T, C))
+    if ns == 2 and gct.dim() == 2 and gct.shape[1] != L.plane_bytes(T * Cout):
+        pad = torch.zeros(2, L.plane_bytes(T * Cout), dtype=torch.uint8, device=gct.device)
+        pad[:, : gct.shape[1]] = gct
+        gct = pad
+    dw = host(L.luq_conv3x3_wgrad(gct, alpha, act, sa, asig, B, H, W, C, Cout, n_samples=ns))
+    assert dw.shape == (Cout, 9 * C)
+    rc, ra, _ = oluq.luq_quantize(g, R=4, seed=seed, counter=6, n_samples=ns)
+    rac, rsa = oint4.int4_quantize(a, is_signed=asig)
+    assert host(alpha)[0].tobytes() == np.float32(ra).tobytes()
+    assert host(sa)[0].tobytes() == np.float32(rsa).tobytes()
+    planes = rc if ns > 1 else rc[0]
+    ref, absref = conv3x3_wgrad_ref(planes, ra, rac, rsa, asig, B, H, W, C, Cout)
+    assert_gemm_close(dw, ref, absref, f"conv dW {B}x{H}x{W}x{C}->{Cout}")
+    s1, _ = conv3x3_wgrad_ref(planes, np.float32(1), rac, np.float32(1), asig, B, H, W, C, Cout)
+    acc = np.rint(s1 * ns).astype(np.int64)
+    assert np.array_equal(dw, epilogue_replica(acc, ra, ns, rsa)), "conv dW epilogue not bit-exact"
+    return dw
+
+
+@pytest.mark.parametrize("B,H,W,C,Cout", [
+    (1, 4, 8, 64, 64),        # one stage, one split
+    (4, 14, 16, 64, 64),      # 896 pixels, several stages, one split
+    (2, 5, 16, 6, 32),        # C not a multiple of 4 (scalar stores), partial channel tiles
+    (3, 9, 32, 96, 96),       # two channel tiles of each, partial second tiles
+    (2, 8, 8, 128, 256),      # several output tiles
+    (1, 2, 96, 8, 64),        # height 2: every row an image border
+    (4, 1, 64, 16, 64),       # height 1
+    (32, 32, 1, 16, 64),      # width 1
+    (2, 3, 160, 8, 40),       # width above the 64-pixel window margin
+    (16, 28, 28, 64, 64),     # several splits (split-K)
+])
+@pytest.mark.parametrize("ns", [1, 2])
+def test_conv_wgrad_parity(L, B, H, W, C, Cout, ns):
+    _wgrad_case(L, B, H, W, C, Cout, ns=ns, seed=B * 1000 + H * 100 + W + C + Cout)
+
+
+def test_conv_wgrad_signed_activations(L):
+    _wgrad_case(L, 2, 12, 12, 64, 64, asig=True, seed=31)
+
+
+def test_conv_wgrad_equals_lowered_gemm(L):
+    """The implicit weight gradient equals luq_gemm_wgrad on the im2col lowering, bit for bit."""
+    B, H, W, C, Co = 8, 14, 14, 64, 64
+    T = B * H * W
+    g = synth.lognormal_grad((T, Co), -12.0, 2.5, 0.5, [33, 1])
+    a = synth.half_normal((T, C), [33, 2])
+    announce("conv wgrad vs lowered")
+    _, gct, alpha, _ = L.luq_quantize_grad(to_dev(g), R=4, seed=1, counter=1, codes=False, codes_t=True)
+    ac, act, sa = L.int4_quantize(to_dev(a), is_signed=False, codes=True, codes_t=True)
+    colt = L.int4_im2col3x3_t(ac, B, H, W, C)
+    low = host(L.luq_gemm_wgrad(gct, alpha, colt, sa, False, T, Co, 9 * C))
+    imp = host(L.luq_conv3x3_wgrad(gct, alpha, act, sa, False, B, H, W, C, Co))
+    assert np.array_equal(low, imp)
+
+
+def test_conv_wgrad_resnet_layer_whole_output(L):
+    """The ResNet-50 layer (batch 64, 56 x 56, 64 -> 64) in the benchmark's
+    launch, the whole dW [64, 576] over 200704 pixels against the oracle."""
+    import bench
+    announce("conv3x3_wgrad full ResNet layer")
+    stages, _, d = bench.build_resnet(L, torch, torch.device("cuda:0"))
+    for s in stages:
+        if s.name in ("luq_quantize_grad", "int4_quantize(act)", "luq_conv3x3_wgrad"):
+            announce("stage", s.name)
+            s.fn()
+    torch.cuda.synchronize()
+    p = synth.RESNET
+    B, H, W, C, Co = p["B"], p["H"], p["W"], p["C"], p["Cout"]
+    dv = d["dev"]
+    dw = host(dv["dw"])
+    rc, ra, _ = oluq.luq_quantize(d["g"], R=4)
+    rac, rsa = oint4.int4_quantize(d["act"].reshape(-1, C), is_signed=False)
+    ref, absref = conv3x3_wgrad_ref(rc[0], ra, rac, rsa, False, B, H, W, C, Co)
+    assert_gemm_close(dw, ref, absref, "resnet dW")
+    s1, _ = conv3x3_wgrad_ref(rc[0], np.float32(1), rac, np.float32(1), False, B, H, W, C, Co)
+    assert np.array_equal(dw, epilogue_replica(np.rint(s1).astype(np.int64), ra, 1, rsa)), "resnet dW epilogue"

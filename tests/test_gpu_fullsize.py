@@ -66,7 +66,7 @@ def _sampled_ranges(n, count, length, seed):
 def conv(L):
     import bench
     announce("full-size conv workload: inputs and stages")
-    stages, _, d = bench.build_resnet(L, torch, DEV, lowered_dx=True)
+    stages, _, d = bench.build_resnet(L, torch, DEV, lowered=True)
     _run(stages, "conv")
     p = synth.RESNET
     d.update(B=p["B"], H=p["H"], Wd=p["W"], C=p["C"], Co=p["Cout"])
