@@ -342,7 +342,7 @@ luq_status luq_conv3x3_dgrad(const uint8_t* g_codes, const float* alpha, int n_s
  *  a_codes_t  [C][T] INT4 codes of the activations (NHWC pixels t; the
  *             codes_t output of int4_quantize on act [T][C]); a_scale 1 float
  *             (device); a_signed 0/1.
- *  B, H, W >= 0 with T = B*H*W a positive multiple of 32 and W <= 256;
+ *  B, H, W >= 0 with T = B*H*W a positive multiple of 32, at most 2^29;
  *             C, Cout >= 1; each code operand below 1 GiB.  n_samples 1 or 2
  *             (sample planes).
  *  dw         out: [Cout][9*C] fp32, columns in (kh, kw, c) order.

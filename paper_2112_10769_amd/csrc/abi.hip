@@ -317,11 +317,13 @@ luq_status luq_conv3x3_wgrad(const uint8_t* g_codes_t, const float* alpha, int n
       mul_overflows(B, H) || mul_overflows(B * H, W) || mul_overflows(B * H * W, Cout) ||
       mul_overflows(B * H * W, C) || mul_overflows(9 * C, Cout))
     return fail(LUQ_ERR_SHAPE, "%s: size overflows", fn);
-  if (W > luq::conv3x3_max_width()) return fail(LUQ_ERR_SHAPE, "%s: image width above 256", fn);
   const int64_t T = B * H * W;
   if (T < 32 || (T & 31)) return fail(LUQ_ERR_SHAPE, "%s: B*H*W must be a positive multiple of 32", fn);
+  if (T > ((int64_t)1 << 29) || W > ((int64_t)1 << 29)) return fail(LUQ_ERR_SHAPE, "%s: B*H*W above 2^29", fn);
   if (Cout * (T / 2) >= ((int64_t)1 << 30) || C * (T / 2) >= ((int64_t)1 << 30))
     return fail(LUQ_ERR_SHAPE, "%s: operand above 1 GiB of codes", fn);
+  if (luq::conv3x3_wgrad_blocks(T, C, Cout) > ((int64_t)1 << 22))
+    return fail(LUQ_ERR_SHAPE, "%s: too many channel tiles", fn);
   if (!g_codes_t || !alpha || !a_codes_t || !a_scale || !dw) return fail(LUQ_ERR_NULL, "%s: NULL operand", fn);
   const size_t need = luq::conv3x3_wgrad_workspace_bytes(T, C, Cout);
   if (need && (!ws || ws_bytes < need)) return fail(LUQ_ERR_WORKSPACE, "%s: workspace too small", fn);

@@ -283,53 +283,54 @@ hipError_t launch_conv3x3_dgrad(const uint8_t* g, int64_t g_plane, int ns, const
   return hipGetLastError();
 }
 
-
 // ---------------------------------------------------------------------------
 // Weight gradient of the same convolution, as an implicit GEMM (Eq. update
 // applied to the lowered convolution, without forming the lowered matrix):
 //
 //   dW[o][(kh*3 + kw)*C + c] = (alpha / ns) * s_a * sum_t (sum_s cg_s[t][o]) * ca[t'][c]
 //
-// with t' = (b, y + kh - 1, x + kw - 1) for t = (b, y, x), terms whose t' lies
-// off the image left out.  Operands are the transposed code layouts (pixels
-// innermost): g^T [Cout][T] and a^T [C][T].
+// with t' = t + (kh - 1)*W + kw - 1 in the flat pixel index for t = (b, y, x),
+// terms whose t' lies off the image left out.  Operands are the transposed
+// code layouts (pixels innermost): g^T [Cout][T] and a^T [C][T].
 //
-// A workgroup owns 64 output channels o, 64 input channels c and a range of
-// pixels t, for all nine taps (the reduction is split over pixel ranges; the
-// int32 chunk sums are combined by splitk_reduce_kernel).  Per stage of 128
-// pixels it expands into LDS, in element order (one int8 per pixel):
-//   - the gradient codes of its 64 output channels at those pixels, three
-//     times: for the taps kw = 0, 1, 2, the first and last with the pixels at
-//     x = 0 and x = W - 1 zeroed (a tap that leaves the image sideways lands,
-//     in the flat pixel index, on the neighbouring row, whose product must
-//     not count);
-//   - a window of the activation codes of its 64 input channels covering
-//     every pixel a tap reads: in the flat pixel index the tap (kh, kw) is the
-//     shift (kh - 1) * W + kw - 1, so the window spans 2W + 2 pixels more.
-// Twelve waves, one per kernel row kh, half of the input and half of the
-// output channels, multiply the three taps kw of their row: a tap's B
-// fragment is the window read at its shift (dword-aligned LDS reads and
-// v_alignbyte, the shift being wave-uniform); for kh = 0 and 2 the A
-// fragment is and-ed with the byte mask of y = 0 or y = H - 1 (mask tables
-// built once per workgroup for its pixels).  Operands are double-buffered in
-// LDS: the expansion of stage t+1 is cut into one piece per 32-deep k-step
-// and issued after that k-step's MFMAs of stage t, one barrier per stage.
+// With u = t + kw - 1 a term reads cg[u - kw + 1] and ca[u + (kh - 1)*W]: the
+// three taps of a kernel row share one activation operand.  The term is valid
+// iff y(u) + kh - 1 lies on the image and, for kw = 0, x(u) != W - 1, for
+// kw = 2, x(u) != 0 (the shift by one pixel then stays inside the row).  So a
+// workgroup owns one kernel row kh and a 64 x 64 block of (o, c), and per
+// stage of 128 pixels u expands into LDS:
+//   - three copies of the gradient codes of its 64 output channels, copy kw
+//     shifted by 1 - kw pixels and and-ed with the byte mask of the u valid
+//     for (kh, kw) (mask tables built once per pixel range);
+//   - the activation codes of its 64 input channels at the pixels
+//     u + (kh - 1)*W: a window of 160 pixels from the 32-pixel boundary below.
+// Each of four waves (two halves of o times two halves of c) builds one B
+// fragment per 32-deep k-step from the window (dword reads, and v_alignbyte
+// when the window's wave-uniform byte offset is not a multiple of 4) and
+// multiplies it with the three copies.  Two groups of four waves take the two
+// halves of the workgroup's pixel range, each with its own double-buffered
+// stages; their sums are added through LDS at the end.  The reduction over
+// pixel ranges is split over workgroups, and their int32 sums are combined
+// exactly, in a fixed order, by conv_wgrad_reduce_kernel.
+//
+// Bytes in LDS are in natural pixel order (the shifts need it).  Carriers are
+// those of the GEMMs: LUQ codes as their values (two samples as their int8
+// sum), unsigned INT4 as 8q, signed INT4 as 16q.
 // ---------------------------------------------------------------------------
 
-constexpr int kWgThreads = 768;
-constexpr int kWgBK = 128;                     // pixels per stage
-constexpr int kWgMaxChunk = 2048;              // pixels per split (mask table bytes)
-constexpr int kWgApitch = kWgBK + 16;          // A rows (bytes)
-constexpr int kWgAcopy = 64 * kWgApitch;       // one masked copy of the A stage
-
-template <int MAXW>
-struct WgLds {
-  // window pixels: a tap reads up to 145 + 2W bytes into it, 20 at a time
-  static constexpr int kWin = (165 + 2 * MAXW + 31) / 32 * 32;
-  static constexpr int kBpitch = kWin + 4;     // odd number of dwords per row
-  static constexpr int kWinChunks = 64 * (kWin / 32);
-  static constexpr int kStage = 3 * kWgAcopy + 64 * kBpitch;
-};
+constexpr int kWgKG = 2;                                   // wave groups (pixel halves)
+constexpr int kWgGroup = 256;                              // threads per wave group
+constexpr int kWgThreads = kWgKG * kWgGroup;
+constexpr int kWgBK = 128;                                 // pixels per stage
+constexpr int kWgGPitch = kWgBK + 16;                      // gradient copy row (bytes)
+constexpr int kWgGCopy = 64 * kWgGPitch;
+constexpr int kWgWin = kWgBK + 32;                         // activation window (pixels)
+constexpr int kWgBPitch = kWgWin + 4;                      // an odd number of dwords
+constexpr int kWgStage = 3 * kWgGCopy + 64 * kWgBPitch;
+constexpr int kWgMaxLg = 1280;                             // pixels per wave group and range
+constexpr int64_t kWgMaxWgPixels = (int64_t)1 << 19;       // pixels one workgroup sums in int32
+constexpr int kWgFar = 1 << 30;                            // a stage start past every image (T <= 2^29)
+static_assert(kWgKG * 2 * kWgStage + 3 * kWgKG * kWgMaxLg <= 160 * 1024, "LDS");
 
 struct ConvWgArgs {
   const uint8_t* g;      // LUQ codes [Cout][T], ns planes
@@ -338,56 +339,54 @@ struct ConvWgArgs {
   const float* alpha;
   const float* ascale;
   float* dw;             // [Cout][9C]
-  int32_t* partial;      // [splits][Cout][9C] chunk sums, or null
+  int32_t* partial;      // [nsplit][Cout][9C] sums of the splits, or null
   int T, H, W, C, Cout;
-  int kchunk;            // pixels per split, a multiple of kWgBK, <= kWgMaxChunk
-  int ctiles;            // ceil(C / 64)
+  int lg;                // pixels per wave group and range, a multiple of 2 * kWgBK
+  int nranges;           // ranges of kWgKG * lg pixels covering [0, T)
+  int nsplit;            // workgroups per (kh, tile); split s sums ranges s, s + nsplit, ...
+  int nblk;              // blocks per tile: 24 * ceil(nsplit / 8)
+  int ctiles;
   int vec;               // 16-byte stores of dW rows
 };
 
-// Element-order bytes from the even / odd split of the GEMM expansions:
-// e holds elements 0, 2, 4, 6 and o elements 1, 3, 5, 7.
-__device__ __forceinline__ void interleave_bytes(uint32_t e, uint32_t o, uint32_t& lo, uint32_t& hi) {
-  lo = __builtin_amdgcn_perm(o, e, 0x05010400u);
-  hi = __builtin_amdgcn_perm(o, e, 0x07030602u);
+// LUQ value bytes of four spread codes: 0 for field 0, else +-2^(field-1)
+__device__ __forceinline__ uint32_t luq_value_bytes(uint32_t s) {
+  const uint32_t m = __builtin_amdgcn_perm(0x40201008u, 0x04020100u, s & 0x07070707u);
+  const uint32_t q = ((s >> 3) & 0x01010101u) | 0x0C0C0C0Cu;  // perm selector 12 / 13: 0x00 / 0xFF
+  return (m ^ __builtin_amdgcn_perm(0u, 0u, q)) + (q & 0x01010101u);
 }
 
-template <int MAXW, int NS, bool ASIGNED>
+// excess-64 LUQ value bytes (64 + v) of four spread codes; the sum of two
+// samples' bytes, xor 0x80, is v0 + v1 in two's complement (R <= 5)
+__device__ __forceinline__ uint32_t luq_ex64_bytes(uint32_t s) {
+  const uint32_t p = __builtin_amdgcn_perm(0x80605048u, 0x44424140u, s & 0x07070707u);
+  const uint32_t sg = (s >> 3) & 0x01010101u;
+  return (p ^ ((sg << 7) - sg)) + sg;
+}
+
+template <int NS, bool ASIGNED>
 __global__ __launch_bounds__(kWgThreads, 1) void conv3x3_wgrad_kernel(ConvWgArgs a) {
-  using Lds = WgLds<MAXW>;
-  __shared__ __attribute__((aligned(16))) uint8_t lds[2 * Lds::kStage];
-  __shared__ __attribute__((aligned(16))) uint8_t vmask[4][kWgMaxChunk];  // 0xFF: y != 0, y != H-1, x != 0, x != W-1
+  __shared__ __attribute__((aligned(16))) uint8_t lds[kWgKG * 2 * kWgStage];
+  __shared__ __attribute__((aligned(16))) uint8_t vmask[3][kWgKG * kWgMaxLg];
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int ct = blockIdx.x % a.ctiles;
-  const int ot = blockIdx.x / a.ctiles;
+  // blocks are dealt round-robin over the 8 XCDs: block 24q + 8kh + x takes
+  // split 8q + x of row kh, so the three rows of a split share one XCD's L2
+  // (the same gradient codes, overlapping activation windows)
+  const int tile = blockIdx.x / a.nblk, bid = blockIdx.x - tile * a.nblk;
+  const int kh = (bid >> 3) % 3;
+  const int split = (bid / 24) * 8 + (bid & 7);
+  if (split >= a.nsplit) return;
+  const int ct = tile % a.ctiles, ot = tile / a.ctiles;
   const int o0 = ot * 64, c0 = ct * 64;
-  const int kb = blockIdx.y * a.kchunk;
-  const int ke = min(kb + a.kchunk, a.T);
-  const int nst = (ke - kb + kWgBK - 1) / kWgBK;
-  const int rowb = a.T >> 1;  // bytes per code row of either operand
-  // the smallest tap shift is -(W + 1); the window starts at the 32-pixel
-  // boundary at or below it
-  const int smin = -(a.W + 1);
-  const int wq = -(((-smin) + 31) >> 5) * 32;
-  const int wr = smin - wq;  // 0..31
 
-  for (int p = tid; p < nst * kWgBK; p += kWgThreads) {
-    const int t = kb + p;
-    uint32_t my0 = 0, my2 = 0, mx0 = 0, mx2 = 0;
-    if (t < ke) {
-      const int r = t / a.W, x = t - r * a.W;
-      const int y = r % a.H;
-      my0 = y != 0 ? 0xFFu : 0u;
-      my2 = y != a.H - 1 ? 0xFFu : 0u;
-      mx0 = x != 0 ? 0xFFu : 0u;
-      mx2 = x != a.W - 1 ? 0xFFu : 0u;
-    }
-    vmask[0][p] = (uint8_t)my0;
-    vmask[1][p] = (uint8_t)my2;
-    vmask[2][p] = (uint8_t)mx0;
-    vmask[3][p] = (uint8_t)mx2;
-  }
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int kg = tid / kWgGroup, lt = tid % kWgGroup, wv = lt >> 6;
+  const int oi = wv & 1, cj = wv >> 1;
+  const int rowb = a.T >> 1;                       // bytes per code row of either operand
+  const int shift = (kh - 1) * a.W;                // activation pixel of u: u + shift
+  const int r = ((shift % 32) + 32) % 32;          // window byte of pixel k0 + shift
+  const int nst = a.lg / kWgBK;
+  uint8_t* mybuf = lds + kg * 2 * kWgStage;
 
   __amdgpu_buffer_rsrc_t rsg[NS];
 #pragma unroll
@@ -396,209 +395,367 @@ __global__ __launch_bounds__(kWgThreads, 1) void conv3x3_wgrad_kernel(ConvWgArgs
   const __amdgpu_buffer_rsrc_t rsa =
       __builtin_amdgcn_make_buffer_rsrc((void*)a.a, (short)0, a.C * rowb, kBufferFlags);
 
-  // load slots: threads 0..255 one A chunk (row tid/4, 32 pixels tid%4);
-  // window chunks q = tid, tid + 768, ... (row q / (kWin/32), 32 pixels)
-  constexpr int WC = Lds::kWin / 32;
-  constexpr int BQ = (Lds::kWinChunks + kWgThreads - 1) / kWgThreads;
-  static_assert(BQ <= 3, "window chunks fit three expansion pieces");
-  const bool has_a = tid < 256;
-  const int arow = (tid & 255) >> 2, ajc = tid & 3;
-  const bool aok = has_a && o0 + arow < a.Cout;
+  // load slots: lane lt handles row lt/4 and chunk j = lt%4 of both operands:
+  // gradient pixels k0 + 32j .. +31 (and, for j = 0 / 3, the dword of the 8
+  // pixels before / after the stage), window pixels 32j .. 32j + 31; the
+  // 64 lanes of the group's first wave also take window chunk 4 of row lt.
+  // Few, wide loads: the address unit, not HBM, limits this loop.
+  const int lrow = lt >> 2, lj = lt & 3;
+  const bool gok = o0 + lrow < a.Cout;
+  const bool aok = c0 + lrow < a.C;
   struct Regs {
     v4u g[NS];
-    v4u b[BQ];
+    uint32_t ge[NS];
+    v4u b, b4;  // window chunk lj; chunk 4 (lanes of wave 0 of the group only)
   };
-  auto load = [&](Regs& r, int t) {
-    const int k0 = kb + t * kWgBK;
-    const int ka = k0 + ajc * 32;
-    const int offa = aok && ka < ke ? (o0 + arow) * rowb + (ka >> 1) : kOutOfRange;
+  // every step issues the same loads, without branches (a stage past the
+  // range is loaded from k0 = kWgFar, beyond every image, which reads
+  // nothing), so the compiler can wait for exactly the older stage's loads
+  // and keep the newer ones in flight
+  auto load = [&](Regs& R, int k0) {
+    const int pg = k0 + 32 * lj;
+    const int offg = gok && pg < a.T ? (o0 + lrow) * rowb + (pg >> 1) : kOutOfRange;
+    const int pe = lj == 0 ? k0 - 8 : k0 + kWgBK;
+    const bool eok = gok && (lj == 0 || lj == 3) && pe >= 0 && pe < a.T;
+    const int offe = eok ? (o0 + lrow) * rowb + (pe >> 1) : kOutOfRange;
 #pragma unroll
-    for (int s = 0; s < NS; ++s) r.g[s] = __builtin_amdgcn_raw_buffer_load_b128(rsg[s], offa, 0, 0);
-#pragma unroll
-    for (int u = 0; u < BQ; ++u) {
-      const int q = tid + u * kWgThreads;
-      const int row = q / WC, jc = q - (q / WC) * WC;
-      const int kw0 = k0 + wq + jc * 32;
-      const bool ok = q < Lds::kWinChunks && c0 + row < a.C && kw0 >= 0 && kw0 < a.T;
-      r.b[u] = __builtin_amdgcn_raw_buffer_load_b128(rsa, ok ? (c0 + row) * rowb + (kw0 >> 1) : kOutOfRange, 0, 0);
+    for (int s = 0; s < NS; ++s) {
+      R.g[s] = __builtin_amdgcn_raw_buffer_load_b128(rsg[s], offg, 0, 0);
+      R.ge[s] = __builtin_amdgcn_raw_buffer_load_b32(rsg[s], offe, 0, 0);
+    }
+    // window chunks of 32 pixels (all on or all off [0, T)): chunk lj of row
+    // lt/4 for every lane, chunk 4 of row lt for the 64 lanes of wave 0
+    const int wbase = k0 + shift - r;
+    const int pb = wbase + 32 * lj;
+    R.b = __builtin_amdgcn_raw_buffer_load_b128(
+        rsa, aok && pb >= 0 && pb < a.T ? (c0 + lrow) * rowb + (pb >> 1) : kOutOfRange, 0, 0);
+    if (wv == 0) {
+      const int p4 = wbase + 4 * 32;
+      R.b4 = __builtin_amdgcn_raw_buffer_load_b128(
+          rsa, c0 + lt < a.C && p4 >= 0 && p4 < a.T ? (c0 + lt) * rowb + (p4 >> 1) : kOutOfRange, 0, 0);
     }
   };
-  // expansion piece 0: the A chunk (three copies); pieces 1..BQ: window chunks
-  auto expand_piece = [&](const Regs& r, int t, uint8_t* stage, int piece) {
-    uint32_t w[8];
-    if (piece == 0) {
-      if (!has_a) return;
-#pragma unroll
-      for (int d = 0; d < 4; ++d) {
-        uint32_t e, o;
-        if constexpr (NS == 1) {
-          expand_luq(r.g[0][d], e, o);
-        } else {
-          uint32_t e0, o0_, e1, o1;
-          expand_luq_excess64(r.g[0][d], e0, o0_);
-          expand_luq_excess64(r.g[1][d], e1, o1);
-          e = (e0 + e1) ^ 0x80808080u;
-          o = (o0_ + o1) ^ 0x80808080u;
-        }
-        interleave_bytes(e, o, w[2 * d], w[2 * d + 1]);
-      }
-      const int mp = t * kWgBK + ajc * 32;
-      const uint4* m0 = reinterpret_cast<const uint4*>(&vmask[2][mp]);
-      const uint4* m2 = reinterpret_cast<const uint4*>(&vmask[3][mp]);
-      const uint4 a0 = m0[0], a1 = m0[1], b0 = m2[0], b1 = m2[1];
-      uint4* d0 = reinterpret_cast<uint4*>(stage + arow * kWgApitch + ajc * 32);
-      uint4* d1 = reinterpret_cast<uint4*>(stage + kWgAcopy + arow * kWgApitch + ajc * 32);
-      uint4* d2 = reinterpret_cast<uint4*>(stage + 2 * kWgAcopy + arow * kWgApitch + ajc * 32);
-      d0[0] = make_uint4(w[0] & a0.x, w[1] & a0.y, w[2] & a0.z, w[3] & a0.w);
-      d0[1] = make_uint4(w[4] & a1.x, w[5] & a1.y, w[6] & a1.z, w[7] & a1.w);
-      d1[0] = make_uint4(w[0], w[1], w[2], w[3]);
-      d1[1] = make_uint4(w[4], w[5], w[6], w[7]);
-      d2[0] = make_uint4(w[0] & b0.x, w[1] & b0.y, w[2] & b0.z, w[3] & b0.w);
-      d2[1] = make_uint4(w[4] & b1.x, w[5] & b1.y, w[6] & b1.z, w[7] & b1.w);
-      return;
-    }
-    const int u = piece - 1;
-    if (u >= BQ) return;
-    const int q = tid + u * kWgThreads;
-    if (q >= Lds::kWinChunks) return;
-    const int row = q / WC, jc = q - (q / WC) * WC;
+  // gradient chunk -> natural-order value bytes w, and the neighbouring pixel
+  // outside the stage (before: nibble 7 of the dword, after: nibble 0) in e
+  auto g_decode = [&](const Regs& R, uint32_t (&w)[8], uint32_t& e) {
 #pragma unroll
     for (int d = 0; d < 4; ++d) {
-      uint32_t e, o;
-      expand_int4<ASIGNED>(r.b[u][d], e, o);
-      interleave_bytes(e, o, w[2 * d], w[2 * d + 1]);
+      uint32_t l0, h0;
+      spread_nibbles(R.g[0][d], l0, h0);
+      if constexpr (NS == 1) {
+        w[2 * d] = luq_value_bytes(l0);
+        w[2 * d + 1] = luq_value_bytes(h0);
+      } else {
+        uint32_t l1, h1;
+        spread_nibbles(R.g[1][d], l1, h1);
+        w[2 * d] = (luq_ex64_bytes(l0) + luq_ex64_bytes(l1)) ^ 0x80808080u;
+        w[2 * d + 1] = (luq_ex64_bytes(h0) + luq_ex64_bytes(h1)) ^ 0x80808080u;
+      }
     }
-    uint32_t* db = reinterpret_cast<uint32_t*>(stage + 3 * kWgAcopy + row * Lds::kBpitch + jc * 32);
+    const uint32_t n0 = lj == 0 ? R.ge[0] >> 28 : R.ge[0] & 0xFu;
+    if constexpr (NS == 1) {
+      e = luq_value_bytes(n0);
+    } else {
+      const uint32_t n1 = lj == 0 ? R.ge[1] >> 28 : R.ge[1] & 0xFu;
+      e = (luq_ex64_bytes(n0) + luq_ex64_bytes(n1)) ^ 0x80808080u;  // zero above byte 0
+    }
+  };
+  // the three shifted, masked copies of a decoded chunk; tpos = the chunk's
+  // first pixel relative to the range (mask table index)
+  auto g_store = [&](const uint32_t (&w)[8], uint32_t e, uint8_t* stage, int tpos) {
+    // lanes 4*row + j hold the chunks j = 0..3 of a row: quad_perm (1,2,3,3)
+    // gives each lane its right neighbour's w[0], (0,0,1,2) its left one's w[7]
+    const uint32_t nx = (uint32_t)__builtin_amdgcn_mov_dpp((int)w[0], 0xF9, 0xF, 0xF, true);
+    const uint32_t pv = (uint32_t)__builtin_amdgcn_mov_dpp((int)w[7], 0x90, 0xF, 0xF, true);
+    const uint32_t next = lj == 3 ? e : nx;           // pixel 32j + 32 in byte 0
+    const uint32_t prev = lj == 0 ? (e << 24) : pv;   // pixel 32j - 1 in byte 3
+    uint32_t c0w[8], c2w[8];
 #pragma unroll
-    for (int k = 0; k < 8; ++k) db[k] = w[k];
+    for (int d = 0; d < 8; ++d) {
+      c0w[d] = __builtin_amdgcn_alignbyte(d < 7 ? w[d + 1] : next, w[d], 1u);  // u holds pixel u + 1
+      c2w[d] = __builtin_amdgcn_alignbyte(w[d], d > 0 ? w[d - 1] : prev, 3u);  // u holds pixel u - 1
+    }
+    const uint4* m0 = reinterpret_cast<const uint4*>(&vmask[0][tpos]);
+    const uint4* m1 = reinterpret_cast<const uint4*>(&vmask[1][tpos]);
+    const uint4* m2 = reinterpret_cast<const uint4*>(&vmask[2][tpos]);
+    uint8_t* base = stage + lrow * kWgGPitch + 32 * lj;
+#pragma unroll
+    for (int hlf = 0; hlf < 2; ++hlf) {
+      const uint4 k0m = m0[hlf], k1m = m1[hlf], k2m = m2[hlf];
+      const int d = 4 * hlf;
+      reinterpret_cast<uint4*>(base)[hlf] =
+          make_uint4(c0w[d] & k0m.x, c0w[d + 1] & k0m.y, c0w[d + 2] & k0m.z, c0w[d + 3] & k0m.w);
+      reinterpret_cast<uint4*>(base + kWgGCopy)[hlf] =
+          make_uint4(w[d] & k1m.x, w[d + 1] & k1m.y, w[d + 2] & k1m.z, w[d + 3] & k1m.w);
+      reinterpret_cast<uint4*>(base + 2 * kWgGCopy)[hlf] =
+          make_uint4(c2w[d] & k2m.x, c2w[d + 1] & k2m.y, c2w[d + 2] & k2m.z, c2w[d + 3] & k2m.w);
+    }
+  };
+  // the window piece: natural-order bytes 8q (unsigned) or 16q (signed)
+  auto b_chunk = [&](const v4u& x4, uint32_t* dst) {
+#pragma unroll
+    for (int d = 0; d < 4; ++d) {
+      const uint32_t x = x4[d];
+      if constexpr (ASIGNED) {
+        const uint32_t z = x << 4;
+        dst[2 * d] = __builtin_amdgcn_perm(x, z, 0x05010400u) & 0xF0F0F0F0u;
+        dst[2 * d + 1] = __builtin_amdgcn_perm(x, z, 0x07030602u) & 0xF0F0F0F0u;
+      } else {
+        const uint32_t y = x >> 4;
+        dst[2 * d] = (__builtin_amdgcn_perm(y, x, 0x05010400u) << 3) & 0x78787878u;
+        dst[2 * d + 1] = (__builtin_amdgcn_perm(y, x, 0x07030602u) << 3) & 0x78787878u;
+      }
+    }
+  };
+  auto b_store = [&](const Regs& R, uint8_t* stage) {
+    uint8_t* win = stage + 3 * kWgGCopy;
+    b_chunk(R.b, reinterpret_cast<uint32_t*>(win + lrow * kWgBPitch + 32 * lj));
+    if (wv == 0) b_chunk(R.b4, reinterpret_cast<uint32_t*>(win + lt * kWgBPitch + 4 * 32));
   };
 
-  // wave: kernel row kh, input channels cj*32 .. +31, output channels oi*32 .. +31
-  const int kh = wave >> 2, cj = (wave >> 1) & 1, oi = wave & 1;
+  // mask tables of the range [rbase, rbase + kWgKG * lg): 0xFF where u is on
+  // [0, T), y(u) + kh - 1 on the image and (copy 0) x(u) != W - 1, (copy 2)
+  // x(u) != 0
+  auto build_masks = [&](int rbase) {
+    const int n4 = kWgKG * a.lg / 4;
+    for (int i = tid; i < n4; i += kWgThreads) {
+      const int u0 = rbase + 4 * i;  // T is a multiple of 4: u0 .. u0 + 3 all on or all off
+      uint32_t m0 = 0, m1 = 0, m2 = 0;
+      if (u0 < a.T) {
+        const int row = u0 / a.W;
+        int x = u0 - row * a.W;
+        int y = row % a.H;
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+          const bool yv = kh == 0 ? y != 0 : (kh == 2 ? y != a.H - 1 : true);
+          if (yv) {
+            m1 |= 0xFFu << (8 * k);
+            if (x != a.W - 1) m0 |= 0xFFu << (8 * k);
+            if (x != 0) m2 |= 0xFFu << (8 * k);
+          }
+          if (++x == a.W) {
+            x = 0;
+            if (++y == a.H) y = 0;
+          }
+        }
+      }
+      reinterpret_cast<uint32_t*>(vmask[0])[i] = m0;
+      reinterpret_cast<uint32_t*>(vmask[1])[i] = m1;
+      reinterpret_cast<uint32_t*>(vmask[2])[i] = m2;
+    }
+  };
+
   const int r32 = lane & 31, h = lane >> 5;
-  const int sh = wr + kh * a.W;  // window offset of the tap (kh, 0)
-  const int aoff = (oi * 32 + r32) * kWgApitch;
-  const int boff = 3 * kWgAcopy + (cj * 32 + r32) * Lds::kBpitch;
+  const int aoff = (oi * 32 + r32) * kWgGPitch;
+  const int boff = 3 * kWgGCopy + (cj * 32 + r32) * kWgBPitch;
+  const uint32_t ra = (uint32_t)(r & 3);
   v16i acc[3];
 #pragma unroll
   for (int kw = 0; kw < 3; ++kw) acc[kw] = v16i{};
-  auto mfma_kstep = [&](const uint8_t* stage, int t, int kk) {
+  auto mfma_kstep = [&](const uint8_t* stage, int kk) {
     const int p = kk * 32 + 16 * h;
-    v4u ym = v4u{0xFFFFFFFFu, 0xFFFFFFFFu, 0xFFFFFFFFu, 0xFFFFFFFFu};
-    if (kh != 1) ym = *reinterpret_cast<const v4u*>(&vmask[kh >> 1][t * kWgBK + p]);
+    const int s = r + p;
+    const uint32_t* src = reinterpret_cast<const uint32_t*>(stage + boff + (s & ~3));
+    v4i fb;
+    if (ra == 0) {
 #pragma unroll
-    for (int kw = 0; kw < 3; ++kw) {
-      const v4u fa = *reinterpret_cast<const v4u*>(stage + kw * kWgAcopy + aoff + p) & ym;
-      const int s = p + sh + kw;
-      const uint32_t* src = reinterpret_cast<const uint32_t*>(stage + boff + (s & ~3));
+      for (int d = 0; d < 4; ++d) fb[d] = (int)src[d];
+    } else {
       uint32_t x[5];
 #pragma unroll
       for (int d = 0; d < 5; ++d) x[d] = src[d];
-      v4i fb;
 #pragma unroll
-      for (int d = 0; d < 4; ++d) fb[d] = (int)__builtin_amdgcn_alignbyte(x[d + 1], x[d], (uint32_t)(s & 3));
-      acc[kw] = __builtin_amdgcn_mfma_i32_32x32x32_i8(fb, (v4i)fa, acc[kw], 0, 0, 0);
+      for (int d = 0; d < 4; ++d) fb[d] = (int)__builtin_amdgcn_alignbyte(x[d + 1], x[d], ra);
     }
-  };
-  // one pipeline step: multiply stage t (buffer cb) while expanding stage t+1
-  // (registers r) into the other buffer, then refill r with stage t+3
-  auto step = [&](int cb, int t, Regs& r) {
-    uint8_t* cur = lds + cb * Lds::kStage;
-    uint8_t* nxt = lds + (cb ^ 1) * Lds::kStage;
-    const bool more = t + 1 < nst;
 #pragma unroll
-    for (int kk = 0; kk < kWgBK / 32; ++kk) {
-      mfma_kstep(cur, t, kk);
-      if (more) expand_piece(r, t + 1, nxt, kk);
+    for (int kw = 0; kw < 3; ++kw) {
+      const v4i fa = *reinterpret_cast<const v4i*>(stage + kw * kWgGCopy + aoff + p);
+      acc[kw] = __builtin_amdgcn_mfma_i32_32x32x32_i8(fb, fa, acc[kw], 0, 0, 0);
     }
-    if (t + 3 < nst) load(r, t + 3);
-    __syncthreads();
   };
 
-  __syncthreads();  // the mask tables are written
-  Regs r0, r1;
-  load(r0, 0);
-  if (1 < nst) load(r1, 1);
-#pragma unroll
-  for (int piece = 0; piece < 4; ++piece) expand_piece(r0, 0, lds, piece);
-  if (2 < nst) load(r0, 2);
-  __syncthreads();
-  for (int t = 0; t < nst; t += 2) {
-    step(0, t, r1);                     // multiply t, expand t+1 (r1), reload r1 with t+3
-    if (t + 1 < nst) step(1, t + 1, r0);  // multiply t+1, expand t+2 (r0), reload r0 with t+4
+  for (int rg = split; rg < a.nranges; rg += a.nsplit) {
+    const int rbase = rg * (kWgKG * a.lg);
+    const int gbase = rbase + kg * a.lg;
+    const int tbase = kg * a.lg;
+    build_masks(rbase);
+    __syncthreads();  // mask tables written
+    // one pipeline step: multiply stage t (buffer cb) while expanding stage
+    // t+1 (registers R) into the other buffer; R is refilled with stage t+3
+    // as soon as it is decoded.
+    // The last step expands an empty stage into the idle buffer: no branch,
+    // so the wait counts stay static.
+    auto step = [&](int cb, int t, Regs& R) {
+      uint8_t* cur = mybuf + cb * kWgStage;
+      uint8_t* nxt = mybuf + (cb ^ 1) * kWgStage;
+      const int tpos = (t + 1 < nst ? tbase + (t + 1) * kWgBK : 0) + 32 * lj;
+      uint32_t w[8], e;
+      mfma_kstep(cur, 0);
+      g_decode(R, w, e);
+      b_store(R, nxt);
+      load(R, t + 3 < nst ? gbase + (t + 3) * kWgBK : kWgFar);  // R is free: refill it early
+      mfma_kstep(cur, 1);
+      g_store(w, e, nxt, tpos);
+      mfma_kstep(cur, 2);
+      mfma_kstep(cur, 3);
+      __syncthreads();
+    };
+    Regs r0, r1;
+    load(r0, gbase);
+    load(r1, 1 < nst ? gbase + kWgBK : kWgFar);
+    {
+      uint32_t w[8], e;
+      g_decode(r0, w, e);
+      g_store(w, e, mybuf, tbase + 32 * lj);
+      b_store(r0, mybuf);
+    }
+    load(r0, 2 < nst ? gbase + 2 * kWgBK : kWgFar);
+    __syncthreads();
+    for (int t = 0; t < nst; t += 2) {  // nst is even
+      step(0, t, r1);      // multiply t, expand t+1 (r1), reload r1 with t+3
+      step(1, t + 1, r0);  // multiply t+1, expand t+2 (r0), reload r0 with t+4
+    }
   }
 
-  // lane holds output channel o0 + oi*32 + l%32 and input channels
-  // c0 + cj*32 + 8q + 4*(l/32) + 0..3 of tap (kh, kw) in registers 4q..4q+3
-  const bool part = a.partial != nullptr;
-  const float sc = part ? 0.0f : epilogue_scale<kAcLuq, NS, ASIGNED>(*a.alpha, *a.ascale);
-  const int64_t ncol = 9LL * a.C;
-  uint32_t* out = part ? reinterpret_cast<uint32_t*>(a.partial + (int64_t)blockIdx.y * a.Cout * ncol)
-                       : reinterpret_cast<uint32_t*>(a.dw);
-  const int o = o0 + oi * 32 + r32;
-  if (o < a.Cout) {
+  // Epilogue through LDS (the stage buffers are free after the last
+  // barrier): each wave group stores its sums as rows [o][kw][c] of a slab of
+  // its own; then every thread adds the groups' values of 4 consecutive c and
+  // writes them, so each (o, kw) row of 64 channels leaves as 256
+  // contiguous bytes.  Lane l holds output channel oi*32 + l%32 and input
+  // channels cj*32 + 8q + 4*(l/32) + 0..3 of tap (kh, kw) in registers 4q..4q+3.
+  constexpr int EP = 3 * 64 + 4;  // slab row pitch (int32): rows 4 banks apart
+  static_assert(kWgKG * 64 * EP * 4 <= kWgKG * 2 * kWgStage, "epilogue slabs fit");
+  int32_t* slab = reinterpret_cast<int32_t*>(lds);
+  {
+    int32_t* my = slab + kg * 64 * EP + (oi * 32 + r32) * EP + cj * 32 + 4 * h;
 #pragma unroll
     for (int kw = 0; kw < 3; ++kw)
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const int c = c0 + cj * 32 + 8 * q + 4 * h;
-        if (c >= a.C) continue;
-        v4u v;
+      for (int q = 0; q < 4; ++q)
+        *reinterpret_cast<v4i*>(my + kw * 64 + 8 * q) =
+            v4i{acc[kw][4 * q], acc[kw][4 * q + 1], acc[kw][4 * q + 2], acc[kw][4 * q + 3]};
+  }
+  __syncthreads();
+  const bool part = a.partial != nullptr;
+  const float sc = part ? 0.0f : epilogue_scale<kAcLuq, NS, ASIGNED>(*a.alpha, *a.ascale);
+  const int64_t ncol = 9LL * a.C;
+  uint32_t* out = part ? reinterpret_cast<uint32_t*>(a.partial + (int64_t)split * a.Cout * ncol)
+                       : reinterpret_cast<uint32_t*>(a.dw);
+  // 192 rows (o, kw) of 16 four-channel pieces
+  for (int i = tid; i < 64 * 3 * 16; i += kWgThreads) {
+    const int row = i >> 4, j = i & 15;
+    const int ol = row / 3, kw = row - 3 * (row / 3);
+    const int o = o0 + ol, c = c0 + 4 * j;
+    if (o >= a.Cout || c >= a.C) continue;
+    v4i x = *reinterpret_cast<const v4i*>(slab + ol * EP + kw * 64 + 4 * j);
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int32_t x = acc[kw][4 * q + r];
-          v[r] = part ? (uint32_t)x : __float_as_uint(__fmul_rn((float)x, sc));
-        }
-        uint32_t* dst = out + (int64_t)o * ncol + (kh * 3 + kw) * a.C + c;
-        if (a.vec) {
-          *reinterpret_cast<v4u*>(dst) = v;
-        } else {
+    for (int g = 1; g < kWgKG; ++g) x += *reinterpret_cast<const v4i*>(slab + g * 64 * EP + ol * EP + kw * 64 + 4 * j);
+    v4u v;
 #pragma unroll
-          for (int r = 0; r < 4; ++r)
-            if (c + r < a.C) dst[r] = v[r];
-        }
+    for (int k = 0; k < 4; ++k) v[k] = part ? (uint32_t)x[k] : __float_as_uint(__fmul_rn((float)x[k], sc));
+    uint32_t* dst = out + (int64_t)o * ncol + (kh * 3 + kw) * a.C + c;
+    if (a.vec) {
+      *reinterpret_cast<v4u*>(dst) = v;
+    } else {
+#pragma unroll
+      for (int k = 0; k < 4; ++k)
+        if (c + k < a.C) dst[k] = v[k];
+    }
+  }
+}
+
+// dW = scale * (sum over splits of the int32 sums), summed exactly in int64
+// in a fixed order.  A block owns 256 consecutive outputs; its 16 waves take
+// the splits p = wave, wave + 16, ... with 16-byte loads (4 outputs a lane,
+// several splits in flight), then the 16 partial sums are added through LDS.
+constexpr int kRedThreads = 1024;
+
+template <int NS, bool ASIGNED>
+__global__ __launch_bounds__(kRedThreads) void conv_wgrad_reduce_kernel(const int32_t* __restrict__ partial,
+                                                                       int splits, int64_t MN, int vec,
+                                                                       const float* alpha, const float* ascale,
+                                                                       float* __restrict__ out) {
+  __shared__ int64_t red[kRedThreads / 64][256];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int64_t i0 = (int64_t)blockIdx.x * 256 + 4 * lane;
+  int64_t s[4] = {0, 0, 0, 0};
+  if (vec && i0 + 3 < MN) {
+    // up to 8 splits per wave in flight before the first add
+    for (int p0 = wave; p0 < splits; p0 += 8 * 16) {
+      v4i v[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const int p = p0 + 16 * u;
+        v[u] = p < splits ? *reinterpret_cast<const v4i*>(partial + (int64_t)p * MN + i0) : v4i{0, 0, 0, 0};
       }
+#pragma unroll
+      for (int u = 0; u < 8; ++u)
+#pragma unroll
+        for (int k = 0; k < 4; ++k) s[k] += v[u][k];
+    }
+  } else {
+    for (int p = wave; p < splits; p += 16)
+#pragma unroll
+      for (int k = 0; k < 4; ++k)
+        if (i0 + k < MN) s[k] += partial[(int64_t)p * MN + i0 + k];
+  }
+#pragma unroll
+  for (int k = 0; k < 4; ++k) red[wave][4 * lane + k] = s[k];
+  __syncthreads();
+  if (threadIdx.x < 256) {
+    const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    int64_t tot = 0;
+#pragma unroll
+    for (int w = 0; w < kRedThreads / 64; ++w) tot += red[w][threadIdx.x];
+    if (i < MN) out[i] = __fmul_rn((float)tot, epilogue_scale<kAcLuq, NS, ASIGNED>(*alpha, *ascale));
   }
 }
 
 struct ConvWgPlan {
-  int kchunk, splits;
+  int lg, nranges, nsplit;
 };
 
 static ConvWgPlan plan_conv_wgrad(int64_t T, int64_t C, int64_t Cout) {
   const int64_t tiles = ((Cout + 63) / 64) * ((C + 63) / 64);
-  const int64_t want = (256 + tiles - 1) / tiles;  // one workgroup per CU
-  int64_t kc = (T + want - 1) / want;
-  kc = (kc + kWgBK - 1) / kWgBK * kWgBK;
-  if (kc < 4 * kWgBK) kc = 4 * kWgBK;              // at least 4 stages per split
-  if (kc > kWgMaxChunk) kc = kWgMaxChunk;
+  // about one workgroup per CU: 3 kernel rows x tiles x nsplit ~ 256
+  int64_t want = 256 / (3 * tiles);
+  if (want < 1) want = 1;
+  int64_t lg = (T + want * kWgKG - 1) / (want * kWgKG);
+  lg = (lg + 2 * kWgBK - 1) / (2 * kWgBK) * (2 * kWgBK);  // an even number of stages
+  if (lg > kWgMaxLg) lg = kWgMaxLg;
+  const int64_t nranges = (T + kWgKG * lg - 1) / (kWgKG * lg);
+  // each workgroup sums at most kWgMaxWgPixels pixels, so its int32 sums
+  // cannot overflow (|term| <= 32 * 8 * 15 or 32 * 16 * 7)
+  const int64_t per = kWgMaxWgPixels / (kWgKG * lg);
+  int64_t nsplit = want;
+  if (nsplit < (nranges + per - 1) / per) nsplit = (nranges + per - 1) / per;
+  if (nsplit > nranges) nsplit = nranges;
   ConvWgPlan p;
-  p.kchunk = (int)kc;
-  p.splits = (int)((T + kc - 1) / kc);
+  p.lg = (int)lg;
+  p.nranges = (int)nranges;
+  p.nsplit = (int)nsplit;
   return p;
 }
 
 size_t conv3x3_wgrad_workspace_bytes(int64_t T, int64_t C, int64_t Cout) {
   const ConvWgPlan p = plan_conv_wgrad(T, C, Cout);
-  return p.splits > 1 ? (size_t)p.splits * (size_t)Cout * (size_t)(9 * C) * sizeof(int32_t) : 0;
+  return p.nsplit > 1 ? (size_t)p.nsplit * (size_t)Cout * (size_t)(9 * C) * sizeof(int32_t) : 0;
 }
 
-template <int MAXW, int NS, bool ASIGNED>
-static void conv_wgrad_launch_t(const ConvWgArgs& a, dim3 grid, hipStream_t st) {
-  hipLaunchKernelGGL((conv3x3_wgrad_kernel<MAXW, NS, ASIGNED>), grid, dim3(kWgThreads), 0, st, a);
+int64_t conv3x3_wgrad_blocks(int64_t T, int64_t C, int64_t Cout) {
+  const ConvWgPlan p = plan_conv_wgrad(T, C, Cout);
+  return ((Cout + 63) / 64) * ((C + 63) / 64) * 24 * ((p.nsplit + 7) / 8);
+}
+
+template <int NS, bool ASIGNED>
+static void conv_wgrad_launch_t(const ConvWgArgs& a, unsigned blocks, hipStream_t st) {
+  hipLaunchKernelGGL((conv3x3_wgrad_kernel<NS, ASIGNED>), dim3(blocks), dim3(kWgThreads), 0, st, a);
   if (a.partial) {
     const int64_t MN = (int64_t)a.Cout * 9 * a.C;
-    hipLaunchKernelGGL((splitk_reduce_kernel<kAcLuq, NS, ASIGNED>), dim3((unsigned)((MN + 63) / 64)), dim3(256), 0, st,
-                       a.partial, (int)grid.y, MN, a.alpha, a.ascale, a.dw);
+    const int vec = (MN % 4) == 0;
+    hipLaunchKernelGGL((conv_wgrad_reduce_kernel<NS, ASIGNED>), dim3((unsigned)((MN + 255) / 256)),
+                       dim3(kRedThreads), 0, st, a.partial, a.nsplit, MN, vec, a.alpha, a.ascale, a.dw);
   }
-}
-
-template <int MAXW>
-static void conv_wgrad_launch_w(const ConvWgArgs& a, int ns, int a_signed, dim3 grid, hipStream_t st) {
-  if (ns == 1)
-    a_signed ? conv_wgrad_launch_t<MAXW, 1, true>(a, grid, st) : conv_wgrad_launch_t<MAXW, 1, false>(a, grid, st);
-  else
-    a_signed ? conv_wgrad_launch_t<MAXW, 2, true>(a, grid, st) : conv_wgrad_launch_t<MAXW, 2, false>(a, grid, st);
 }
 
 hipError_t launch_conv3x3_wgrad(const uint8_t* g, int64_t g_plane, int ns, const float* alpha, const uint8_t* act,
@@ -613,20 +770,23 @@ hipError_t launch_conv3x3_wgrad(const uint8_t* g, int64_t g_plane, int ns, const
   a.alpha = alpha;
   a.ascale = ascale;
   a.dw = dw;
-  a.partial = p.splits > 1 ? static_cast<int32_t*>(ws) : nullptr;
+  a.partial = p.nsplit > 1 ? static_cast<int32_t*>(ws) : nullptr;
   a.T = (int)T;
   a.H = (int)H;
   a.W = (int)W;
   a.C = (int)C;
   a.Cout = (int)Cout;
-  a.kchunk = p.kchunk;
+  a.lg = p.lg;
+  a.nranges = p.nranges;
+  a.nsplit = p.nsplit;
+  a.nblk = 24 * ((p.nsplit + 7) / 8);
   a.ctiles = (int)((C + 63) / 64);
   a.vec = (C % 4) == 0 && (((uintptr_t)(a.partial ? (void*)a.partial : (void*)dw)) & 15) == 0;
-  const dim3 grid((unsigned)(((Cout + 63) / 64) * a.ctiles), (unsigned)p.splits);
-  if (W <= 64)
-    conv_wgrad_launch_w<64>(a, ns, a_signed, grid, st);
+  const unsigned blocks = (unsigned)conv3x3_wgrad_blocks(T, C, Cout);
+  if (ns == 1)
+    a_signed ? conv_wgrad_launch_t<1, true>(a, blocks, st) : conv_wgrad_launch_t<1, false>(a, blocks, st);
   else
-    conv_wgrad_launch_w<256>(a, ns, a_signed, grid, st);
+    a_signed ? conv_wgrad_launch_t<2, true>(a, blocks, st) : conv_wgrad_launch_t<2, false>(a, blocks, st);
   return hipGetLastError();
 }
 

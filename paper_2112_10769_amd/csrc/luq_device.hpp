@@ -184,10 +184,11 @@ __device__ __forceinline__ void transpose8x8_nibbles(uint32_t (&r)[8]) {
 // The 8 nibbles of x, one per byte in element order: lo = elements 0..3,
 // hi = elements 4..7.
 __device__ __forceinline__ void spread_nibbles(uint32_t x, uint32_t& lo, uint32_t& hi) {
-  const uint32_t t0 = __builtin_amdgcn_perm(x, x, 0x01010000u);  // bytes b0 b0 b1 b1
-  const uint32_t t1 = __builtin_amdgcn_perm(x, x, 0x03030202u);  // bytes b2 b2 b3 b3
-  lo = (t0 & 0x000F000Fu) | ((t0 >> 4) & 0x0F000F00u);
-  hi = (t1 & 0x000F000Fu) | ((t1 >> 4) & 0x0F000F00u);
+  // byte 2i of the selection from x, byte 2i+1 from x >> 4 (whose byte i
+  // starts with the high nibble of x's byte i)
+  const uint32_t y = x >> 4;
+  lo = __builtin_amdgcn_perm(y, x, 0x05010400u) & 0x0F0F0F0Fu;
+  hi = __builtin_amdgcn_perm(y, x, 0x07030602u) & 0x0F0F0F0Fu;
 }
 
 // Sum of the decoded values of two LUQ codes per byte (one nibble per byte):

@@ -58,6 +58,7 @@ hipError_t launch_conv3x3_dgrad(const uint8_t* g, int64_t g_plane, int ns, const
 // dW [Cout][9*C] of the same convolution from LUQ codes of g transposed
 // [Cout][T] (ns planes) and INT4 codes of the activations transposed [C][T].
 size_t conv3x3_wgrad_workspace_bytes(int64_t T, int64_t C, int64_t Cout);
+int64_t conv3x3_wgrad_blocks(int64_t T, int64_t C, int64_t Cout);
 hipError_t launch_conv3x3_wgrad(const uint8_t* g, int64_t g_plane, int ns, const float* alpha, const uint8_t* act,
                                 const float* ascale, int a_signed, int64_t B, int64_t H, int64_t W, int64_t C,
                                 int64_t Cout, float* dw, void* ws, hipStream_t st);

@@ -239,7 +239,7 @@ def _cw(**kw):
     (dict(g=NUL), 1), (dict(alpha=NUL), 1), (dict(a=NUL), 1), (dict(as_=NUL), 1), (dict(dw=NUL), 1),
     (dict(ns=0), 4), (dict(ns=0x12), 4),
     (dict(B=-1), 2), (dict(C=0), 2), (dict(Co=0), 2), (dict(B=0), 2), (dict(H=3, W=3), 2),
-    (dict(B=1 << 14, H=256, W=256), 2), (dict(B=1, H=32, W=257), 2),
+    (dict(B=1 << 14, H=256, W=256), 2), (dict(B=17, H=1 << 15, W=1 << 10, C=1, Co=1), 2),
     (dict(g=PMIS), 6), (dict(a=PMIS), 6), (dict(dw=ctypes.c_void_p(0x10002)), 6),
     (dict(B=64, H=56, W=56, ws=NUL), 5), (dict(B=64, H=56, W=56, wsb=1024), 5),
     (dict(B=64, H=56, W=56, ws=PMIS), 6),
