@@ -481,12 +481,15 @@ __global__ __launch_bounds__(kWgThreads, 1) void conv3x3_wgrad_kernel(ConvWgArgs
     uint8_t* base = stage + lrow * kWgGPitch + 32 * lj;
 #pragma unroll
     for (int hlf = 0; hlf < 2; ++hlf) {
-      const uint4 k0m = m0[hlf], k1m = m1[hlf], k2m = m2[hlf];
+      const uint4 k0m = m0[hlf], k2m = m2[hlf];
+      const uint4 k1m = kh == 1 ? make_uint4(0u, 0u, 0u, 0u) : m1[hlf];
       const int d = 4 * hlf;
       reinterpret_cast<uint4*>(base)[hlf] =
           make_uint4(c0w[d] & k0m.x, c0w[d + 1] & k0m.y, c0w[d + 2] & k0m.z, c0w[d + 3] & k0m.w);
+      // copy 1 needs no mask for the middle row (pixels past T load as zero)
       reinterpret_cast<uint4*>(base + kWgGCopy)[hlf] =
-          make_uint4(w[d] & k1m.x, w[d + 1] & k1m.y, w[d + 2] & k1m.z, w[d + 3] & k1m.w);
+          kh == 1 ? make_uint4(w[d], w[d + 1], w[d + 2], w[d + 3])
+                  : make_uint4(w[d] & k1m.x, w[d + 1] & k1m.y, w[d + 2] & k1m.z, w[d + 3] & k1m.w);
       reinterpret_cast<uint4*>(base + 2 * kWgGCopy)[hlf] =
           make_uint4(c2w[d] & k2m.x, c2w[d + 1] & k2m.y, c2w[d + 2] & k2m.z, c2w[d + 3] & k2m.w);
     }
@@ -578,8 +581,6 @@ __global__ __launch_bounds__(kWgThreads, 1) void conv3x3_wgrad_kernel(ConvWgArgs
     const int rbase = rg * (kWgKG * a.lg);
     const int gbase = rbase + kg * a.lg;
     const int tbase = kg * a.lg;
-    build_masks(rbase);
-    __syncthreads();  // mask tables written
     // one pipeline step: multiply stage t (buffer cb) while expanding stage
     // t+1 (registers R) into the other buffer; R is refilled with stage t+3
     // as soon as it is decoded.
@@ -603,6 +604,8 @@ __global__ __launch_bounds__(kWgThreads, 1) void conv3x3_wgrad_kernel(ConvWgArgs
     Regs r0, r1;
     load(r0, gbase);
     load(r1, 1 < nst ? gbase + kWgBK : kWgFar);
+    build_masks(rbase);  // while the first stages load
+    __syncthreads();     // mask tables written
     {
       uint32_t w[8], e;
       g_decode(r0, w, e);

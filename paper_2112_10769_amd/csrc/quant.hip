@@ -559,8 +559,9 @@ struct Int4Args {
   float* scale_out;
 };
 
-__device__ __forceinline__ Int4Params int4_block_params(const Int4Args& a) {
-  __shared__ uint32_t scratch[kThreads / kWave];
+// Scale and rounding parameters from the range: clip when positive, else the
+// max key mbits of the tensor (Section 3.3, Appendix A.1).
+__device__ __forceinline__ Int4Params int4_params(const Int4Args& a, uint32_t mbits) {
   Int4Params p;
   const float Q = a.is_signed ? 7.0f : 15.0f;
   float m, s;
@@ -568,7 +569,6 @@ __device__ __forceinline__ Int4Params int4_block_params(const Int4Args& a) {
   if (a.clip > 0.0f) {
     m = a.clip;
   } else {
-    const uint32_t mbits = reduce_partials(a.partial, a.nparts, scratch);
     nonfinite = mbits >= 0x7F800000u;
     m = __uint_as_float(mbits);
   }
@@ -589,6 +589,11 @@ __device__ __forceinline__ Int4Params int4_block_params(const Int4Args& a) {
   p.hi = Q;
   if (blockIdx.x == 0 && threadIdx.x == 0) *a.scale_out = s;
   return p;
+}
+
+__device__ __forceinline__ Int4Params int4_block_params(const Int4Args& a) {
+  __shared__ uint32_t scratch[kThreads / kWave];
+  return int4_params(a, a.clip > 0.0f ? 0u : reduce_partials(a.partial, a.nparts, scratch));
 }
 
 __device__ __forceinline__ uint32_t int4_nibble(uint32_t b, const Int4Params& p) {
@@ -638,6 +643,62 @@ __global__ __launch_bounds__(kThreads) void int4_encode_tile_kernel(Int4Args a, 
   const Int4Params p = int4_block_params(a);
   uint32_t unused = 0;
   encode_tiles<1>(Int4Enc<BF16, NT>{&a, &p}, a.rows, a.cols, lg, lt, a.codes, a.codes_t, 0, lds, unused);
+}
+
+// Small tensors (up to kInt4SmallN elements, such as a convolution's weight):
+// one launch instead of two.  Each of a few workgroups takes the maximum of
+// the whole tensor itself (it is small and stays in L2 after the first
+// read), with eight 8-element groups in flight per thread, and then encodes
+// its share of the tiles or groups.
+constexpr int64_t kInt4SmallN = 1 << 16;
+constexpr int kInt4SmallBlocks = 16;
+
+template <bool BF16, int MODE>
+__global__ __launch_bounds__(kThreads) void int4_small_kernel(Int4Args a, int lg, int lt) {
+  __shared__ uint32_t scratch[kThreads / kWave];
+  __shared__ __attribute__((aligned(16))) uint32_t lds[(1 << kInt4TileLg) + 32 * kTilePad];
+  uint32_t m = 0;
+  if (a.clip <= 0.0f) {
+    constexpr int U = 8;
+    const int64_t ngroups = a.n >> 3;
+    int64_t g = threadIdx.x;
+    for (; g + (U - 1) * kThreads < ngroups; g += U * kThreads) {
+      U8 v[U];
+#pragma unroll
+      for (int u = 0; u < U; ++u) v[u] = load8<BF16>(a.x, (g + u * kThreads) * 8);
+#pragma unroll
+      for (int u = 0; u < U; ++u)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) m = max(m, max_key<MODE>(v[u].v[e]));
+    }
+    for (; g < ngroups; g += kThreads) {
+      const U8 v = load8<BF16>(a.x, g * 8);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) m = max(m, max_key<MODE>(v.v[e]));
+    }
+    if (threadIdx.x == 0 && (a.n & 7)) {
+      const U8 v = load8_tail<BF16>(a.x, ngroups * 8, a.n);  // missing elements read +0 (key 0)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) m = max(m, max_key<MODE>(v.v[e]));
+    }
+    m = block_max_u32(m, scratch);
+  }
+  const Int4Params p = int4_params(a, m);
+  if (a.codes_t) {
+    uint32_t unused = 0;
+    encode_tiles<1>(Int4Enc<BF16, false>{&a, &p}, a.rows, a.cols, lg, lt, a.codes, a.codes_t, 0, lds, unused);
+    return;
+  }
+  const int64_t ngroups = (a.n + 7) >> 3;
+  for (int64_t g = (int64_t)blockIdx.x * kThreads + threadIdx.x; g < ngroups; g += (int64_t)gridDim.x * kThreads) {
+    const bool full = (g * 8 + 8) <= a.n;
+    const U8 v = full ? load8<BF16>(a.x, g * 8) : load8_tail<BF16>(a.x, g * 8, a.n);
+    const uint32_t word = p.zero ? 0u : int4_word(v, p);
+    if (full)
+      store_word<false>(a.codes + g * 4, word);
+    else
+      store_bytes(a.codes + g * 4, word, (int)((a.n - g * 8 + 1) >> 1));
+  }
 }
 
 // ------------------------------- launchers ---------------------------------
@@ -825,6 +886,16 @@ hipError_t launch_luq_quantize_hindsight(const void* g, int bf16, int64_t rows, 
 
 template <bool BF16>
 static hipError_t int4_launch_t(Int4Args a, hipStream_t st) {
+  if (a.n <= kInt4SmallN) {
+    const TileShape t = tile_shape(a.rows, a.cols, kInt4TileLg);
+    int blocks = a.codes_t ? t.blocks : (int)((((a.n + 7) >> 3) + kThreads - 1) / kThreads);
+    if (blocks > kInt4SmallBlocks) blocks = kInt4SmallBlocks;
+    if (a.is_signed)
+      hipLaunchKernelGGL((int4_small_kernel<BF16, 0>), dim3(blocks), dim3(kThreads), 0, st, a, t.lg, t.lt);
+    else
+      hipLaunchKernelGGL((int4_small_kernel<BF16, 1>), dim3(blocks), dim3(kThreads), 0, st, a, t.lg, t.lt);
+    return hipGetLastError();
+  }
   if (a.clip <= 0.0f) {
     if (a.is_signed)
       launch_max_pass<BF16, 0>(a.x, a.n, a.nparts, const_cast<uint32_t*>(a.partial), st);
