@@ -11,16 +11,21 @@
 // [Cout][3][3][C] in the transposed layout [9*C][Cout].  No lowered matrix
 // is formed: the output is T x C floats, not T x 9C.
 //
-// A workgroup owns kBM consecutive pixels and 64 channels.  For each 64-deep
-// chunk of Cout it expands, once, into LDS:
-//   - the gradient codes of its pixels and of the W + 1 pixels on either
-//     side (every tap of every pixel reads inside that halo, because a tap
-//     shifts the flat pixel index by (1 - kh) * W + (1 - kw)),
-//   - the 9 x 64 x 64 weight codes of the chunk;
+// A tile is kBM consecutive pixels times 64 channels.  For each 64-deep chunk
+// of Cout a workgroup expands into LDS:
+//   - the gradient codes of the tile's pixels and of the W + 1 pixels on
+//     either side (every tap of every pixel reads inside that halo, because a
+//     tap shifts the flat pixel index by (1 - kh) * W + (1 - kw)),
+//   - the 9 x 64 x 64 weight codes of the chunk (once per workgroup when
+//     Cout <= 64: they then stay in LDS for all its tiles);
 // then multiplies nine taps of two 32-deep k-steps.  A tap's A fragment is
 // the halo shifted by the tap's pixel offset; a lane whose pixel's tap falls
-// off the image reads a zero row instead.  Expansion and MFMA carrier are
-// those of the GEMMs (gemm_kernel.hpp): exact int32 sums, scales applied once.
+// off the image reads a zero row instead.  Workgroups are persistent (about
+// two per CU) and walk their tiles in order; the codes of the next (tile,
+// chunk) are loaded into registers while the current one is multiplied, so
+// the loads of one tile overlap the MFMAs and output stores of the previous.
+// Expansion and MFMA carrier are those of the GEMMs (gemm_kernel.hpp): exact
+// int32 sums, scales applied once.
 #include "gemm_kernel.hpp"
 
 namespace luq {
@@ -30,11 +35,17 @@ constexpr int kConvBM = 256;       // pixels per workgroup (4 waves x 64)
 constexpr int kConvBN = 64;        // channels per workgroup
 constexpr int kConvPitch = 80;     // LDS row pitch (64 int8 + 16 pad)
 
+constexpr int kConvEP = 64 + 4;                               // epilogue slab pitch (words)
+constexpr int kConvSlabs = 4 * 32 * kConvEP * 4;               // epilogue slabs (bytes)
+
 template <int MAXW>
 struct ConvLds {
   static constexpr int kHalo = kConvBM + 2 * (MAXW + 1);        // halo rows
-  static constexpr int kZeroRow = kHalo;                         // an all-zero row
-  static constexpr int kABytes = (kHalo + 1) * kConvPitch;
+  // A region: the halo, then (past the epilogue slabs, which reuse the
+  // region) an all-zero row that stays zero
+  static constexpr int kZeroRow =
+      ((kHalo * kConvPitch > kConvSlabs ? kHalo * kConvPitch : kConvSlabs) + kConvPitch - 1) / kConvPitch;
+  static constexpr int kABytes = (kZeroRow + 1) * kConvPitch;
   static constexpr int kBBytes = 9 * kConvBN * kConvPitch;
   static constexpr int kBytes = kABytes + kBBytes;
   static constexpr int kAPieces = (2 * kHalo + kConvThreads - 1) / kConvThreads;   // per thread
@@ -49,7 +60,7 @@ struct ConvArgs {
   const float* wscale;
   float* dact;           // [T][C]
   int T, H, W, C, Cout;
-  int tiles_m;
+  int tiles_m;           // pixel tiles; each workgroup walks blockIdx.x + k * gridDim.x
   int vec;               // dact rows 16-byte aligned with C % 4 == 0
 };
 
@@ -57,19 +68,17 @@ template <int MAXW, int NS, bool WSIGNED>
 __global__ __launch_bounds__(kConvThreads, MAXW <= 64 ? 2 : 1) void conv3x3_dgrad_kernel(ConvArgs a) {
   using Lds = ConvLds<MAXW>;
   __shared__ __attribute__((aligned(16))) uint8_t lds[Lds::kBytes];
+  static_assert(kConvSlabs <= Lds::kZeroRow * kConvPitch, "epilogue slabs stay below the zero row");
   uint8_t* As = lds;
   uint8_t* Bs = lds + Lds::kABytes;
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  // tiles of consecutive pixels go to one XCD (blocks are dealt round-robin
-  // over the 8 XCDs), so the halos two neighbours share hit the same L2
-  int L = blockIdx.x;
-  if ((a.tiles_m & 7) == 0) L = (L & 7) * (a.tiles_m >> 3) + (L >> 3);
-  const int t0 = L * kConvBM;
   const int c0 = blockIdx.y * kConvBN;
-  const int hoff = a.W + 1;                       // halo rows before t0
+  const int hoff = a.W + 1;                       // halo rows before a tile
   const int hrows = kConvBM + 2 * hoff;
   const int rowb = a.Cout >> 1;                   // bytes per code row (both operands)
+  const int nchunks = (a.Cout + 63) >> 6;
+  const bool resident = nchunks == 1;             // weights expanded once
 
   __amdgpu_buffer_rsrc_t rsg[NS];
 #pragma unroll
@@ -81,66 +90,50 @@ __global__ __launch_bounds__(kConvThreads, MAXW <= 64 ? 2 : 1) void conv3x3_dgra
   // the zero row (read by taps off the image)
   if (tid < 4) reinterpret_cast<uint4*>(As + Lds::kZeroRow * kConvPitch)[tid] = make_uint4(0, 0, 0, 0);
 
-  // Per lane: the LDS byte offsets of its two A-fragment rows (pixel rows
-  // wave*64 + i*32 + lane%32 of the tile) and which of the nine taps of each
-  // stay on the image.
-  int abase[2];
-  uint32_t tapok[2];
-#pragma unroll
-  for (int i = 0; i < 2; ++i) {
-    const int r = wave * 64 + i * 32 + (lane & 31);
-    const int t = t0 + r;
-    abase[i] = (r + hoff) * kConvPitch + (lane >> 5) * 16;
-    uint32_t ok = 0;
-    if (t < a.T) {
-      const int hw = a.H * a.W;
-      const int rem = t % hw;
-      const int y = rem / a.W, x = rem - (rem / a.W) * a.W;
-#pragma unroll
-      for (int kh = 0; kh < 3; ++kh)
-#pragma unroll
-        for (int kw = 0; kw < 3; ++kw) {
-          const int ys = y + 1 - kh, xs = x + 1 - kw;
-          if (ys >= 0 && ys < a.H && xs >= 0 && xs < a.W) ok |= 1u << (kh * 3 + kw);
-        }
-    }
-    tapok[i] = ok;
-  }
-  const int zbase = Lds::kZeroRow * kConvPitch + (lane >> 5) * 16;
+  // Tile of the k-th item of this workgroup: tiles of consecutive pixels go
+  // to one XCD (blocks are dealt round-robin over the 8 XCDs and the grid is
+  // a multiple of 8 wide), so the halos two neighbours share hit one L2.
+  auto tile_of = [&](int k) {
+    int L = blockIdx.x + k * gridDim.x;
+    if ((a.tiles_m & 7) == 0 && (gridDim.x & 7) == 0) L = (L & 7) * (a.tiles_m >> 3) + (L >> 3);
+    return L;
+  };
+  const int nitems = ((a.tiles_m - (int)blockIdx.x + (int)gridDim.x - 1) / (int)gridDim.x) * nchunks;
 
-  v16i acc[2][2];
-#pragma unroll
-  for (int i = 0; i < 2; ++i)
-#pragma unroll
-    for (int j = 0; j < 2; ++j) acc[i][j] = v16i{};
-
-  const int nchunks = (a.Cout + 63) >> 6;
-  for (int cc = 0; cc < nchunks; ++cc) {
-    if (cc > 0) __syncthreads();  // the previous chunk's fragments are consumed
-    // ---- load: halo pieces (row h, half hf: 32 codes of o) and weight pieces
+  // ---- loads of item it (tile it / nchunks, Cout chunk it % nchunks) into
+  // registers: halo pieces (row h, half hf: 32 codes of o) and weight pieces
+  struct Regs {
     v4u ga[Lds::kAPieces][NS];
     v4u wb[Lds::kBPieces];
+  };
+  auto load = [&](Regs& r, int it) {
+    const bool live = it < nitems;
+    const int t0 = tile_of(live ? it / nchunks : 0) * kConvBM;
+    const int cc = live ? it % nchunks : 0;
 #pragma unroll
     for (int q = 0; q < Lds::kAPieces; ++q) {
       const int p = tid + q * kConvThreads;
       const int h = p >> 1, hf = p & 1;
       const int pix = t0 - hoff + h;
-      const bool in = p < 2 * hrows && pix >= 0 && pix < a.T && cc * 64 + hf * 32 < a.Cout;
+      const bool in = live && p < 2 * hrows && pix >= 0 && pix < a.T && cc * 64 + hf * 32 < a.Cout;
       const int off = in ? pix * rowb + cc * 32 + hf * 16 : kOutOfRange;
 #pragma unroll
-      for (int s = 0; s < NS; ++s) ga[q][s] = __builtin_amdgcn_raw_buffer_load_b128(rsg[s], off, 0, 0);
+      for (int s = 0; s < NS; ++s) r.ga[q][s] = __builtin_amdgcn_raw_buffer_load_b128(rsg[s], off, 0, 0);
     }
+    const bool wlive = live && (!resident || it == 0);
 #pragma unroll
     for (int q = 0; q < Lds::kBPieces; ++q) {
       const int p = tid + q * kConvThreads;
       const int row = p >> 1, hf = p & 1;              // row = tap * 64 + c
       const int tap = row >> 6, c = row & 63;
-      const bool in = p < 2 * 9 * kConvBN && c0 + c < a.C && cc * 64 + hf * 32 < a.Cout;
+      const bool in = wlive && p < 2 * 9 * kConvBN && c0 + c < a.C && cc * 64 + hf * 32 < a.Cout;
       const int off = in ? (tap * a.C + c0 + c) * rowb + cc * 32 + hf * 16 : kOutOfRange;
-      wb[q] = __builtin_amdgcn_raw_buffer_load_b128(rsw, off, 0, 0);
+      r.wb[q] = __builtin_amdgcn_raw_buffer_load_b128(rsw, off, 0, 0);
     }
-    // ---- expand to int8 in LDS (even-k nibbles of a word in one word, odd-k
-    // in the next; both operands alike)
+  };
+  // ---- expand to int8 in LDS (even-k nibbles of a word in one word, odd-k
+  // in the next; both operands alike)
+  auto expand = [&](const Regs& r, bool weights) {
 #pragma unroll
     for (int q = 0; q < Lds::kAPieces; ++q) {
       const int p = tid + q * kConvThreads;
@@ -150,11 +143,11 @@ __global__ __launch_bounds__(kConvThreads, MAXW <= 64 ? 2 : 1) void conv3x3_dgra
 #pragma unroll
       for (int d = 0; d < 4; ++d) {
         if constexpr (NS == 1) {
-          expand_luq(ga[q][0][d], w[2 * d], w[2 * d + 1]);
+          expand_luq(r.ga[q][0][d], w[2 * d], w[2 * d + 1]);
         } else {
           uint32_t l0, h0, l1, h1;
-          expand_luq_excess64(ga[q][0][d], l0, h0);
-          expand_luq_excess64(ga[q][1][d], l1, h1);
+          expand_luq_excess64(r.ga[q][0][d], l0, h0);
+          expand_luq_excess64(r.ga[q][1][d], l1, h1);
           w[2 * d] = (l0 + l1) ^ 0x80808080u;
           w[2 * d + 1] = (h0 + h1) ^ 0x80808080u;
         }
@@ -163,6 +156,7 @@ __global__ __launch_bounds__(kConvThreads, MAXW <= 64 ? 2 : 1) void conv3x3_dgra
       dst[0] = make_uint4(w[0], w[1], w[2], w[3]);
       dst[1] = make_uint4(w[4], w[5], w[6], w[7]);
     }
+    if (!weights) return;
 #pragma unroll
     for (int q = 0; q < Lds::kBPieces; ++q) {
       const int p = tid + q * kConvThreads;
@@ -170,11 +164,54 @@ __global__ __launch_bounds__(kConvThreads, MAXW <= 64 ? 2 : 1) void conv3x3_dgra
       const int row = p >> 1, hf = p & 1;
       uint32_t w[8];
 #pragma unroll
-      for (int d = 0; d < 4; ++d) expand_int4<WSIGNED>(wb[q][d], w[2 * d], w[2 * d + 1]);
+      for (int d = 0; d < 4; ++d) expand_int4<WSIGNED>(r.wb[q][d], w[2 * d], w[2 * d + 1]);
       uint4* dst = reinterpret_cast<uint4*>(Bs + row * kConvPitch + hf * 32);
       dst[0] = make_uint4(w[0], w[1], w[2], w[3]);
       dst[1] = make_uint4(w[4], w[5], w[6], w[7]);
     }
+  };
+
+  const float sc = epilogue_scale<kAcLuq, NS, WSIGNED>(*a.alpha, *a.wscale);
+  const int zbase = Lds::kZeroRow * kConvPitch + (lane >> 5) * 16;
+  v16i acc[2][2];
+  int abase[2];
+  uint32_t tapok[2];
+  Regs r;
+  load(r, 0);
+  for (int it = 0; it < nitems; ++it) {
+    const int cc = it % nchunks;
+    const int t0 = tile_of(it / nchunks) * kConvBM;
+    if (cc == 0) {
+      // per lane: the LDS byte offsets of its two A-fragment rows (pixel rows
+      // wave*64 + i*32 + lane%32 of the tile) and which of the nine taps of
+      // each stay on the image
+#pragma unroll
+      for (int i = 0; i < 2; ++i) {
+        const int rr = wave * 64 + i * 32 + (lane & 31);
+        const int t = t0 + rr;
+        abase[i] = (rr + hoff) * kConvPitch + (lane >> 5) * 16;
+        uint32_t ok = 0;
+        if (t < a.T) {
+          const int hw = a.H * a.W;
+          const int rem = t % hw;
+          const int y = rem / a.W, x = rem - (rem / a.W) * a.W;
+#pragma unroll
+          for (int kh = 0; kh < 3; ++kh)
+#pragma unroll
+            for (int kw = 0; kw < 3; ++kw) {
+              const int ys = y + 1 - kh, xs = x + 1 - kw;
+              if (ys >= 0 && ys < a.H && xs >= 0 && xs < a.W) ok |= 1u << (kh * 3 + kw);
+            }
+        }
+        tapok[i] = ok;
+      }
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j) acc[i][j] = v16i{};
+    }
+    expand(r, !resident || it == 0);
+    load(r, it + 1);  // the next item's codes load while this one is multiplied
     __syncthreads();
 
     // ---- nine taps x two 32-deep k-steps
@@ -201,47 +238,53 @@ __global__ __launch_bounds__(kConvThreads, MAXW <= 64 ? 2 : 1) void conv3x3_dgra
             acc[i][j] = __builtin_amdgcn_mfma_i32_32x32x32_i8(fb[j], fa[i], acc[i][j], 0, 0, 0);
       }
     }
-  }
+    __syncthreads();  // every wave is done with the operands in LDS
+    if (cc != nchunks - 1) continue;
 
-  // ---- epilogue through LDS: lane l of MFMA tile (i, j) holds pixel row l%32
-  // and, in registers 4q..4q+3, channels 8q + 4*(l/32) + 0..3 of the 32.  Each
-  // wave stages 32 rows x 64 channels, then stores 16-byte row segments
-  // (16 lanes per row, 4 rows per instruction).
-  constexpr int EP = 64 + 4;  // slab pitch in words
-  static_assert(4 * 32 * EP * 4 <= Lds::kBytes, "epilogue slabs fit");
-  uint32_t* E = reinterpret_cast<uint32_t*>(lds) + wave * 32 * EP;
-  const float sc = epilogue_scale<kAcLuq, NS, WSIGNED>(*a.alpha, *a.wscale);
-  const int srow = lane >> 4, scol = (lane & 15) * 4;
-  __syncthreads();  // every wave is done with the operands in LDS
+    // ---- epilogue through LDS slabs in the A region (below the zero row):
+    // lane l of MFMA tile (i, j) holds pixel row l%32 and, in registers
+    // 4q..4q+3, channels 8q + 4*(l/32) + 0..3 of the 32.  Each wave stages
+    // 32 rows x 64 channels, then stores 16-byte row segments (16 lanes per
+    // row, 4 rows per instruction).
+    uint32_t* E = reinterpret_cast<uint32_t*>(As) + wave * 32 * kConvEP;
+    const int srow = lane >> 4, scol = (lane & 15) * 4;
 #pragma unroll
-  for (int i = 0; i < 2; ++i) {
+    for (int i = 0; i < 2; ++i) {
 #pragma unroll
-    for (int j = 0; j < 2; ++j)
+      for (int j = 0; j < 2; ++j)
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        v4u v;
+        for (int q = 0; q < 4; ++q) {
+          v4u v;
 #pragma unroll
-        for (int r = 0; r < 4; ++r) v[r] = __float_as_uint(__fmul_rn((float)acc[i][j][4 * q + r], sc));
-        *reinterpret_cast<v4u*>(E + (lane & 31) * EP + j * 32 + 8 * q + 4 * (lane >> 5)) = v;
-      }
-    __syncthreads();
+          for (int k = 0; k < 4; ++k) v[k] = __float_as_uint(__fmul_rn((float)acc[i][j][4 * q + k], sc));
+          *reinterpret_cast<v4u*>(E + (lane & 31) * kConvEP + j * 32 + 8 * q + 4 * (lane >> 5)) = v;
+        }
+      // the slab is private to the wave: a wave barrier orders its writes
+      // before its reads
+      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+      __builtin_amdgcn_wave_barrier();
+      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
 #pragma unroll
-    for (int rr = 0; rr < 32; rr += 4) {
-      const int t = t0 + wave * 64 + i * 32 + rr + srow;
-      const int c = c0 + scol;
-      if (t < a.T && c < a.C) {
-        const v4u v = *reinterpret_cast<const v4u*>(E + (rr + srow) * EP + scol);
-        float* dst = a.dact + (int64_t)t * a.C + c;
-        if (a.vec) {
-          *reinterpret_cast<v4u*>(dst) = v;
-        } else {
+      for (int rr = 0; rr < 32; rr += 4) {
+        const int t = t0 + wave * 64 + i * 32 + rr + srow;
+        const int c = c0 + scol;
+        if (t < a.T && c < a.C) {
+          const v4u v = *reinterpret_cast<const v4u*>(E + (rr + srow) * kConvEP + scol);
+          float* dst = a.dact + (int64_t)t * a.C + c;
+          if (a.vec) {
+            *reinterpret_cast<v4u*>(dst) = v;
+          } else {
 #pragma unroll
-          for (int r = 0; r < 4; ++r)
-            if (c + r < a.C) dst[r] = __uint_as_float(v[r]);
+            for (int k = 0; k < 4; ++k)
+              if (c + k < a.C) dst[k] = __uint_as_float(v[k]);
+          }
         }
       }
+      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+      __builtin_amdgcn_wave_barrier();
+      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
     }
-    __syncthreads();
+    __syncthreads();  // the slabs are free before the next expansion
   }
 }
 
@@ -272,7 +315,13 @@ hipError_t launch_conv3x3_dgrad(const uint8_t* g, int64_t g_plane, int ns, const
   a.Cout = (int)Cout;
   a.tiles_m = (a.T + kConvBM - 1) / kConvBM;
   a.vec = (C % 4) == 0 && (((uintptr_t)dact) & 15) == 0;
-  const dim3 grid((unsigned)a.tiles_m, (unsigned)((C + kConvBN - 1) / kConvBN));
+  // persistent workgroups: about two per CU (one for wide images), a multiple
+  // of 8 wide, each taking tiles blockIdx.x, blockIdx.x + gridDim.x, ...
+  const int ctiles = (int)((C + kConvBN - 1) / kConvBN);
+  int per = (W <= 64 ? 512 : 256) / ctiles;
+  per = per < 8 ? 8 : per & ~7;
+  const int gx = a.tiles_m < per ? a.tiles_m : per;
+  const dim3 grid((unsigned)gx, (unsigned)ctiles);
   if (W <= 64) {
     if (ns == 1) conv_launch_w<64, 1>(a, w_signed, grid, st);
     else conv_launch_w<64, 2>(a, w_signed, grid, st);
