@@ -86,6 +86,8 @@ def _conv_case(L, B, H, W, C, Cout, ns=1, wsig=True, seed=0, zero_grad=False, us
     (1, 2, 256, 4, 32),       # the widest image accepted
     (3, 1, 37, 16, 64),       # height 1
     (2, 45, 1, 16, 64),       # width 1
+    (160, 32, 32, 8, 96),     # 640 tiles: workgroups walk two tiles, two Cout chunks each
+    (8, 90, 100, 8, 96),      # wide-halo kernel with workgroups walking two tiles
 ])
 @pytest.mark.parametrize("ns", [1, 2])
 def test_conv_dgrad_parity(L, B, H, W, C, Cout, ns):
@@ -192,6 +194,7 @@ def _wgrad_case(L, B, H, W, C, Cout, ns=1, asig=False, seed=0):
     (32, 32, 1, 16, 64),      # width 1
     (2, 3, 160, 8, 40),       # width above the 64-pixel window margin
     (16, 28, 28, 64, 64),     # several splits (split-K)
+    (4, 256, 256, 8, 8),      # more pixel ranges than workgroups: some take two
 ])
 @pytest.mark.parametrize("ns", [1, 2])
 def test_conv_wgrad_parity(L, B, H, W, C, Cout, ns):
