@@ -312,7 +312,7 @@ luq_status int4_im2col3x3_t(const uint8_t* act_codes, int64_t B, int64_t H, int6
  *             output of int4_quantize on W [Cout][9*C]; w_scale 1 float
  *             (device); w_signed 0/1.
  *  B, H, W, C >= 0 (nothing is done when B*H*W or C is 0); W <= 256;
- *             Cout a multiple of 32 in [32, 16384]; each code operand below
+ *             C <= 2^20; Cout a multiple of 32 in [32, 16384]; each code operand below
  *             1 GiB.  n_samples 1 or 2 (codes from this library, R <= 5 for 2).
  *  dact       out: [T][C] fp32, row-major (NHWC).
  *  No workspace.  Errors: LUQ_ERR_SHAPE, LUQ_ERR_PARAM, LUQ_ERR_NULL,

@@ -293,6 +293,7 @@ luq_status luq_conv3x3_dgrad(const uint8_t* g_codes, const float* alpha, int n_s
   if (Cout < 32 || (Cout & 31) || Cout > 16384)
     return fail(LUQ_ERR_SHAPE, "%s: Cout must be a multiple of 32 in [32, 16384]", fn);
   if (W > luq::conv3x3_max_width()) return fail(LUQ_ERR_SHAPE, "%s: image width above 256", fn);
+  if (C > ((int64_t)1 << 20)) return fail(LUQ_ERR_SHAPE, "%s: more than 2^20 input channels", fn);
   if (T * (Cout / 2) >= ((int64_t)1 << 30) || 9 * C * (Cout / 2) >= ((int64_t)1 << 30))
     return fail(LUQ_ERR_SHAPE, "%s: operand above 1 GiB of codes", fn);
   if (!g_codes || !alpha || !w_codes_t || !w_scale || !dact) return fail(LUQ_ERR_NULL, "%s: NULL operand", fn);

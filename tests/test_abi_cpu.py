@@ -202,7 +202,7 @@ def _cv(**kw):
     (dict(g=NUL), 1), (dict(alpha=NUL), 1), (dict(w=NUL), 1), (dict(ws_=NUL), 1), (dict(out=NUL), 1),
     (dict(ns=0), 4), (dict(ns=3), 4),
     (dict(B=-1), 2), (dict(Co=48), 2), (dict(Co=0), 2), (dict(Co=16), 2), (dict(Co=32768), 2),
-    (dict(W=257), 2), (dict(B=4096, H=256, W=256, Co=64), 2),
+    (dict(W=257), 2), (dict(B=4096, H=256, W=256, Co=64), 2), (dict(B=1, H=1, W=1, C=(1 << 20) + 1, Co=32), 2),
     (dict(g=PMIS), 6), (dict(w=PMIS), 6), (dict(out=ctypes.c_void_p(0x10002)), 6),
     (dict(B=0), 0), (dict(C=0), 0), (dict(B=0, g=NUL, out=NUL), 0),
 ])
