@@ -141,49 +141,113 @@ __device__ __forceinline__ void encode_tiles(const Enc& enc, int64_t rows, int64
   const int64_t ntr = (rows + tr - 1) / tr, ntc = (cgs + tg - 1) / tg;
   for (int64_t t = blockIdx.x; t < ntr * ntc; t += gridDim.x) {
     const int64_t r0 = (t / ntc) * tr, g0 = (t % ntc) * tg;
-    // two items per trip (tw is a multiple of 2 * kThreads): both loads are
-    // in flight before either is encoded
-    constexpr int U = 2;
-    for (int q0 = threadIdx.x; q0 < tw; q0 += U * kThreads) {
-      int g[U], r[U];
-      bool ok[U];
-      int64_t e0[U];
-      U8 v[U];
+    if constexpr (Enc::kPipeline) {
+      // two items per trip (tw is a multiple of 2 * kThreads, so the trip count
+      // is even): the next trip's loads are issued before this trip's items are
+      // encoded, so one trip's encode hides the next one's memory latency.  The
+      // fetch after the last trip re-reads the first one (in bounds, ignored):
+      // every trip issues the same loads and the wait counts stay static.
+      constexpr int U = 2;
+      const int ntrips = tw / (U * kThreads);
+      struct Trip {
+        int g[U], r[U];
+        bool ok[U];
+        int64_t e0[U];
+        U8 v[U];
+      };
+      auto fetch = [&](Trip& T, int trip) {
 #pragma unroll
-      for (int u = 0; u < U; ++u) {
-        const int q = q0 + u * kThreads;
-        g[u] = q & (tg - 1);
-        r[u] = q >> lg;
-        const int64_t row = r0 + r[u], cg = g0 + g[u];
-        ok[u] = row < rows && cg < cgs;
-        e0[u] = row * cols + cg * 8;
-        if (ok[u]) {
-          v[u] = enc.load(e0[u]);
-          if constexpr (Enc::kTrack) mx = max(mx, max_key8(v[u]));
+        for (int u = 0; u < U; ++u) {
+          const int q = threadIdx.x + (trip * U + u) * kThreads;
+          T.g[u] = q & (tg - 1);
+          T.r[u] = q >> lg;
+          const int64_t row = r0 + T.r[u], cg = g0 + T.g[u];
+          T.ok[u] = row < rows && cg < cgs;
+          T.e0[u] = row * cols + cg * 8;
+          T.v[u] = enc.load(T.ok[u] ? T.e0[u] : 0);  // no branch: an item off the tensor reads element 0
         }
+      };
+      auto encode = [&](const Trip& T) {
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+          if constexpr (Enc::kTrack) {
+            if (T.ok[u]) mx = max(mx, max_key8(T.v[u]));
+          }
+          uint32_t w[NS];
+#pragma unroll
+          for (int s = 0; s < NS; ++s) w[s] = 0;
+          if (T.ok[u]) {
+#pragma unroll
+            for (int s = 0; s < NS; ++s) w[s] = enc.word(T.v[u], (uint64_t)(T.e0[u] >> 3), s);
+            if constexpr (SUM) {
+              uint32_t lo, hi;
+              smp_sum_bytes(w[0], w[1], lo, hi);
+              w[0] = lo;
+              w[1] = hi;
+              if (codes) store_word2<Enc::kNT>(codes + T.e0[u], lo, hi);
+            } else {
+#pragma unroll
+              for (int s = 0; s < NS; ++s)
+                if (codes) store_word<Enc::kNT>(codes + s * plane + (T.e0[u] >> 1), w[s]);
+            }
+          }
+#pragma unroll
+          for (int s = 0; s < NS; ++s) lds[(s * tg + T.g[u]) * pitch + T.r[u]] = w[s];
+        }
+      };
+      Trip ta, tb;
+      fetch(ta, 0);
+      for (int trip = 0; trip < ntrips; trip += 2) {
+        fetch(tb, trip + 1);
+        encode(ta);
+        fetch(ta, trip + 2 < ntrips ? trip + 2 : 0);
+        encode(tb);
       }
+    } else {
+      // two items per trip (tw is a multiple of 2 * kThreads): both loads are
+      // in flight before either is encoded
+      constexpr int U = 2;
+      for (int q0 = threadIdx.x; q0 < tw; q0 += U * kThreads) {
+        int g[U], r[U];
+        bool ok[U];
+        int64_t e0[U];
+        U8 v[U];
 #pragma unroll
-      for (int u = 0; u < U; ++u) {
-        uint32_t w[NS];
-#pragma unroll
-        for (int s = 0; s < NS; ++s) w[s] = 0;
-        if (ok[u]) {
-#pragma unroll
-          for (int s = 0; s < NS; ++s) w[s] = enc.word(v[u], (uint64_t)(e0[u] >> 3), s);
-          if constexpr (SUM) {
-            uint32_t lo, hi;
-            smp_sum_bytes(w[0], w[1], lo, hi);
-            w[0] = lo;
-            w[1] = hi;
-            if (codes) store_word2<Enc::kNT>(codes + e0[u], lo, hi);
-          } else {
-#pragma unroll
-            for (int s = 0; s < NS; ++s)
-              if (codes) store_word<Enc::kNT>(codes + s * plane + (e0[u] >> 1), w[s]);
+        for (int u = 0; u < U; ++u) {
+          const int q = q0 + u * kThreads;
+          g[u] = q & (tg - 1);
+          r[u] = q >> lg;
+          const int64_t row = r0 + r[u], cg = g0 + g[u];
+          ok[u] = row < rows && cg < cgs;
+          e0[u] = row * cols + cg * 8;
+          if (ok[u]) {
+            v[u] = enc.load(e0[u]);
+            if constexpr (Enc::kTrack) mx = max(mx, max_key8(v[u]));
           }
         }
 #pragma unroll
-        for (int s = 0; s < NS; ++s) lds[(s * tg + g[u]) * pitch + r[u]] = w[s];
+        for (int u = 0; u < U; ++u) {
+          uint32_t w[NS];
+#pragma unroll
+          for (int s = 0; s < NS; ++s) w[s] = 0;
+          if (ok[u]) {
+#pragma unroll
+            for (int s = 0; s < NS; ++s) w[s] = enc.word(v[u], (uint64_t)(e0[u] >> 3), s);
+            if constexpr (SUM) {
+              uint32_t lo, hi;
+              smp_sum_bytes(w[0], w[1], lo, hi);
+              w[0] = lo;
+              w[1] = hi;
+              if (codes) store_word2<Enc::kNT>(codes + e0[u], lo, hi);
+            } else {
+#pragma unroll
+              for (int s = 0; s < NS; ++s)
+                if (codes) store_word<Enc::kNT>(codes + s * plane + (e0[u] >> 1), w[s]);
+            }
+          }
+#pragma unroll
+          for (int s = 0; s < NS; ++s) lds[(s * tg + g[u]) * pitch + r[u]] = w[s];
+        }
       }
     }
     __syncthreads();
@@ -491,6 +555,7 @@ __global__ __launch_bounds__(kThreads) void luq_encode_flat_kernel(LuqArgs a) {
 template <bool BF16, bool NT, bool SCALED, bool HS = false>
 struct LuqEnc {
   static constexpr bool kTrack = HS;
+  static constexpr bool kPipeline = true;  // ALU-heavy words: overlap the next loads with them
   static constexpr bool kNT = NT;
   const LuqArgs* a;
   const LuqParams* p;
@@ -630,6 +695,7 @@ __global__ __launch_bounds__(kThreads) void int4_encode_flat_kernel(Int4Args a) 
 template <bool BF16, bool NT>
 struct Int4Enc {
   static constexpr bool kTrack = false;
+  static constexpr bool kPipeline = false;  // memory-bound: the plain trips measure faster
   static constexpr bool kNT = NT;
   const Int4Args* a;
   const Int4Params* p;
