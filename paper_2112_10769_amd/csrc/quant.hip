@@ -34,6 +34,13 @@ constexpr int kThreads = 256;
 constexpr int kDirectPartials = 2048;
 constexpr int kMaxPartials = 16384;
 constexpr int kMaxEncodeBlocks = 4096;
+// Tensors above kCacheBytes (the 256 MB last-level cache) are streamed: the
+// max pass reads all but the last kKeepBytes of them non-temporally and the
+// encode pass, whose loads and code stores are then non-temporal too, walks
+// the tensor from its end, so that it starts on the part the max pass left
+// in the cache.
+constexpr int64_t kCacheBytes = 256LL << 20;
+constexpr int64_t kKeepBytes = 192LL << 20;
 
 // Max-pass keys.  MODE 0: |x| (LUQ, signed INT4).  MODE 1: max(x, 0) with
 // non-finite values of either sign kept (unsigned INT4).
@@ -64,10 +71,25 @@ __global__ __launch_bounds__(kThreads) void max_partial_kernel(const void* __res
 #pragma unroll
   for (int i = 0; i < G; ++i) m[i] = 0;
   int64_t g = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+  if constexpr (NT) {
+    // streamed tensor: all but its last kKeepBytes bypass the caches; that
+    // tail, read last, is left in the last-level cache for the encode pass,
+    // which starts there
+    const int64_t cut = ngroups - kKeepBytes / (BF16 ? 16 : 32);
+    for (; g + (G - 1) * stride < cut; g += G * stride) {
+      U8 v[G];
+#pragma unroll
+      for (int i = 0; i < G; ++i) v[i] = load8<BF16, true>(x, (g + i * stride) * 8);
+#pragma unroll
+      for (int i = 0; i < G; ++i)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) m[i] = max(m[i], max_key<MODE>(v[i].v[e]));
+    }
+  }
   for (; g + (G - 1) * stride < ngroups; g += G * stride) {
     U8 v[G];
 #pragma unroll
-    for (int i = 0; i < G; ++i) v[i] = load8<BF16, NT>(x, (g + i * stride) * 8);
+    for (int i = 0; i < G; ++i) v[i] = load8<BF16, false>(x, (g + i * stride) * 8);
 #pragma unroll
     for (int i = 0; i < G; ++i)
 #pragma unroll
@@ -139,7 +161,8 @@ __device__ __forceinline__ void encode_tiles(const Enc& enc, int64_t rows, int64
   const int tw = 1 << lt, tg = 1 << lg, tr = tw >> lg, pitch = tr + kTilePad;
   const int64_t cgs = cols >> 3;
   const int64_t ntr = (rows + tr - 1) / tr, ntc = (cgs + tg - 1) / tg;
-  for (int64_t t = blockIdx.x; t < ntr * ntc; t += gridDim.x) {
+  for (int64_t k = blockIdx.x; k < ntr * ntc; k += gridDim.x) {
+    const int64_t t = Enc::kNT ? ntr * ntc - 1 - k : k;  // a streamed tensor is walked from its end
     const int64_t r0 = (t / ntc) * tr, g0 = (t % ntc) * tg;
     if constexpr (Enc::kPipeline) {
       // two items per trip (tw is a multiple of 2 * kThreads, so the trip count
@@ -473,30 +496,33 @@ __device__ __forceinline__ uint32_t luq_flat_body(const LuqArgs& a, const LuqPar
   uint32_t mx = 0;
   const int64_t nfull = a.n >> 3;
   const int64_t stride = (int64_t)gridDim.x * kThreads;
+  // step k of the walk takes group k, or with NT (streamed tensor) group
+  // nfull - 1 - k: the walk starts at the end of the tensor
+  const auto at = [&](int64_t k) { return NT ? nfull - 1 - k : k; };
   int64_t g = (int64_t)blockIdx.x * kThreads + threadIdx.x;
   // four groups per trip (then two): every load of a trip is in flight before
   // any of its groups is encoded
   for (; g + 3 * stride < nfull; g += 4 * stride) {
     U8 v[4];
 #pragma unroll
-    for (int u = 0; u < 4; ++u) v[u] = load8<BF16, NT>(a.g, (g + u * stride) * 8);
+    for (int u = 0; u < 4; ++u) v[u] = load8<BF16, NT>(a.g, at(g + u * stride) * 8);
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
       if (HS) mx = max(mx, max_key8(v[u]));
-      luq_emit_group<NT, NS, SUM, SCALED, HS>(a, p, v[u], g + u * stride);
+      luq_emit_group<NT, NS, SUM, SCALED, HS>(a, p, v[u], at(g + u * stride));
     }
   }
   for (; g + stride < nfull; g += 2 * stride) {
-    const U8 v0 = load8<BF16, NT>(a.g, g * 8);
-    const U8 v1 = load8<BF16, NT>(a.g, (g + stride) * 8);
+    const U8 v0 = load8<BF16, NT>(a.g, at(g) * 8);
+    const U8 v1 = load8<BF16, NT>(a.g, at(g + stride) * 8);
     if (HS) mx = max(mx, max(max_key8(v0), max_key8(v1)));
-    luq_emit_group<NT, NS, SUM, SCALED, HS>(a, p, v0, g);
-    luq_emit_group<NT, NS, SUM, SCALED, HS>(a, p, v1, g + stride);
+    luq_emit_group<NT, NS, SUM, SCALED, HS>(a, p, v0, at(g));
+    luq_emit_group<NT, NS, SUM, SCALED, HS>(a, p, v1, at(g + stride));
   }
   if (g < nfull) {
-    const U8 v = load8<BF16, NT>(a.g, g * 8);
+    const U8 v = load8<BF16, NT>(a.g, at(g) * 8);
     if (HS) mx = max(mx, max_key8(v));
-    luq_emit_group<NT, NS, SUM, SCALED, HS>(a, p, v, g);
+    luq_emit_group<NT, NS, SUM, SCALED, HS>(a, p, v, at(g));
   }
   if ((a.n & 7) && blockIdx.x == 0 && threadIdx.x == 0) {
     const U8 v = load8_tail<BF16>(a.g, nfull * 8, a.n);  // missing elements read +0
@@ -680,8 +706,9 @@ template <bool BF16, bool NT>
 __global__ __launch_bounds__(kThreads) void int4_encode_flat_kernel(Int4Args a) {
   const Int4Params p = int4_block_params(a);
   const int64_t ngroups = (a.n + 7) >> 3;
-  for (int64_t g = (int64_t)blockIdx.x * kThreads + threadIdx.x; g < ngroups;
-       g += (int64_t)gridDim.x * kThreads) {
+  for (int64_t k = (int64_t)blockIdx.x * kThreads + threadIdx.x; k < ngroups;
+       k += (int64_t)gridDim.x * kThreads) {
+    const int64_t g = NT ? ngroups - 1 - k : k;  // a streamed tensor is walked from its end
     const bool full = (g * 8 + 8) <= a.n;
     const U8 v = full ? load8<BF16, NT>(a.x, g * 8) : load8_tail<BF16>(a.x, g * 8, a.n);
     const uint32_t word = p.zero ? 0u : int4_word(v, p);
@@ -819,10 +846,9 @@ static TileShape tile_shape(int64_t rows, int64_t cols, int max_lt) {
   return t;
 }
 
-// Max pass.  Tensors that fit in the 256 MB last-level cache are read with
-// ordinary loads so that the encode pass can find them there; larger ones
-// are streamed with non-temporal loads.
-constexpr int64_t kCacheBytes = 256LL << 20;
+// Max pass.  Tensors that fit in the last-level cache are read with ordinary
+// loads so that the encode pass can find them there; larger ones are streamed
+// with non-temporal loads, except for their last kKeepBytes.
 
 template <bool BF16, int MODE>
 static void launch_max_pass(const void* x, int64_t n, int nblocks, uint32_t* partial, hipStream_t st) {
