@@ -42,7 +42,8 @@ notes of the repository):
   when alpha was rounded as a subnormal).
 * If alpha rounds to 0 (max|x| = 0, or so small that max/2^R underflows
   float32) every code is 0.
-* Non-finite input: alpha = NaN and every code is 0.
+* Non-finite input: alpha = NaN and every code is 0.  In-hindsight mode: a
+  step whose measured maximum is not finite leaves the estimate unchanged.
 * Packing: two codes per byte, element 2b in the low nibble of byte b; an
   odd element count leaves the last high nibble 0.
 """
@@ -191,6 +192,12 @@ def luq_quantize_hindsight(x, m_hat, dtype="f32", R=4, seed=0, counter=0, n_samp
     the estimate is the power-of-two one (the combination of the appendix's
     power-of-two LUQ with hindsight).
 
+    Eq. hindsight is an average of measured maxima and says nothing of a
+    step whose maximum is not a number (an overflowed gradient).  Reading:
+    such a step, which a training loop skips, does not enter the average, so
+    m_next is m_hat unchanged; otherwise one overflow would make every later
+    alpha NaN.
+
     Returns (codes, alpha, maxabs, m_next).
     """
     xf = to_float32(x, dtype).ravel()
@@ -211,7 +218,8 @@ def luq_quantize_hindsight(x, m_hat, dtype="f32", R=4, seed=0, counter=0, n_samp
             e = luq_fields(a_top, alpha, R, luq_uniforms(N, seed, counter, s))
             nib = e | np.where((e != 0) & np.signbit(xf), 8, 0).astype(np.uint8)
             codes[s] = pack_nibbles(nib)
-    return codes, alpha, maxabs, hindsight_update(maxabs, m, eta)
+    m_next = hindsight_update(maxabs, m, eta) if np.isfinite(maxabs) else np.float32(m_hat)
+    return codes, alpha, maxabs, m_next
 
 
 def luq_nibbles_range(xf, start, alpha, R, seed, counter, sample):

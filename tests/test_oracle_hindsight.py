@@ -75,6 +75,24 @@ def test_unbiased_below_the_estimated_top():
         assert abs(mi - xi) <= 5 * sd + (hi - lo) * 2.0 ** -16, (xi, mi)
 
 
+def test_overflow_step_inside_a_sequence_keeps_the_estimate():
+    """A run of steps with one overflowed gradient: the estimate after the
+    overflow equals the estimate before it, and the following finite steps
+    continue Eq. hindsight from there (alpha stays finite)."""
+    m = np.float32(1.0)
+    seq = []
+    for t in range(4):
+        x = synth.grad_1d(500, "f32", 0.1, seed=300 + t)
+        if t == 2:
+            x[17] = np.inf
+        _, a, mx, m_next = luq_quantize_hindsight(x, m, R=4, seed=0, counter=t)
+        seq.append((a, mx, m, m_next))
+        m = m_next
+    assert seq[2][3] == seq[2][2] and not np.isfinite(seq[2][1])
+    assert np.isfinite(seq[3][0]) and seq[3][0] == luq_alpha(seq[2][2], 4)
+    assert seq[3][3] == hindsight_update(seq[3][1], seq[3][2], 0.1)
+
+
 def test_update_rule_closed_form_and_sequence():
     # eta = 1/2 and powers of two: exact averages
     assert hindsight_update(np.float32(8.0), np.float32(4.0), 0.5) == np.float32(6.0)
@@ -110,6 +128,13 @@ def test_degenerate_estimates_and_inputs():
     codes, a, mx, m_next = luq_quantize_hindsight(y, np.float32(1.0), R=4)
     nib = unpack_nibbles(codes[0], y.size)
     assert nib[7] & 7 == 5 and nib[9] == 5 | 8
-    assert np.isnan(mx) and np.isnan(m_next)
+    # an overflowed step is not averaged into the estimate: it stays as it was
+    assert np.isnan(mx) and m_next == np.float32(1.0)
+    y[7] = 0.0
+    codes, a, mx, m_next = luq_quantize_hindsight(y, np.float32(0.5), R=4)
+    assert mx == np.float32(np.inf) and m_next == np.float32(0.5)
+    # a stored estimate that reads as 0 is kept as stored
+    _, _, _, m_next = luq_quantize_hindsight(y, np.float32(-3.0), R=4)
+    assert m_next == np.float32(-3.0)
     codes, a, mx, m_next = luq_quantize_hindsight(np.zeros(0, np.float32), np.float32(2.0), R=4)
     assert mx == 0 and m_next == hindsight_update(np.float32(0.0), np.float32(2.0), 0.1)
