@@ -15,13 +15,16 @@
  *    where noted.  The library never allocates or frees memory; it keeps no
  *    state between calls.
  *  - All work is enqueued asynchronously on `stream` (a hipStream_t; NULL is
- *    the null stream).  No call synchronizes with the host.
+ *    the null stream).  No call synchronizes with the host, except
+ *    luq_query_status.
  *  - Scales (alpha, s) live in device memory: no host round trip.
  *  - Argument errors are detected on the host, before anything is enqueued,
  *    and returned as a luq_status; nothing is launched in that case.
  *    luq_last_error() then holds a message (thread-local).
  *  - Data errors (a non-finite input element) are reported through the
- *    outputs: the scale becomes NaN and every code 0.
+ *    outputs (the scale becomes NaN and every code 0) and, asynchronously,
+ *    through a status word in the quantizer's workspace, which
+ *    luq_query_status reads (LUQ_ERR_NONFINITE).
  *  - Base pointers must be 16-byte aligned (LUQ_ERR_ALIGN otherwise).
  *
  * Code formats (two 4-bit codes per byte, element 2b in the low nibble)
@@ -47,7 +50,7 @@
 extern "C" {
 #endif
 
-#define LUQ_ABI_VERSION 6
+#define LUQ_ABI_VERSION 7
 
 typedef int luq_status;
 enum {
@@ -58,7 +61,9 @@ enum {
   LUQ_ERR_PARAM = 4,     /* R, n_samples or another parameter out of range   */
   LUQ_ERR_WORKSPACE = 5, /* workspace missing or smaller than required       */
   LUQ_ERR_ALIGN = 6,     /* a pointer is not 16-byte aligned                 */
-  LUQ_ERR_HIP = 7        /* the HIP runtime rejected a launch                */
+  LUQ_ERR_HIP = 7,       /* the HIP runtime rejected a launch or a copy      */
+  LUQ_ERR_NONFINITE = 8  /* (luq_query_status) the quantized tensor, or the
+                            in-hindsight estimate, was NaN or infinite       */
 };
 
 typedef enum { LUQ_F32 = 0, LUQ_BF16 = 1 } luq_dtype;
@@ -101,9 +106,32 @@ const char* luq_last_error(void);
 size_t luq_plane_bytes(int64_t n);
 
 /* Device workspace (bytes) an operation needs; 0 if none.  The workspace
- * holds per-block partial maxima (quantizers) or split-K partial sums
- * (GEMMs); its contents on entry do not matter. */
+ * holds per-block partial maxima and a status word (quantizers) or split-K
+ * partial sums (GEMMs); its contents on entry do not matter. */
 size_t luq_workspace_size(int op, int64_t d0, int64_t d1, int64_t d2);
+
+/*
+ * luq_query_status -- the data status of the last quantizer call
+ * (luq_quantize_grad, luq_quantize_grad_hindsight or int4_quantize) that
+ * used the workspace ws.  Alpha (Eq. alpha) and the INT4 scale (Appendix
+ * A.1) are defined only for a finite maximum; every such call writes, on
+ * the device and in stream order, whether its maximum was finite.
+ *
+ *  ws      the workspace passed to that call (device memory, 16-byte
+ *          aligned).
+ *  stream  the stream the call was enqueued on: the word is copied to the
+ *          host after it and the stream is synchronized (so this call may
+ *          not be captured into a HIP graph).
+ *
+ * Returns LUQ_OK (finite input), LUQ_ERR_NONFINITE (a NaN or infinite
+ * element; for luq_quantize_grad_hindsight also a NaN or infinite
+ * estimate), LUQ_ERR_NULL / LUQ_ERR_ALIGN for a bad ws, LUQ_ERR_HIP if the
+ * copy fails, or LUQ_ERR_WORKSPACE if ws holds no quantizer status (no
+ * quantizer has written it, or another operation reused it since).  An
+ * int4_quantize call with clip > 0 takes no maximum and writes LUQ_OK when
+ * it is given a workspace (none otherwise).
+ */
+luq_status luq_query_status(const void* ws, void* stream);
 
 /*
  * luq_quantize_grad -- LUQ of a neural-gradient tensor (Section 4).
@@ -139,9 +167,11 @@ size_t luq_workspace_size(int op, int64_t d0, int64_t d1, int64_t d2);
  *           [cols][rows] int8 sums (row stride rows bytes).  At least one of
  *           codes, codes_t.
  *  alpha    out: 1 float.  0 when max|g| = 0 (all codes 0); NaN when g has
- *           a non-finite element (all codes 0).
+ *           a non-finite element (all codes 0; luq_query_status then
+ *           returns LUQ_ERR_NONFINITE).
  *  maxabs   out: 1 float, max|g| (non-finite when g is), or NULL.
- *  ws       workspace of luq_workspace_size(LUQ_OP_QUANTIZE_GRAD, rows*cols).
+ *  ws       workspace of luq_workspace_size(LUQ_OP_QUANTIZE_GRAD, rows*cols)
+ *           (may be NULL when rows*cols = 0); receives the status word.
  */
 luq_status luq_quantize_grad(const void* g, luq_dtype dt, int64_t rows, int64_t cols, int R,
                              uint64_t seed, uint32_t counter, int n_samples, uint8_t* codes,
@@ -163,7 +193,10 @@ luq_status luq_quantize_grad(const void* g, luq_dtype dt, int64_t rows, int64_t 
  * tensor's maximum), and NaN elements, take the top code R + 1 with their
  * sign.  An estimate that is NaN or infinite gives alpha = NaN and all codes
  * 0; one that is 0 or negative gives alpha = 0 and all codes 0.  With
- * *state = max|g| the codes equal luq_quantize_grad's.  R may carry
+ * *state = max|g| the codes equal luq_quantize_grad's.  When max|g| is not
+ * finite (an overflowed step) *state is left unchanged, so the estimate
+ * survives the step; luq_query_status reports LUQ_ERR_NONFINITE for such a
+ * step and for a non-finite estimate.  R may carry
  * LUQ_ALPHA_PW2: alpha is then the power-of-two alpha of the estimate (the
  * appendix combines power-of-two LUQ with hindsight).
  *
@@ -193,7 +226,8 @@ luq_status luq_quantize_grad_hindsight(const void* g, luq_dtype dt, int64_t rows
  *  Q = 7 (signed, codes -7..7) or 15 (unsigned, codes 0..15).
  *  inv = fl32(Q / m), s = fl32(m / Q), q = clamp(rne(fl32(x * inv))), with a
  *  NaN product (0 * inf for tiny m) giving q = 0.  m = 0: s = 0, codes 0.
- *  Non-finite x (when clip <= 0): s = NaN, codes 0.
+ *  Non-finite x (when clip <= 0): s = NaN, codes 0 (luq_query_status:
+ *  LUQ_ERR_NONFINITE).
  *
  *  x        [rows][cols] row-major, dtype dt.  Shape rules as for
  *           luq_quantize_grad.
@@ -201,7 +235,7 @@ luq_status luq_quantize_grad_hindsight(const void* g, luq_dtype dt, int64_t rows
  *           NULL, not both).
  *  scale    out: 1 float s.
  *  ws       workspace of luq_workspace_size(LUQ_OP_INT4_QUANTIZE, rows*cols)
- *           (may be NULL when clip > 0).
+ *           (may be NULL when clip > 0); receives the status word.
  */
 luq_status int4_quantize(const void* x, luq_dtype dt, int64_t rows, int64_t cols, int is_signed,
                          float clip, uint8_t* codes, uint8_t* codes_t, float* scale, void* ws,

@@ -17,6 +17,7 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libluq.so")
 
 LUQ_OK = 0
+LUQ_ERR_NONFINITE = 8
 LUQ_F32, LUQ_BF16 = 0, 1
 ALPHA_PW2 = 0x100  # or-ed into R: power-of-two alpha
 SMP_SUM = 0x10     # or-ed into n_samples = 2: the two samples as int8 sums
@@ -24,7 +25,7 @@ OP_QUANTIZE_GRAD, OP_INT4_QUANTIZE, OP_GEMM_DGRAD, OP_GEMM_WGRAD, OP_GEMM_FWD, O
 
 EXPORTS = (
     "luq_abi_version", "luq_status_string", "luq_last_error", "luq_plane_bytes",
-    "luq_workspace_size", "luq_quantize_grad", "luq_quantize_grad_hindsight", "int4_quantize",
+    "luq_workspace_size", "luq_query_status", "luq_quantize_grad", "luq_quantize_grad_hindsight", "int4_quantize",
     "luq_gemm_dgrad", "luq_gemm_wgrad", "int4_gemm_fwd", "int4_im2col3x3_t", "luq_conv3x3_dgrad",
     "luq_conv3x3_wgrad",
 )
@@ -50,6 +51,8 @@ def _load():
     lib.luq_plane_bytes.argtypes = [i64]
     lib.luq_workspace_size.restype = sz
     lib.luq_workspace_size.argtypes = [i32, i64, i64, i64]
+    lib.luq_query_status.restype = i32
+    lib.luq_query_status.argtypes = [vp, vp]
     lib.luq_quantize_grad.restype = i32
     lib.luq_quantize_grad.argtypes = [vp, i32, i64, i64, i32, u64, u32, i32, vp, vp, vp, vp, vp, sz, vp]
     lib.luq_quantize_grad_hindsight.restype = i32
@@ -107,6 +110,16 @@ def plane_bytes(n):
 
 def workspace_size(op, d0, d1=0, d2=0):
     return int(LIB.luq_workspace_size(op, d0, d1, d2))
+
+
+def query_status(ws):
+    """Status of the last quantizer call that used the workspace tensor ws
+    (synchronizes torch's current stream): LUQ_OK or LUQ_ERR_NONFINITE;
+    raises LuqError for anything else."""
+    st = LIB.luq_query_status(_ptr(ws), _stream(ws.device))
+    if st not in (LUQ_OK, LUQ_ERR_NONFINITE):
+        _check(st, "luq_query_status")
+    return st
 
 
 def _bytes(n, dev):

@@ -61,11 +61,30 @@ const char* luq_status_string(luq_status s) {
     case LUQ_ERR_WORKSPACE: return "workspace missing or too small";
     case LUQ_ERR_ALIGN: return "pointer not 16-byte aligned";
     case LUQ_ERR_HIP: return "HIP runtime error";
+    case LUQ_ERR_NONFINITE: return "input tensor has a non-finite element";
     default: return "unknown status";
   }
 }
 
 const char* luq_last_error(void) { return g_last_error; }
+
+luq_status luq_query_status(const void* ws, void* stream) {
+  g_last_error[0] = 0;
+  if (!ws) return fail(LUQ_ERR_NULL, "%s: ws is NULL", "luq_query_status");
+  if (!aligned16(ws)) return fail(LUQ_ERR_ALIGN, "%s: ws must be 16-byte aligned", "luq_query_status");
+  const hipStream_t st = static_cast<hipStream_t>(stream);
+  uint32_t word = 0;
+  hipError_t e = hipMemcpyAsync(&word, static_cast<const uint8_t*>(ws) + luq::quant_status_offset(),
+                                sizeof(word), hipMemcpyDeviceToHost, st);
+  if (e == hipSuccess) e = hipStreamSynchronize(st);
+  if (e != hipSuccess) return hip_status(e);
+  if ((word & luq::kStatusTagMask) != luq::kStatusTag)
+    return fail(LUQ_ERR_WORKSPACE, "%s: the workspace holds no quantizer status", "luq_query_status");
+  const luq_status s = (luq_status)(word & 0xFFFFu);
+  if (s == LUQ_ERR_NONFINITE) return fail(LUQ_ERR_NONFINITE, "%s: the last quantized tensor was not finite",
+                                          "luq_query_status");
+  return s;
+}
 
 size_t luq_plane_bytes(int64_t n) { return n <= 0 ? 0 : luq::plane_bytes(n); }
 

@@ -19,6 +19,12 @@ inline size_t plane_bytes(int64_t n) {
 }
 
 size_t quant_workspace_bytes(int64_t n);
+// Byte offset, in a quantizer's workspace, of the status word of its last
+// call: kStatusTag | luq_status, so that a word no quantizer wrote is told
+// apart.
+size_t quant_status_offset();
+constexpr uint32_t kStatusTag = 0x4C510000u;
+constexpr uint32_t kStatusTagMask = 0xFFFF0000u;
 
 hipError_t launch_luq_quantize(const void* g, int bf16, int64_t rows, int64_t cols, int R, int pw2,
                                uint64_t seed, uint32_t counter, int ns, uint8_t* codes,

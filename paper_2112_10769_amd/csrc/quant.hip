@@ -34,6 +34,10 @@ constexpr int kThreads = 256;
 constexpr int kDirectPartials = 2048;
 constexpr int kMaxPartials = 16384;
 constexpr int kMaxEncodeBlocks = 4096;
+// Word of the quantizer workspace after the partials and their fold: the
+// status of the last call (kStatusTag | LUQ_OK or LUQ_ERR_NONFINITE).
+constexpr int kStatusWord = kMaxPartials + 1;
+constexpr uint32_t kStatusNonfinite = 8;  // LUQ_ERR_NONFINITE
 // Tensors above kCacheBytes (the 256 MB last-level cache) are streamed: the
 // max pass reads all but the last kKeepBytes of them non-temporally and the
 // encode pass, whose loads and code stores are then non-temporal too, walks
@@ -451,6 +455,7 @@ struct LuqArgs {
   // maximum per encode block written at the end
   const float* state;
   uint32_t* part_out;
+  uint32_t* status;  // status word, or null
 };
 
 // Key of the in-hindsight estimate: NaN stays NaN, anything not positive is 0.
@@ -469,6 +474,7 @@ __device__ __forceinline__ LuqParams luq_block_params(const LuqArgs& a) {
   if (!HS && blockIdx.x == 0 && threadIdx.x == 0) {
     *a.alpha_out = alpha;
     if (a.max_out) *a.max_out = __uint_as_float(mbits);
+    if (a.status) *a.status = kStatusTag | (mbits >= 0x7F800000u ? kStatusNonfinite : 0u);
   }
   return p;
 }
@@ -608,10 +614,14 @@ __global__ __launch_bounds__(kThreads) void luq_encode_tile_kernel(LuqArgs a, in
 // In-hindsight fold, after the encode: the measured maximum (from the encode
 // blocks' partials), alpha of this step (from the estimate the encode read)
 // and the next estimate, Eq. hindsight: m' = fl32(fl32(c1 max) + fl32(c0 m))
-// with c1 = fl32(1 - eta), c0 = eta.
+// with c1 = fl32(1 - eta), c0 = eta.  A step whose measured maximum is not
+// finite (an overflowed gradient) leaves the estimate as it was, so that one
+// such step does not make every later alpha NaN; it reports
+// LUQ_ERR_NONFINITE, as does a non-finite estimate.
 __global__ __launch_bounds__(1024) void hindsight_fold_kernel(const uint32_t* __restrict__ part, int nparts,
                                                              float* state, float c1, float c0, int R,
-                                                             bool pw2, float* alpha_out, float* maxabs_out) {
+                                                             bool pw2, float* alpha_out, float* maxabs_out,
+                                                             uint32_t* status) {
   __shared__ uint32_t scratch[1024 / kWave];
   const uint32_t m = reduce_partials(part, nparts, scratch);
   if (threadIdx.x == 0) {
@@ -621,13 +631,17 @@ __global__ __launch_bounds__(1024) void hindsight_fold_kernel(const uint32_t* __
     const float mx = __uint_as_float(m);
     *alpha_out = alpha;
     if (maxabs_out) *maxabs_out = mx;
-    *state = __fadd_rn(__fmul_rn(c1, mx), __fmul_rn(c0, __uint_as_float(mkey)));
+    const bool measured_ok = m < 0x7F800000u;
+    if (measured_ok) *state = __fadd_rn(__fmul_rn(c1, mx), __fmul_rn(c0, __uint_as_float(mkey)));
+    if (status) *status = kStatusTag | (measured_ok && mkey < 0x7F800000u ? 0u : kStatusNonfinite);
   }
 }
 
-__global__ void write_two_floats_kernel(float* a, float va, float* b, float vb) {
+// Empty tensors: the scalar outputs and the status word (when given).
+__global__ void write_two_floats_kernel(float* a, float va, float* b, float vb, uint32_t* status) {
   if (a) *a = va;
   if (b) *b = vb;
+  if (status) *status = kStatusTag;
 }
 
 // ------------------------------- INT4 --------------------------------------
@@ -648,6 +662,7 @@ struct Int4Args {
   uint8_t* codes;
   uint8_t* codes_t;
   float* scale_out;
+  uint32_t* status;  // status word, or null
 };
 
 // Scale and rounding parameters from the range: clip when positive, else the
@@ -678,7 +693,10 @@ __device__ __forceinline__ Int4Params int4_params(const Int4Args& a, uint32_t mb
   }
   p.lo = a.is_signed ? -7.0f : 0.0f;
   p.hi = Q;
-  if (blockIdx.x == 0 && threadIdx.x == 0) *a.scale_out = s;
+  if (blockIdx.x == 0 && threadIdx.x == 0) {
+    *a.scale_out = s;
+    if (a.status) *a.status = kStatusTag | (nonfinite ? kStatusNonfinite : 0u);
+  }
   return p;
 }
 
@@ -809,7 +827,10 @@ static int max_pass_blocks(int64_t n) {
   return (int)b;
 }
 
-size_t quant_workspace_bytes(int64_t /*n*/) { return (kMaxPartials + 1) * sizeof(uint32_t); }
+// partials, their fold and the status word
+size_t quant_workspace_bytes(int64_t /*n*/) { return (kStatusWord + 1) * sizeof(uint32_t); }
+
+size_t quant_status_offset() { return kStatusWord * sizeof(uint32_t); }
 
 static int encode_blocks_flat(int64_t n) {
   const int64_t groups = (n + 7) >> 3;
@@ -925,8 +946,9 @@ hipError_t launch_luq_quantize(const void* g, int bf16, int64_t rows, int64_t co
                                uint8_t* codes_t, float* alpha, float* maxabs, void* ws,
                                hipStream_t st) {
   const int64_t n = rows * cols;
+  uint32_t* status = ws ? static_cast<uint32_t*>(ws) + kStatusWord : nullptr;
   if (n == 0) {
-    hipLaunchKernelGGL(write_two_floats_kernel, dim3(1), dim3(1), 0, st, alpha, 0.0f, maxabs, 0.0f);
+    hipLaunchKernelGGL(write_two_floats_kernel, dim3(1), dim3(1), 0, st, alpha, 0.0f, maxabs, 0.0f, status);
     return hipGetLastError();
   }
   LuqArgs a;
@@ -946,6 +968,9 @@ hipError_t launch_luq_quantize(const void* g, int bf16, int64_t rows, int64_t co
   a.plane = (int64_t)plane_bytes(n);
   a.alpha_out = alpha;
   a.max_out = maxabs;
+  a.state = nullptr;
+  a.part_out = nullptr;
+  a.status = status;
   return bf16 ? luq_launch_t<true>(a, ns, a.nparts, st) : luq_launch_t<false>(a, ns, a.nparts, st);
 }
 
@@ -973,6 +998,7 @@ hipError_t launch_luq_quantize_hindsight(const void* g, int bf16, int64_t rows, 
   a.max_out = maxabs;
   a.state = state;
   a.part_out = static_cast<uint32_t*>(ws);
+  a.status = nullptr;  // written by the fold
   int nblocks = 0;
   if (n > 0) {
     const bool nt = stream_reads(n, bf16 != 0);
@@ -981,7 +1007,8 @@ hipError_t launch_luq_quantize_hindsight(const void* g, int bf16, int64_t rows, 
                          : luq_encode_launch<false, false, true>(a, ns, st));
   }
   hipLaunchKernelGGL(hindsight_fold_kernel, dim3(1), dim3(1024), 0, st, a.part_out, nblocks, state,
-                     1.0f - eta, eta, R, pw2 != 0, alpha, maxabs);  // c1 = fl32(1 - eta) (host float arithmetic)
+                     1.0f - eta, eta, R, pw2 != 0, alpha, maxabs,
+                     ws ? static_cast<uint32_t*>(ws) + kStatusWord : nullptr);  // c1 = fl32(1 - eta) (host float arithmetic)
   return hipGetLastError();
 }
 
@@ -1023,9 +1050,10 @@ hipError_t launch_int4_quantize(const void* x, int bf16, int64_t rows, int64_t c
                                 float clip, uint8_t* codes, uint8_t* codes_t, float* scale,
                                 void* ws, hipStream_t st) {
   const int64_t n = rows * cols;
+  uint32_t* status = ws ? static_cast<uint32_t*>(ws) + kStatusWord : nullptr;
   if (n == 0) {
     hipLaunchKernelGGL(write_two_floats_kernel, dim3(1), dim3(1), 0, st, scale, 0.0f,
-                       (float*)nullptr, 0.0f);
+                       (float*)nullptr, 0.0f, status);
     return hipGetLastError();
   }
   Int4Args a;
@@ -1040,6 +1068,7 @@ hipError_t launch_int4_quantize(const void* x, int bf16, int64_t rows, int64_t c
   a.codes = codes;
   a.codes_t = codes_t;
   a.scale_out = scale;
+  a.status = status;
   return bf16 ? int4_launch_t<true>(a, st) : int4_launch_t<false>(a, st);
 }
 

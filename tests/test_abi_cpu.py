@@ -32,7 +32,7 @@ def _declared():
 
 def test_every_declared_function_is_exported():
     names = _declared()
-    assert len(names) == 14, names
+    assert len(names) == 15, names
     for n in names:
         assert hasattr(LIB, n), n
     assert set(names) == set(luq.EXPORTS)
@@ -41,8 +41,9 @@ def test_every_declared_function_is_exported():
 def test_version_and_strings():
     v = int(re.search(r"#define LUQ_ABI_VERSION (\d+)", open(HEADER).read()).group(1))
     assert LIB.luq_abi_version() == v
-    for s in range(8):
+    for s in range(9):
         assert LIB.luq_status_string(s)
+    assert b"non-finite" in LIB.luq_status_string(8)
     assert LIB.luq_status_string(99) == b"unknown status"
 
 
@@ -251,3 +252,40 @@ def test_conv_wgrad_validation(kw, status):
 def test_conv_wgrad_workspace():
     assert luq.workspace_size(luq.OP_CONV_WGRAD, 64 * 56 * 56, 64, 64) > 0
     assert luq.workspace_size(luq.OP_CONV_WGRAD, 0, 64, 64) == 0
+
+
+def test_query_status_rejects_bad_workspace_on_the_host():
+    """Null and misaligned workspaces are refused before any HIP call."""
+    assert LIB.luq_query_status(NUL, None) == 1
+    assert LIB.luq_query_status(PMIS, None) == 6
+    assert luq.LUQ_ERR_NONFINITE == 8
+
+
+def test_quantizer_workspace_holds_the_status_word():
+    """The status word sits after the 16384 partials and their fold."""
+    assert luq.workspace_size(luq.OP_QUANTIZE_GRAD, 1) == (16384 + 2) * 4
+    assert luq.workspace_size(luq.OP_INT4_QUANTIZE, 1 << 30) == (16384 + 2) * 4
+
+
+@pytest.mark.parametrize("T,C,Cout", [
+    (200704, 64, 64),            # the ResNet-50 layer
+    (1 << 20, 384, 384),         # many channel tiles, few splits
+    (1 << 20, 64, 64),
+    (1 << 22, 64, 64),
+    (1 << 24, 256, 512),
+    (1 << 29, 8, 8),
+])
+def test_conv_wgrad_plan_keeps_int32_sums_exact(T, C, Cout):
+    """The weight gradient's workgroups sum their pixel ranges in int32: for
+    the largest terms (LUQ 2^6 -- R = 6, or two R = 5 samples -- times the
+    INT4 carrier 8 * 15) the pixels one workgroup sums must stay below
+    2^31 / 7680.  The split count comes from the workspace the plan asks for
+    (one [Cout][9C] int32 slab per split); a workgroup then sums at most
+    ceil(ranges / splits) ranges of 2 * lg <= 2560 pixels, i.e. fewer than
+    T / splits + 2 * 2560 pixels."""
+    ws = luq.workspace_size(luq.OP_CONV_WGRAD, T, C, Cout)
+    slab = Cout * 9 * C * 4
+    assert ws % slab == 0
+    nsplit = max(ws // slab, 1)
+    worst_pixels = T / nsplit + 2 * 2560
+    assert worst_pixels * 64 * 120 < 2 ** 31, (nsplit, worst_pixels)
