@@ -380,7 +380,11 @@ constexpr int kWgWin = kWgBK + 32;                         // activation window 
 constexpr int kWgBPitch = kWgWin + 4;                      // an odd number of dwords
 constexpr int kWgStage = 3 * kWgGCopy + 64 * kWgBPitch;
 constexpr int kWgMaxLg = 1280;                             // pixels per wave group and range
-constexpr int64_t kWgMaxWgPixels = (int64_t)1 << 19;       // pixels one workgroup sums in int32
+// Pixels one workgroup sums in int32 (both wave groups together).  A term is
+// at most 64 * 120 in magnitude: LUQ values up to 2^6 (R = 6, or the sum of
+// two R = 5 samples) times INT4 carriers up to 8 * 15 or 16 * 7, and
+// 2^18 * 7680 < 2^31.
+constexpr int64_t kWgMaxWgPixels = (int64_t)1 << 18;
 constexpr int kWgFar = 1 << 30;                            // a stage start past every image (T <= 2^29)
 static_assert(kWgKG * 2 * kWgStage + 3 * kWgKG * kWgMaxLg <= 160 * 1024, "LDS");
 
@@ -780,7 +784,7 @@ static ConvWgPlan plan_conv_wgrad(int64_t T, int64_t C, int64_t Cout) {
   if (lg > kWgMaxLg) lg = kWgMaxLg;
   const int64_t nranges = (T + kWgKG * lg - 1) / (kWgKG * lg);
   // each workgroup sums at most kWgMaxWgPixels pixels, so its int32 sums
-  // cannot overflow (|term| <= 32 * 8 * 15 or 32 * 16 * 7)
+  // cannot overflow (|term| <= 64 * 120)
   const int64_t per = kWgMaxWgPixels / (kWgKG * lg);
   int64_t nsplit = want;
   if (nsplit < (nranges + per - 1) / per) nsplit = (nranges + per - 1) / per;

@@ -149,17 +149,17 @@ def test_conv_dgrad_resnet_layer_whole_output(L):
 from oracle.conv import conv3x3_wgrad_ref  # noqa: E402
 
 
-def _wgrad_case(L, B, H, W, C, Cout, ns=1, asig=False, seed=0):
+def _wgrad_case(L, B, H, W, C, Cout, ns=1, asig=False, seed=0, R=4):
     T = B * H * W
     g = synth.lognormal_grad((T, Cout), -12.0, 2.5, 0.5, [seed, 1])
     a = synth.normal((T, C), 1.0, [seed, 2]) if asig else synth.half_normal((T, C), [seed, 2])
-    announce("conv3x3_wgrad", dict(B=B, H=H, W=W, C=C, Cout=Cout, ns=ns, asig=asig, seed=seed))
+    announce("conv3x3_wgrad", dict(B=B, H=H, W=W, C=C, Cout=Cout, ns=ns, asig=asig, seed=seed, R=R))
     gd, ad = to_dev(g), to_dev(a)
     if T % 8 == 0 and Cout % 8 == 0 and C % 8 == 0:
-        _, gct, alpha, _ = L.luq_quantize_grad(gd, R=4, seed=seed, counter=6, n_samples=ns, codes=False, codes_t=True)
+        _, gct, alpha, _ = L.luq_quantize_grad(gd, R=R, seed=seed, counter=6, n_samples=ns, codes=False, codes_t=True)
         _, act, sa = L.int4_quantize(ad, is_signed=asig, codes=False, codes_t=True)
     else:  # row-major codes transposed on the host (the quantizers' codes_t needs multiples of 8)
-        gc, _, alpha, _ = L.luq_quantize_grad(gd, R=4, seed=seed, counter=6, n_samples=ns)
+        gc, _, alpha, _ = L.luq_quantize_grad(gd, R=R, seed=seed, counter=6, n_samples=ns)
         gch = host(gc)
         gct = to_dev(np.stack([transpose_codes(gch[s], T, Cout) for s in range(ns)]).reshape(ns, -1))
         ac, _, sa = L.int4_quantize(ad, is_signed=asig)
@@ -170,7 +170,7 @@ def _wgrad_case(L, B, H, W, C, Cout, ns=1, asig=False, seed=0):
         gct = pad
     dw = host(L.luq_conv3x3_wgrad(gct, alpha, act, sa, asig, B, H, W, C, Cout, n_samples=ns))
     assert dw.shape == (Cout, 9 * C)
-    rc, ra, _ = oluq.luq_quantize(g, R=4, seed=seed, counter=6, n_samples=ns)
+    rc, ra, _ = oluq.luq_quantize(g, R=R, seed=seed, counter=6, n_samples=ns)
     rac, rsa = oint4.int4_quantize(a, is_signed=asig)
     assert host(alpha)[0].tobytes() == np.float32(ra).tobytes()
     assert host(sa)[0].tobytes() == np.float32(rsa).tobytes()
@@ -199,6 +199,45 @@ def _wgrad_case(L, B, H, W, C, Cout, ns=1, asig=False, seed=0):
 @pytest.mark.parametrize("ns", [1, 2])
 def test_conv_wgrad_parity(L, B, H, W, C, Cout, ns):
     _wgrad_case(L, B, H, W, C, Cout, ns=ns, seed=B * 1000 + H * 100 + W + C + Cout)
+
+
+@pytest.mark.parametrize("R,ns", [(6, 1), (5, 2)])
+@pytest.mark.parametrize("B,H,W,C,Cout", [(4, 14, 16, 64, 64), (16, 28, 28, 64, 64)])
+def test_conv_wgrad_parity_wide_levels(L, B, H, W, C, Cout, R, ns):
+    """Codes whose values reach 2^6: R = 6, or the sum of two R = 5 samples."""
+    _wgrad_case(L, B, H, W, C, Cout, ns=ns, R=R, seed=B * 7 + R)
+
+
+@pytest.mark.parametrize("R,ns", [(6, 1), (5, 2)])
+def test_conv_wgrad_largest_terms_many_pixels(L, R, ns):
+    """Every term at its largest magnitude, 64 * 120 in carrier units (a
+    constant gradient puts every element on the top LUQ level, 2^6 in units
+    of alpha for R = 6 and for the sum of two R = 5 samples; a constant
+    activation gives the top unsigned INT4 code 15, carried as 8 * 15), over
+    2^20 pixels and 6 x 6 channel tiles, so that few workgroups each sum
+    long pixel ranges.  The exact result has a closed form: tap (kh, kw)
+    gathers B (H - |kh - 1|) (W - |kw - 1|) products 2^6 * 15 in value units."""
+    B, H, W, C, Co = 16, 256, 256, 384, 384
+    T = B * H * W
+    announce("conv3x3_wgrad largest terms", dict(T=T, C=C, Cout=Co, R=R, ns=ns))
+    g = torch.full((T, Co), 1.0, dtype=torch.float32, device="cuda:0")
+    _, gct, alpha, _ = L.luq_quantize_grad(g, R=R, n_samples=ns, codes=False, codes_t=True)
+    del g
+    a = torch.full((T, C), 0.75, dtype=torch.float32, device="cuda:0")
+    _, act, sa = L.int4_quantize(a, is_signed=False, codes=False, codes_t=True)
+    del a
+    dw = host(L.luq_conv3x3_wgrad(gct, alpha, act, sa, False, B, H, W, C, Co, n_samples=ns))
+    al, s_a = host(alpha)[0], host(sa)[0]
+    assert al == np.float32(2.0 ** -R) and s_a == np.float32(np.float32(0.75) / np.float32(15))
+    # the kernels' epilogue on the exact carrier sums: fl32(fl32(acc) * fl32(fl32(alpha / ns) * s_a) * 2^-3)
+    sc = np.float32(np.float32(np.float32(al) * np.float32(1.0 / ns)) * s_a) * np.float32(0.125)
+    for kh in range(3):
+        for kw in range(3):
+            count = B * (H - abs(kh - 1)) * (W - abs(kw - 1))
+            acc = count * 64 * 120  # two samples of 2^5 add up to 2^6 per element as well
+            want = np.float32(np.float32(acc) * sc)
+            block = dw[:, (kh * 3 + kw) * C:(kh * 3 + kw + 1) * C]
+            assert np.all(block == want), (kh, kw, np.unique(block)[:4], want)
 
 
 def test_conv_wgrad_signed_activations(L):
