@@ -50,7 +50,7 @@
 extern "C" {
 #endif
 
-#define LUQ_ABI_VERSION 7
+#define LUQ_ABI_VERSION 8
 
 typedef int luq_status;
 enum {
@@ -177,6 +177,32 @@ luq_status luq_quantize_grad(const void* g, luq_dtype dt, int64_t rows, int64_t 
                              uint64_t seed, uint32_t counter, int n_samples, uint8_t* codes,
                              uint8_t* codes_t, float* alpha, float* maxabs, void* ws,
                              size_t ws_bytes, void* stream);
+
+/*
+ * luq_quantize_grad_noalloc -- luq_quantize_grad for callers that cannot
+ * allocate device memory (code being captured into a HIP graph, tight
+ * serving loops, hosts that forbid allocation): the same codes, alpha and
+ * maxabs, bit for bit, with the workspace taken from a static device array
+ * inside the library instead of a caller's buffer.  The caller still passes
+ * the input and the outputs; the call allocates and frees nothing.
+ *
+ *  Arguments as for luq_quantize_grad, without ws and ws_bytes.
+ *  Scratch: one array of luq_workspace_size(LUQ_OP_QUANTIZE_GRAD, n) bytes
+ *           (65544: 16384 partial maxima, their fold and a status word; the
+ *           same for every n) per GPU the library runs on, held until the
+ *           process ends.  A size whose workspace exceeded it would be
+ *           refused with LUQ_ERR_SHAPE.
+ *  Every call on one GPU uses that GPU's array, which keeps the last call's
+ *  contents (nothing in it needs to start at zero): calls that overlap in
+ *  time on one GPU (other streams, other host threads) race and must be
+ *  ordered by the caller.  The status word it writes is not reachable
+ *  through luq_query_status; a non-finite input shows as alpha = NaN.
+ *  Errors as for luq_quantize_grad, plus LUQ_ERR_HIP when the array's
+ *  device address cannot be found on the current device.
+ */
+luq_status luq_quantize_grad_noalloc(const void* g, luq_dtype dt, int64_t rows, int64_t cols, int R,
+                                     uint64_t seed, uint32_t counter, int n_samples, uint8_t* codes,
+                                     uint8_t* codes_t, float* alpha, float* maxabs, void* stream);
 
 /*
  * luq_quantize_grad_hindsight -- LUQ in one pass over g with the

@@ -25,7 +25,7 @@ OP_QUANTIZE_GRAD, OP_INT4_QUANTIZE, OP_GEMM_DGRAD, OP_GEMM_WGRAD, OP_GEMM_FWD, O
 
 EXPORTS = (
     "luq_abi_version", "luq_status_string", "luq_last_error", "luq_plane_bytes",
-    "luq_workspace_size", "luq_query_status", "luq_quantize_grad", "luq_quantize_grad_hindsight", "int4_quantize",
+    "luq_workspace_size", "luq_query_status", "luq_quantize_grad", "luq_quantize_grad_noalloc", "luq_quantize_grad_hindsight", "int4_quantize",
     "luq_gemm_dgrad", "luq_gemm_wgrad", "int4_gemm_fwd", "int4_im2col3x3_t", "luq_conv3x3_dgrad",
     "luq_conv3x3_wgrad",
 )
@@ -55,6 +55,8 @@ def _load():
     lib.luq_query_status.argtypes = [vp, vp]
     lib.luq_quantize_grad.restype = i32
     lib.luq_quantize_grad.argtypes = [vp, i32, i64, i64, i32, u64, u32, i32, vp, vp, vp, vp, vp, sz, vp]
+    lib.luq_quantize_grad_noalloc.restype = i32
+    lib.luq_quantize_grad_noalloc.argtypes = [vp, i32, i64, i64, i32, u64, u32, i32, vp, vp, vp, vp, vp]
     lib.luq_quantize_grad_hindsight.restype = i32
     lib.luq_quantize_grad_hindsight.argtypes = [vp, i32, i64, i64, i32, u64, u32, i32, f32, vp, vp, vp, vp, vp, vp,
                                                 sz, vp]
@@ -167,6 +169,20 @@ def luq_quantize_grad(g, R=4, seed=0, counter=0, n_samples=1, codes=True, codes_
                                _ptr(codes), _ptr(codes_t), _ptr(alpha), _ptr(maxabs), _ptr(ws),
                                ws.numel(), _stream(dev))
     _check(st, "luq_quantize_grad")
+    return codes, codes_t, alpha, maxabs
+
+
+def luq_quantize_grad_noalloc(g, codes, codes_t, alpha, maxabs=None, R=4, seed=0, counter=0, n_samples=1,
+                              pw2=False):
+    """luq_quantize_grad with the library's static scratch instead of a
+    workspace: the caller passes every output buffer (codes / codes_t may be
+    None), and nothing is allocated.  Returns (codes, codes_t, alpha, maxabs)."""
+    rows, cols = _shape2d(g)
+    n = rows * cols
+    st = LIB.luq_quantize_grad_noalloc(_ptr(g) if n else None, _dtype(g), rows, cols, R | (ALPHA_PW2 if pw2 else 0),
+                                       seed & (2**64 - 1), counter & 0xFFFFFFFF, n_samples, _ptr(codes),
+                                       _ptr(codes_t), _ptr(alpha), _ptr(maxabs), _stream(g.device))
+    _check(st, "luq_quantize_grad_noalloc")
     return codes, codes_t, alpha, maxabs
 
 

@@ -109,35 +109,64 @@ size_t luq_workspace_size(int op, int64_t d0, int64_t d1, int64_t d2) {
   }
 }
 
+// Checks of luq_quantize_grad's arguments other than the workspace; R loses
+// the LUQ_ALPHA_PW2 flag, which goes to *pw2.
+static luq_status quantize_grad_checks(const char* fn, const void* g, luq_dtype dt, int64_t rows, int64_t cols,
+                                       int* R, int* pw2, int n_samples, const uint8_t* codes,
+                                       const uint8_t* codes_t, const float* alpha, const float* maxabs) {
+  if (dt != LUQ_F32 && dt != LUQ_BF16) return fail(LUQ_ERR_DTYPE, "%s: dtype", fn);
+  luq_status st = check_matrix(rows, cols, codes_t != nullptr, fn);
+  if (st != LUQ_OK) return st;
+  *pw2 = (*R & LUQ_ALPHA_PW2) ? 1 : 0;
+  *R &= ~LUQ_ALPHA_PW2;
+  if (*R < 4 || *R > 6) return fail(LUQ_ERR_PARAM, "%s: R must be 4, 5 or 6", fn);
+  st = check_samples(n_samples, *R, fn);
+  if (st != LUQ_OK) return st;
+  if (!alpha) return fail(LUQ_ERR_NULL, "%s: alpha is NULL", fn);
+  if (rows * cols > 0) {
+    if (!g) return fail(LUQ_ERR_NULL, "%s: g is NULL", fn);
+    if (!codes && !codes_t) return fail(LUQ_ERR_NULL, "%s: no code output", fn);
+    if (!aligned16(g) || !aligned16(codes) || !aligned16(codes_t))
+      return fail(LUQ_ERR_ALIGN, "%s: g, codes and codes_t must be 16-byte aligned", fn);
+  }
+  if (!aligned4(alpha) || !aligned4(maxabs)) return fail(LUQ_ERR_ALIGN, "%s: alpha / maxabs misaligned", fn);
+  return LUQ_OK;
+}
+
 luq_status luq_quantize_grad(const void* g, luq_dtype dt, int64_t rows, int64_t cols, int R,
                              uint64_t seed, uint32_t counter, int n_samples, uint8_t* codes,
                              uint8_t* codes_t, float* alpha, float* maxabs, void* ws,
                              size_t ws_bytes, void* stream) {
+  const char* fn = "luq_quantize_grad";
   g_last_error[0] = 0;
-  if (dt != LUQ_F32 && dt != LUQ_BF16) return fail(LUQ_ERR_DTYPE, "%s: dtype", "luq_quantize_grad");
-  luq_status st = check_matrix(rows, cols, codes_t != nullptr, "luq_quantize_grad");
+  int pw2 = 0;
+  const luq_status st = quantize_grad_checks(fn, g, dt, rows, cols, &R, &pw2, n_samples, codes, codes_t, alpha,
+                                             maxabs);
   if (st != LUQ_OK) return st;
-  const int pw2 = (R & LUQ_ALPHA_PW2) ? 1 : 0;
-  R &= ~LUQ_ALPHA_PW2;
-  if (R < 4 || R > 6) return fail(LUQ_ERR_PARAM, "%s: R must be 4, 5 or 6", "luq_quantize_grad");
-  st = check_samples(n_samples, R, "luq_quantize_grad");
-  if (st != LUQ_OK) return st;
-  if (!alpha) return fail(LUQ_ERR_NULL, "%s: alpha is NULL", "luq_quantize_grad");
-  const int64_t n = rows * cols;
-  if (n > 0) {
-    if (!g) return fail(LUQ_ERR_NULL, "%s: g is NULL", "luq_quantize_grad");
-    if (!codes && !codes_t) return fail(LUQ_ERR_NULL, "%s: no code output", "luq_quantize_grad");
-    if (!ws || ws_bytes < luq_workspace_size(LUQ_OP_QUANTIZE_GRAD, n, 0, 0))
-      return fail(LUQ_ERR_WORKSPACE, "%s: workspace too small", "luq_quantize_grad");
-    if (!aligned16(g) || !aligned16(codes) || !aligned16(codes_t) || !aligned16(ws))
-      return fail(LUQ_ERR_ALIGN, "%s: g, codes, codes_t and ws must be 16-byte aligned",
-                  "luq_quantize_grad");
+  if (rows * cols > 0) {
+    if (!ws || ws_bytes < luq_workspace_size(LUQ_OP_QUANTIZE_GRAD, rows * cols, 0, 0))
+      return fail(LUQ_ERR_WORKSPACE, "%s: workspace too small", fn);
+    if (!aligned16(ws)) return fail(LUQ_ERR_ALIGN, "%s: ws must be 16-byte aligned", fn);
   }
-  if (!aligned4(alpha) || !aligned4(maxabs))
-    return fail(LUQ_ERR_ALIGN, "%s: alpha / maxabs misaligned", "luq_quantize_grad");
   return hip_status(luq::launch_luq_quantize(g, dt == LUQ_BF16, rows, cols, R, pw2, seed, counter,
                                              n_samples, codes, codes_t, alpha, maxabs, ws,
                                              static_cast<hipStream_t>(stream)));
+}
+
+luq_status luq_quantize_grad_noalloc(const void* g, luq_dtype dt, int64_t rows, int64_t cols, int R,
+                                     uint64_t seed, uint32_t counter, int n_samples, uint8_t* codes,
+                                     uint8_t* codes_t, float* alpha, float* maxabs, void* stream) {
+  const char* fn = "luq_quantize_grad_noalloc";
+  g_last_error[0] = 0;
+  int pw2 = 0;
+  const luq_status st = quantize_grad_checks(fn, g, dt, rows, cols, &R, &pw2, n_samples, codes, codes_t, alpha,
+                                             maxabs);
+  if (st != LUQ_OK) return st;
+  if (luq_workspace_size(LUQ_OP_QUANTIZE_GRAD, rows * cols, 0, 0) > luq::noalloc_scratch_bytes())
+    return fail(LUQ_ERR_SHAPE, "%s: the tensor needs more scratch than the library's static array holds", fn);
+  return hip_status(luq::launch_luq_quantize_noalloc(g, dt == LUQ_BF16, rows, cols, R, pw2, seed, counter,
+                                                     n_samples, codes, codes_t, alpha, maxabs,
+                                                     static_cast<hipStream_t>(stream)));
 }
 
 luq_status luq_quantize_grad_hindsight(const void* g, luq_dtype dt, int64_t rows, int64_t cols, int R,

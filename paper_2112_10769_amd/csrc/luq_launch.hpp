@@ -31,6 +31,13 @@ hipError_t launch_luq_quantize(const void* g, int bf16, int64_t rows, int64_t co
                                uint8_t* codes_t, float* alpha, float* maxabs, void* ws,
                                hipStream_t st);
 
+// luq_quantize_grad with its workspace in the library's per-device static
+// scratch array (no allocation); noalloc_scratch_bytes() is that array's size.
+size_t noalloc_scratch_bytes();
+hipError_t launch_luq_quantize_noalloc(const void* g, int bf16, int64_t rows, int64_t cols, int R, int pw2,
+                                       uint64_t seed, uint32_t counter, int ns, uint8_t* codes, uint8_t* codes_t,
+                                       float* alpha, float* maxabs, hipStream_t st);
+
 hipError_t launch_luq_quantize_hindsight(const void* g, int bf16, int64_t rows, int64_t cols, int R, int pw2,
                                          uint64_t seed, uint32_t counter, int ns, float eta, uint8_t* codes,
                                          uint8_t* codes_t, float* state, float* alpha, float* maxabs, void* ws,

@@ -22,6 +22,8 @@
 //
 // The "tile" encoders also write the transposed code matrix (see
 // encode_tiles below).
+#include <atomic>
+
 #include "luq_device.hpp"
 #include "luq_launch.hpp"
 
@@ -972,6 +974,58 @@ hipError_t launch_luq_quantize(const void* g, int bf16, int64_t rows, int64_t co
   a.part_out = nullptr;
   a.status = status;
   return bf16 ? luq_launch_t<true>(a, ns, a.nparts, st) : luq_launch_t<false>(a, ns, a.nparts, st);
+}
+
+// ---------------------------- allocation-free LUQ ----------------------------
+//
+// For callers that cannot allocate device memory: the workspace of
+// luq_quantize_grad (partial maxima, their fold, the status word) lives in
+// this file-scope device array instead, one copy per GPU, held until the
+// process ends.  In host code `scratch` names a host-side stand-in, not the
+// device array: its device address is looked up once per device with
+// hipGetSymbolAddress and only that address is used.  Calls on one GPU share
+// the array, so calls that overlap in time on one GPU race; nothing in it
+// needs to start at zero (every word a call reads, the same call wrote).
+constexpr size_t kScratchWords = kStatusWord + 1;
+static __device__ __align__(256) uint32_t scratch[kScratchWords];
+
+constexpr int kMaxScratchDevices = 64;
+static std::atomic<uint32_t*> g_scratch_ptr[kMaxScratchDevices];
+
+size_t noalloc_scratch_bytes() { return sizeof(uint32_t) * kScratchWords; }
+
+// The device address of `scratch` on the current device (looked up on the
+// first call on that device); null with the HIP error in *err on failure.
+static uint32_t* scratch_on_current_device(hipError_t* err) {
+  int dev = 0;
+  *err = hipGetDevice(&dev);
+  if (*err != hipSuccess) return nullptr;
+  if (dev < 0 || dev >= kMaxScratchDevices) {
+    *err = hipErrorInvalidDevice;
+    return nullptr;
+  }
+  uint32_t* p = g_scratch_ptr[dev].load(std::memory_order_acquire);
+  if (!p) {
+    void* addr = nullptr;
+    *err = hipGetSymbolAddress(&addr, HIP_SYMBOL(scratch));
+    if (*err != hipSuccess || !addr) {
+      if (*err == hipSuccess) *err = hipErrorInvalidSymbol;
+      return nullptr;
+    }
+    p = static_cast<uint32_t*>(addr);
+    g_scratch_ptr[dev].store(p, std::memory_order_release);  // racing threads store the same address
+  }
+  return p;
+}
+
+hipError_t launch_luq_quantize_noalloc(const void* g, int bf16, int64_t rows, int64_t cols, int R, int pw2,
+                                       uint64_t seed, uint32_t counter, int ns, uint8_t* codes, uint8_t* codes_t,
+                                       float* alpha, float* maxabs, hipStream_t st) {
+  if (quant_workspace_bytes(rows * cols) > noalloc_scratch_bytes()) return hipErrorInvalidValue;
+  hipError_t err = hipSuccess;
+  uint32_t* ws = scratch_on_current_device(&err);
+  if (!ws) return err;
+  return launch_luq_quantize(g, bf16, rows, cols, R, pw2, seed, counter, ns, codes, codes_t, alpha, maxabs, ws, st);
 }
 
 hipError_t launch_luq_quantize_hindsight(const void* g, int bf16, int64_t rows, int64_t cols, int R, int pw2,

@@ -32,7 +32,7 @@ def _declared():
 
 def test_every_declared_function_is_exported():
     names = _declared()
-    assert len(names) == 15, names
+    assert len(names) == 16, names
     for n in names:
         assert hasattr(LIB, n), n
     assert set(names) == set(luq.EXPORTS)
@@ -289,3 +289,31 @@ def test_conv_wgrad_plan_keeps_int32_sums_exact(T, C, Cout):
     nsplit = max(ws // slab, 1)
     worst_pixels = T / nsplit + 2 * 2560
     assert worst_pixels * 64 * 120 < 2 ** 31, (nsplit, worst_pixels)
+
+
+def _qn(**kw):
+    a = dict(g=P, dt=0, rows=4, cols=8, R=4, seed=0, counter=0, ns=1, codes=P2, codes_t=NUL, alpha=P3, maxabs=NUL)
+    a.update(kw)
+    return LIB.luq_quantize_grad_noalloc(a["g"], a["dt"], a["rows"], a["cols"], a["R"], a["seed"], a["counter"],
+                                         a["ns"], a["codes"], a["codes_t"], a["alpha"], a["maxabs"], None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(dt=2), 3),
+    (dict(rows=-1), 2),
+    (dict(rows=3, cols=7), 2),
+    (dict(rows=4, cols=12, codes_t=P), 2),
+    (dict(R=7), 4),
+    (dict(R=6, ns=2), 4),
+    (dict(ns=3), 4),
+    (dict(alpha=NUL), 1),
+    (dict(g=NUL), 1),
+    (dict(codes=NUL), 1),
+    (dict(g=PMIS), 6),
+    (dict(codes=PMIS), 6),
+])
+def test_noalloc_quantizer_rejects_bad_arguments_on_the_host(kw, status):
+    """The allocation-free LUQ entry point validates like luq_quantize_grad
+    (no workspace argument) and launches nothing on error."""
+    assert _qn(**kw) == status
+    assert LIB.luq_last_error()
