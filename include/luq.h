@@ -50,7 +50,7 @@
 extern "C" {
 #endif
 
-#define LUQ_ABI_VERSION 8
+#define LUQ_ABI_VERSION 9
 
 typedef int luq_status;
 enum {
@@ -82,6 +82,16 @@ typedef enum { LUQ_F32 = 0, LUQ_BF16 = 1 } luq_dtype;
  * for R <= 5. */
 #define LUQ_SMP_SUM 0x10
 
+/* Or-ed into n_samples = 1 of luq_gemm_dgrad and luq_gemm_wgrad: the MACs
+ * run on the FP6 carrier (the scaled f8f6f4 MFMA of CDNA4, e3m2 x e2m3)
+ * instead of INT8.  Every code is exact in FP6 -- the LUQ level alpha 2^(e-1)
+ * as the e3m2 value 2^(e-3) (R <= 6), an INT4 code q as the e2m3 value q/8 --
+ * and the fp32 sums are exact for reductions of up to 16384 (longer ones are
+ * split and combined exactly), so the result equals the INT8 carrier's bit
+ * for bit.  The codes are first converted into FP6 blocks in the workspace,
+ * which is luq_workspace_size(LUQ_OP_GEMM_DGRAD_FP6 / _WGRAD_FP6, ...). */
+#define LUQ_CARRIER_FP6 0x40
+
 /* Operation ids for luq_workspace_size. */
 enum {
   LUQ_OP_QUANTIZE_GRAD = 0, /* d0 = number of elements                     */
@@ -89,7 +99,9 @@ enum {
   LUQ_OP_GEMM_DGRAD = 2,    /* d0 = M, d1 = N, d2 = K                        */
   LUQ_OP_GEMM_WGRAD = 3,    /* d0 = T, d1 = Nout, d2 = Kin                   */
   LUQ_OP_GEMM_FWD = 4,      /* d0 = M, d1 = N, d2 = K                        */
-  LUQ_OP_CONV_WGRAD = 5     /* d0 = B*H*W, d1 = C, d2 = Cout                 */
+  LUQ_OP_CONV_WGRAD = 5,    /* d0 = B*H*W, d1 = C, d2 = Cout                 */
+  LUQ_OP_GEMM_DGRAD_FP6 = 6, /* luq_gemm_dgrad with LUQ_CARRIER_FP6: M, N, K  */
+  LUQ_OP_GEMM_WGRAD_FP6 = 7  /* luq_gemm_wgrad with LUQ_CARRIER_FP6: T, Nout, Kin */
 };
 
 /* ABI version of the loaded library (LUQ_ABI_VERSION of its build). */
@@ -279,7 +291,9 @@ luq_status int4_quantize(const void* x, luq_dtype dt, int64_t rows, int64_t cols
  *  g_codes    n_samples planes of [M][K] LUQ codes (plane stride
  *             luq_plane_bytes(M*K)); with n_samples = LUQ_SMP_SUM | 2 the
  *             [M][K] int8 sums of two samples (luq_quantize_grad's output in
- *             that format), scale alpha / 2.
+ *             that format), scale alpha / 2.  n_samples = LUQ_CARRIER_FP6 | 1
+ *             selects the FP6 carrier for one plane (same result; workspace
+ *             luq_workspace_size(LUQ_OP_GEMM_DGRAD_FP6, M, N, K)).
  *  alpha      1 float (device), the LUQ alpha of g.
  *  w_codes_t  [N][K] INT4 codes; w_scale 1 float (device); w_signed 0/1.
  *  M, N >= 1; K >= 32 and a multiple of 32; each code operand below 2 GiB.
@@ -306,7 +320,9 @@ luq_status luq_gemm_dgrad(const uint8_t* g_codes, const float* alpha, int n_samp
  * in a fixed order, so the result does not depend on the split.
  *
  *  g_codes_t is n_samples planes of codes, or with n_samples =
- *  LUQ_SMP_SUM | 2 the [Nout][T] int8 sums of two samples.
+ *  LUQ_SMP_SUM | 2 the [Nout][T] int8 sums of two samples;
+ *  LUQ_CARRIER_FP6 | 1 selects the FP6 carrier for one plane (same result;
+ *  workspace luq_workspace_size(LUQ_OP_GEMM_WGRAD_FP6, T, Nout, Kin)).
  *  T >= 32 and a multiple of 32; Nout, Kin >= 1; each code operand below
  *  2 GiB.
  *  ws  workspace of luq_workspace_size(LUQ_OP_GEMM_WGRAD, T, Nout, Kin).

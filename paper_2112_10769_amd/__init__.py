@@ -21,7 +21,9 @@ LUQ_ERR_NONFINITE = 8
 LUQ_F32, LUQ_BF16 = 0, 1
 ALPHA_PW2 = 0x100  # or-ed into R: power-of-two alpha
 SMP_SUM = 0x10     # or-ed into n_samples = 2: the two samples as int8 sums
+CARRIER_FP6 = 0x40  # or-ed into n_samples = 1 of the backward GEMMs: FP6 MFMA carrier
 OP_QUANTIZE_GRAD, OP_INT4_QUANTIZE, OP_GEMM_DGRAD, OP_GEMM_WGRAD, OP_GEMM_FWD, OP_CONV_WGRAD = 0, 1, 2, 3, 4, 5
+OP_GEMM_DGRAD_FP6, OP_GEMM_WGRAD_FP6 = 6, 7
 
 EXPORTS = (
     "luq_abi_version", "luq_status_string", "luq_last_error", "luq_plane_bytes",
@@ -242,7 +244,7 @@ def luq_gemm_dgrad(g_codes, alpha, w_codes_t, w_scale, w_signed, M, N, K, n_samp
     """dX [M, N] = Q(g) Q(W) from g codes [M, K] and transposed W codes [N, K]."""
     dev = g_codes.device
     dx = torch.empty(M, N, dtype=torch.float32, device=dev) if dx is None else dx
-    wsb = workspace_size(OP_GEMM_DGRAD, M, N, K)
+    wsb = workspace_size(OP_GEMM_DGRAD_FP6 if n_samples & CARRIER_FP6 else OP_GEMM_DGRAD, M, N, K)
     ws = _bytes(wsb, dev) if ws is None else ws
     st = LIB.luq_gemm_dgrad(_ptr(g_codes), _ptr(alpha), n_samples, _ptr(w_codes_t), _ptr(w_scale),
                             1 if w_signed else 0, M, N, K, _ptr(dx), _ptr(ws), ws.numel(), _stream(dev))
@@ -254,7 +256,7 @@ def luq_gemm_wgrad(g_codes_t, alpha, a_codes_t, a_scale, a_signed, T, Nout, Kin,
     """dW [Nout, Kin] = Q(g)^T Q(a) from transposed codes g^T [Nout, T] and a^T [Kin, T]."""
     dev = g_codes_t.device
     dw = torch.empty(Nout, Kin, dtype=torch.float32, device=dev) if dw is None else dw
-    wsb = workspace_size(OP_GEMM_WGRAD, T, Nout, Kin)
+    wsb = workspace_size(OP_GEMM_WGRAD_FP6 if n_samples & CARRIER_FP6 else OP_GEMM_WGRAD, T, Nout, Kin)
     ws = _bytes(wsb, dev) if ws is None else ws
     st = LIB.luq_gemm_wgrad(_ptr(g_codes_t), _ptr(alpha), n_samples, _ptr(a_codes_t), _ptr(a_scale),
                             1 if a_signed else 0, T, Nout, Kin, _ptr(dw), _ptr(ws), ws.numel(), _stream(dev))

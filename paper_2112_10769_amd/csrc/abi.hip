@@ -8,6 +8,8 @@
 #include "../../include/luq.h"
 #include "luq_launch.hpp"
 
+static_assert(LUQ_CARRIER_FP6 == luq::kCarrierFp6, "carrier flag");
+
 namespace {
 
 thread_local char g_last_error[256] = "";
@@ -99,6 +101,10 @@ size_t luq_workspace_size(int op, int64_t d0, int64_t d1, int64_t d2) {
       return (d0 > 0 && d1 > 0 && d2 > 0) ? luq::gemm_workspace_bytes(d1, d2, d0, 1) : 0;
     case LUQ_OP_GEMM_FWD:
       return (d0 > 0 && d1 > 0 && d2 > 0) ? luq::gemm_fwd_workspace_bytes(d0, d1, d2) : 0;
+    case LUQ_OP_GEMM_DGRAD_FP6:
+      return (d0 > 0 && d1 > 0 && d2 > 0) ? luq::gemm_fp6_workspace_bytes(d0, d1, d2) : 0;
+    case LUQ_OP_GEMM_WGRAD_FP6:
+      return (d0 > 0 && d1 > 0 && d2 > 0) ? luq::gemm_fp6_workspace_bytes(d1, d2, d0) : 0;
     case LUQ_OP_CONV_WGRAD:
       return (d0 > 0 && d1 > 0 && d2 > 0 && d0 < ((int64_t)1 << 31) && d1 < ((int64_t)1 << 28) &&
               d2 < ((int64_t)1 << 28))
@@ -262,6 +268,17 @@ static luq_status gemm_common(const char* name, const uint8_t* A, const float* a
                               int64_t N, int64_t K, float* C, void* ws, size_t ws_bytes,
                               void* stream) {
   if (!A || !alpha || !B || !bscale || !C) return fail(LUQ_ERR_NULL, "%s: NULL operand", name);
+  if (ns & LUQ_CARRIER_FP6) {
+    if (ns != (LUQ_CARRIER_FP6 | 1))
+      return fail(LUQ_ERR_PARAM, "%s: the FP6 carrier takes one sample (n_samples = LUQ_CARRIER_FP6 | 1)", name);
+    luq_status st = gemm_shape(name, M, N, K);
+    if (st != LUQ_OK) return st;
+    if (!luq::gemm_fp6_fits(M, N, K)) return fail(LUQ_ERR_SHAPE, "%s: an FP6 operand reaches 2 GiB", name);
+    st = gemm_checks(name, A, alpha, B, bscale, M, N, K, C, luq::gemm_fp6_workspace_bytes(M, N, K), ws, ws_bytes);
+    if (st != LUQ_OK) return st;
+    return hip_status(luq::launch_gemm_luq_int4_fp6(A, alpha, B, bscale, b_signed ? 1 : 0, M, N, K, C, ws,
+                                                    static_cast<hipStream_t>(stream)));
+  }
   if (ns != 1 && ns != 2 && ns != (LUQ_SMP_SUM | 2))
     return fail(LUQ_ERR_PARAM, "%s: n_samples must be 1, 2 or LUQ_SMP_SUM | 2", name);
   luq_status st = gemm_shape(name, M, N, K, ns == (LUQ_SMP_SUM | 2) ? 1 : 0);

@@ -55,6 +55,16 @@ hipError_t launch_gemm_luq_int4(const uint8_t* A, int64_t a_plane, int ns, const
                                 int64_t N, int64_t K, float* C, void* ws, size_t ws_bytes,
                                 hipStream_t st);
 
+// The same product on the FP6 carrier (one sample): the codes are converted
+// once into fragment-major FP6 blocks in the workspace, then multiplied with
+// the scaled f8f6f4 MFMA; bit-identical to launch_gemm_luq_int4.
+constexpr int kCarrierFp6 = 0x40;
+size_t gemm_fp6_workspace_bytes(int64_t M, int64_t N, int64_t K);
+bool gemm_fp6_fits(int64_t M, int64_t N, int64_t K);
+hipError_t launch_gemm_luq_int4_fp6(const uint8_t* A, const float* alpha, const uint8_t* B, const float* bscale,
+                                    int b_signed, int64_t M, int64_t N, int64_t K, float* C, void* ws,
+                                    hipStream_t st);
+
 // y[m][n] = x_scale * w_scale * sum_k X[m][k] * W[n][k], INT4 codes, K-major.
 size_t gemm_fwd_workspace_bytes(int64_t M, int64_t N, int64_t K);
 hipError_t launch_gemm_int4_fwd(const uint8_t* X, const float* x_scale, int x_signed, const uint8_t* W,

@@ -317,3 +317,24 @@ def test_noalloc_quantizer_rejects_bad_arguments_on_the_host(kw, status):
     (no workspace argument) and launches nothing on error."""
     assert _qn(**kw) == status
     assert LIB.luq_last_error()
+
+
+def test_fp6_carrier_workspace_sizes():
+    """The FP6 carrier's workspace holds both operands as FP6 blocks (3/4 byte
+    per code, rows padded to 32, K to 64) plus split sums when it splits."""
+    M, N, K = 8192, 4096, 16384
+    assert luq.workspace_size(luq.OP_GEMM_DGRAD_FP6, M, N, K) == (M + N) * K * 3 // 4
+    assert luq.workspace_size(luq.OP_GEMM_WGRAD_FP6, 8192, 16384, 4096) == (16384 + 4096) * 8192 * 3 // 4
+    # ragged rows and k: 37 rows pad to 64, K = 96 to 128
+    assert luq.workspace_size(luq.OP_GEMM_DGRAD_FP6, 37, 8, 96) >= (64 + 32) * 128 * 3 // 4
+    # a reduction above 16384 is split: split sums come on top
+    assert luq.workspace_size(luq.OP_GEMM_DGRAD_FP6, 64, 64, 32768) > (64 + 64) * 32768 * 3 // 4
+
+
+def test_fp6_carrier_rejects_on_the_host():
+    def dg(ns, ws_bytes=WS, K=64):
+        return LIB.luq_gemm_dgrad(P, P3, ns, P2, P3, 1, 8, 8, K, P, P, ws_bytes, None)
+    assert dg(luq.CARRIER_FP6 | 2) == 4
+    assert dg(luq.CARRIER_FP6 | luq.SMP_SUM | 2) == 4
+    assert dg(luq.CARRIER_FP6 | 1, ws_bytes=16) == 5
+    assert dg(luq.CARRIER_FP6 | 1, K=48) == 2
