@@ -19,7 +19,9 @@ would still have to fold).  `small` is one linear layer, 256 tokens x
 512 -> 512, on fp32 gradients lognormal(-10, 2) with 50% zeros, half-normal
 activations (unsigned INT4) and He weights.
 `--workload mlp_smp` is the MLP layer with two SMP samples stored as int8
-sums (the bytes of two 4-bit planes); `mlp_smp_planes` keeps two planes.
+sums (the bytes of two 4-bit planes); `mlp_smp_planes` keeps two planes;
+`mlp_fp6` runs both GEMMs on the FP6 carrier (priced against its 10.1 PF
+peak instead of INT8's 5.0 POPS).
 
 Prints one JSON line.  `value` is roofline-normalised throughput: the sum,
 over the step's kernels, of each kernel's roofline time (algorithmic HBM
@@ -53,6 +55,7 @@ sys.path.insert(0, ROOT)
 
 HBM_PEAK = 8.0e12      # bytes/s
 I8_PEAK = 5.0e15       # int8 dense ops/s
+FP6_PEAK = 10.1e15     # fp6 / fp4 dense ops/s (the FP6 carrier's MFMA)
 METRIC = "LUQ quantize GB/s + 4-bit bwd GEMM TFLOP/s (as % of roofline), 1 MI355X"
 METRIC_FWD = "INT4 quantize GB/s + 4-bit fwd GEMM TFLOP/s (as % of roofline), 1 MI355X"
 
@@ -62,7 +65,7 @@ def parse():
     p.add_argument("--gpus", type=int, default=1)
     p.add_argument("--steps", type=int, default=20)
     p.add_argument("--warmup", type=int, default=5)
-    p.add_argument("--workload", default="mlp", choices=["mlp", "mlp_smp", "mlp_smp_planes", "mlp_fwd", "resnet",
+    p.add_argument("--workload", default="mlp", choices=["mlp", "mlp_fp6", "mlp_smp", "mlp_smp_planes", "mlp_fwd", "resnet",
                                                          "resnet_lowered", "small", "luq_sweep"])
     p.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     p.add_argument("--sweep-log2", default=None,
@@ -73,14 +76,17 @@ def parse():
 
 
 class Stage:
-    def __init__(self, name, fn, bytes_, ops=0.0):
-        self.name, self.fn, self.bytes, self.ops = name, fn, float(bytes_), float(ops)
+    """One launch of the step; `peak` is the dense MFMA peak of the carrier its
+    MACs run on (INT8, or FP6 for the FP6 carrier)."""
+
+    def __init__(self, name, fn, bytes_, ops=0.0, peak=I8_PEAK):
+        self.name, self.fn, self.bytes, self.ops, self.peak = name, fn, float(bytes_), float(ops), peak
 
     def roofline_s(self):
-        return max(self.bytes / HBM_PEAK, self.ops / I8_PEAK)
+        return max(self.bytes / HBM_PEAK, self.ops / self.peak)
 
     def bound(self):
-        return "hbm" if self.bytes / HBM_PEAK >= self.ops / I8_PEAK else "mfma"
+        return "hbm" if self.bytes / HBM_PEAK >= self.ops / self.peak else "mfma"
 
 
 def build_resnet(L, torch, dev, lowered=False, d=None):
@@ -162,8 +168,10 @@ def build_resnet(L, torch, dev, lowered=False, d=None):
 
 
 def build_mlp(L, torch, dev, ns=1, T=None, D=None, F=None, d=None):
-    """Backward of the MLP up-projection.  ns: 1, 2 (two SMP sample planes) or
-    L.SMP_SUM | 2 (the two samples as int8 sums, same bytes as two planes)."""
+    """Backward of the MLP up-projection.  ns: 1, 2 (two SMP sample planes),
+    L.SMP_SUM | 2 (the two samples as int8 sums, same bytes as two planes) or
+    L.CARRIER_FP6 | 1 (one sample, both GEMMs on the FP6 carrier; their
+    workspaces hold the operands converted to FP6 blocks)."""
     import synth
     T = T or synth.MLP["T"]
     D = D or synth.MLP["D"]
@@ -175,6 +183,7 @@ def build_mlp(L, torch, dev, ns=1, T=None, D=None, F=None, d=None):
     u8 = lambda n: torch.empty(int(n), dtype=torch.uint8, device=dev)
     f32 = lambda *s: torch.empty(*s, dtype=torch.float32, device=dev)
     summed = bool(ns & L.SMP_SUM)
+    fp6 = bool(ns & L.CARRIER_FP6)
     nsamp = ns & 0xF
     gbytes = T * F if summed else nsamp * L.plane_bytes(T * F)
     gc, gct, alpha, gmax = u8(gbytes), u8(gbytes), f32(1), f32(1)
@@ -184,23 +193,27 @@ def build_mlp(L, torch, dev, ns=1, T=None, D=None, F=None, d=None):
     wsq = u8(L.workspace_size(L.OP_QUANTIZE_GRAD, T * F))
     wsx = u8(L.workspace_size(L.OP_INT4_QUANTIZE, T * D))
     wsw = u8(L.workspace_size(L.OP_INT4_QUANTIZE, F * D))
-    wsd = u8(max(L.workspace_size(L.OP_GEMM_DGRAD, T, D, F), 1))
-    wsg = u8(max(L.workspace_size(L.OP_GEMM_WGRAD, T, F, D), 1))
+    wsd = u8(max(L.workspace_size(L.OP_GEMM_DGRAD_FP6 if fp6 else L.OP_GEMM_DGRAD, T, D, F), 1))
+    wsg = u8(max(L.workspace_size(L.OP_GEMM_WGRAD_FP6 if fp6 else L.OP_GEMM_WGRAD, T, F, D), 1))
     n_g, n_x, n_w = T * F, T * D, F * D
+    peak = FP6_PEAK if fp6 else I8_PEAK
     stages = [
-        Stage("luq_quantize_grad", lambda: L.luq_quantize_grad(g, 4, 0, 0, ns, gc, gct, alpha, gmax, wsq),
+        Stage("luq_quantize_grad", lambda: L.luq_quantize_grad(g, 4, 0, 0, ns & ~L.CARRIER_FP6, gc, gct, alpha, gmax,
+                                                               wsq),
               2 * 2 * n_g + 2 * nsamp * n_g / 2),
         Stage("int4_quantize(x)", lambda: L.int4_quantize(x, True, 0.0, False, xct, sx, wsx), 2 * 2 * n_x + n_x / 2),
         Stage("int4_quantize(W)", lambda: L.int4_quantize(w, True, 0.0, False, wct, sw, wsw), 2 * 4 * n_w + n_w / 2),
         Stage("luq_gemm_dgrad", lambda: L.luq_gemm_dgrad(gc, alpha, wct, sw, True, T, D, F, ns, dx, wsd),
-              nsamp * T * F / 2 + D * F / 2 + 4 * T * D, 2.0 * T * D * F),
+              nsamp * T * F / 2 + D * F / 2 + 4 * T * D, 2.0 * T * D * F, peak),
         Stage("luq_gemm_wgrad", lambda: L.luq_gemm_wgrad(gct, alpha, xct, sx, True, T, F, D, ns, dw, wsg),
-              nsamp * F * T / 2 + D * T / 2 + 4 * F * D, 2.0 * T * D * F),
+              nsamp * F * T / 2 + D * T / 2 + 4 * F * D, 2.0 * T * D * F, peak),
     ]
     d["dev"] = dict(g=g, x=x, w=w, gc=gc, gct=gct, alpha=alpha, gmax=gmax, xct=xct, sx=sx, wct=wct, sw=sw,
                     dx=dx, dw=dw)
-    cfg = {"workload": "transformer_mlp_bwd" + ("_smp2" if nsamp == 2 else "") + ("_planes" if ns == 2 else ""),
-           "tokens": T, "d_model": D, "hidden": F, "grad": "lognormal(-14,3) bf16", "R": 4, "n_samples": nsamp}
+    cfg = {"workload": "transformer_mlp_bwd" + ("_smp2" if nsamp == 2 else "") + ("_planes" if ns == 2 else "")
+           + ("_fp6" if fp6 else ""),
+           "tokens": T, "d_model": D, "hidden": F, "grad": "lognormal(-14,3) bf16", "R": 4, "n_samples": nsamp,
+           "gemm_carrier": "fp6 e3m2 x e2m3 (10.1 PF peak)" if fp6 else "int8 (5.0 POPS peak)"}
     if nsamp == 2:
         cfg["smp_operand"] = "int8 sums of the two samples" if summed else "two 4-bit planes"
     return stages, cfg, d
@@ -770,7 +783,7 @@ def main():
     elif args.workload == "small":
         stages, cfg, d = build_small(L, torch, dev, d=d)
     else:
-        ns = {"mlp_smp": L.SMP_SUM | 2, "mlp_smp_planes": 2}.get(args.workload, 1)
+        ns = {"mlp_smp": L.SMP_SUM | 2, "mlp_smp_planes": 2, "mlp_fp6": L.CARRIER_FP6 | 1}.get(args.workload, 1)
         stages, cfg, d = build_mlp(L, torch, dev, ns, d=d)
     step_s, per = time_stages(torch, stages, args.steps, args.warmup)
     roof_total = sum(s.roofline_s() for s in stages)
@@ -787,8 +800,9 @@ def main():
         roof = {"kernel": dom.name, "bound": "hbm", "achieved": round(dom.bytes / t / 1e9, 1), "peak": 8000.0,
                 "unit": "GB/s", "frac": round(dom.bytes / t / HBM_PEAK, 4), "traffic": traffic}
     else:
-        roof = {"kernel": dom.name, "bound": "mfma", "achieved": round(dom.ops / t / 1e12, 1), "peak": 5000.0,
-                "unit": "TFLOP/s", "frac": round(dom.ops / t / I8_PEAK, 4), "traffic": traffic}
+        roof = {"kernel": dom.name, "bound": "mfma", "achieved": round(dom.ops / t / 1e12, 1),
+                "peak": round(dom.peak / 1e12, 1), "unit": "TFLOP/s", "frac": round(dom.ops / t / dom.peak, 4),
+                "traffic": traffic}
     roof["algorithmic_bytes"] = dom.bytes
     roof["launch_us"] = round(t * 1e6, 2)
     out = {
