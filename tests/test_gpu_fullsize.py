@@ -5,10 +5,10 @@ builders), run once in stage order.
 Where the oracle finishes in seconds the whole output is compared (the conv
 workload's quantizers, im2col and weight gradient); otherwise outputs are
 sampled -- code ranges and single elements computed one by one by the
-oracle from their flat indices, GEMM rows computed from exactly the codes
-they need -- and properties that hold at any size are checked on the whole
-output (maxabs, alpha, the transposed layout against the row-major one,
-valid code set).
+oracle from their flat indices, GEMM rows and whole 256-row tile bands
+computed from exactly the codes they need -- and properties that hold at any
+size are checked on the whole output (maxabs, alpha, the transposed layout
+against the row-major one, valid code set).
 """
 import numpy as np
 import pytest
@@ -239,6 +239,49 @@ def test_mlp_wgrad_sampled_rows(mlp, mlp_data):
     assert np.array_equal(dw, epilogue_replica(acc, alpha, ns, xs)), "mlp dW epilogue not bit-exact"
 
 
+def test_mlp_dgrad_full_row_band(mlp, mlp_data):
+    """dX rows 4096..4351: one whole 256-row tile band across all 4096 columns
+    (every column tile of the 256 x 256 kernel)."""
+    T, F = mlp_data["g"].shape
+    D = mlp_data["x"].shape[1]
+    ns, dv = mlp["ns"], mlp["dev"]
+    alpha = np.float32(oluq.luq_alpha(np.float32(np.abs(mlp_data["gf"]).max()), 4))
+    wc, ws = mlp_data["wq"]
+    r0, nr = 4096, 256
+    idx = np.arange(r0 * F, (r0 + nr) * F, dtype=np.int64)
+    planes = np.stack([pack_nibbles(_g_nibbles_at(mlp_data, idx, alpha, s)) for s in range(ns)])
+    dx = host(dv["dx"])[r0:r0 + nr]
+    A = sum(oluq.luq_decode_int(planes[s], nr * F).reshape(nr, F) for s in range(ns))
+    Bm = oint4.int4_decode_int(wc, F * D, True).reshape(F, D)
+    acc = (A.astype(np.float64) @ Bm.astype(np.float64)).astype(np.int64)
+    absacc = np.abs(A).astype(np.float64) @ np.abs(Bm).astype(np.float64)
+    sc = np.float64(alpha) / ns * np.float64(ws)
+    assert_gemm_close(dx, acc * sc, absacc * sc, f"mlp dX band ns={ns}")
+    assert np.array_equal(dx, epilogue_replica(acc, alpha, ns, ws)), "mlp dX band epilogue not bit-exact"
+
+
+def test_mlp_wgrad_full_row_band(mlp, mlp_data):
+    """dW rows (output features) 8192..8447: one whole 256-row tile band
+    across all 4096 columns, over the 8192 tokens."""
+    T, F = mlp_data["g"].shape
+    D = mlp_data["x"].shape[1]
+    ns, dv = mlp["ns"], mlp["dev"]
+    alpha = np.float32(oluq.luq_alpha(np.float32(np.abs(mlp_data["gf"]).max()), 4))
+    xc, xs = mlp_data["xq"]
+    o0, no = 8192, 256
+    outs = np.arange(o0, o0 + no, dtype=np.int64)
+    idx = (np.arange(T)[:, None] * F + outs[None, :]).ravel()      # g[:, outs], token-major
+    planes = np.stack([pack_nibbles(_g_nibbles_at(mlp_data, idx, alpha, s)) for s in range(ns)])
+    dw = host(dv["dw"])[o0:o0 + no]
+    G = sum(oluq.luq_decode_int(planes[s], T * no).reshape(T, no) for s in range(ns))
+    X = oint4.int4_decode_int(xc, T * D, True).reshape(T, D)
+    acc = (G.T.astype(np.float64) @ X.astype(np.float64)).astype(np.int64)
+    absacc = np.abs(G.T).astype(np.float64) @ np.abs(X).astype(np.float64)
+    sc = np.float64(alpha) / ns * np.float64(xs)
+    assert_gemm_close(dw, acc * sc, absacc * sc, f"mlp dW band ns={ns}")
+    assert np.array_equal(dw, epilogue_replica(acc, alpha, ns, xs)), "mlp dW band epilogue not bit-exact"
+
+
 @pytest.fixture(scope="module")
 def mlp_fwd(L, mlp_data):
     import bench
@@ -294,6 +337,29 @@ def _sweep_case(L, g, dtype, what):
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 def test_sweep_2pow28(L, dtype):
     _sweep_case(L, synth.sweep(28, dtype), dtype, "2^28")
+
+
+def _tiled_draw(k, dtype, seed):
+    """2^k elements that repeat one 2^24-element lognormal(-10, 3) draw (25%
+    zeros) with a different sign pattern per copy: the marginal distribution
+    of the sweep, cheap to build at 2^29 and 2^30."""
+    base = synth.lognormal_grad((1 << 24,), -10.0, 3.0, 0.25, [4, seed])
+    copies = 1 << (k - 24)
+    flips = np.random.default_rng(seed).random(copies) < 0.5
+    if dtype == "bf16":
+        b = synth.to_bf16_bits(base)
+        sign = np.where(flips, np.uint16(0x8000), np.uint16(0))
+        return (b[None, :] ^ sign[:, None]).ravel()
+    return (base[None, :] * np.where(flips, -1.0, 1.0).astype(np.float32)[:, None]).ravel()
+
+
+@pytest.mark.parametrize("k,dtype", [(29, "bf16"), (30, "bf16"), (29, "f32")])
+def test_sweep_large_streamed(L, k, dtype):
+    """The streamed quantizer paths at the sweep's largest bf16 sizes and
+    fp32 2^29 (sampled code ranges, whole-tensor max, alpha and code set)."""
+    g = _tiled_draw(k, dtype, 100 + k)
+    _sweep_case(L, g, dtype, f"2^{k}")
+    torch.cuda.empty_cache()
 
 
 def test_sweep_2pow30_fp32_beyond_4GiB(L):
