@@ -440,6 +440,56 @@ __device__ __forceinline__ uint32_t luq_word(const U8& v, uint64_t blk, uint32_t
   return fields | (gather_signs(v) & (nz << 3));
 }
 
+typedef short s16x2 __attribute__((ext_vector_type(2)));
+
+__device__ __forceinline__ s16x2 as_s16x2(uint32_t x) { return __builtin_bit_cast(s16x2, x); }
+__device__ __forceinline__ uint32_t as_u32(s16x2 x) { return __builtin_bit_cast(uint32_t, x); }
+
+// luq_word for bf16 input on the unscaled path (alpha >= 2^-96, so alpha and
+// alpha/2 have zero low halves, as every bf16 magnitude does): the same codes,
+// with the bin index, base field, [n1 >= 1] and max(n1, 1) computed for two
+// elements at once with 16-bit packed integer operations.  Elements are
+// paired (i, i+4), so a pair's base fields land in nibbles i and i+4 with one
+// shift-or, and the 16-bit bin index equals the 32-bit one:
+// ((a - a1) << 16) >> 23 = (a - a1) >> 7 for 16-bit a, a1 (|a - a1| < 2^15).
+// The rounding decision per element is luq_word's fused multiply-add.
+__device__ __forceinline__ uint32_t luq_word_bf16(const U8& v, uint64_t blk, uint32_t sample, uint32_t counter,
+                                                  uint32_t k0, uint32_t k1, const LuqParams& p) {
+  const U4 y = philox4x32_10(U4{(uint32_t)blk, (uint32_t)(blk >> 32), sample, counter}, k0, k1);
+  const uint32_t w[4] = {y.x, y.y, y.z, y.w};
+  // the loaded bf16 words: elements 2i (low half) and 2i+1 (high half)
+  uint32_t q[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) q[i] = (v.v[2 * i] >> 16) | (v.v[2 * i + 1] & 0xFFFF0000u);
+  const s16x2 a1 = as_s16x2((p.a1_bits >> 16) * 0x10001u);
+  uint32_t base = 0, sg = 0;
+  U8 r;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    // pair i: element i in the low half, element i + 4 in the high half
+    const uint32_t pr = __builtin_amdgcn_perm(q[2 + (i >> 1)], q[i >> 1], (i & 1) ? 0x07060302u : 0x05040100u);
+    sg |= ((pr >> 12) & 0x00080008u) << (4 * i);    // signs of elements i, i+4 at bits 4i+3, 4i+19
+    const uint32_t pm = pr & 0x7FFF7FFFu;
+    const s16x2 n1 = (as_s16x2(pm) - a1) >> 7;
+    const s16x2 f0 = __builtin_elementwise_max(n1, (s16x2){0, 0});
+    uint32_t ge;  // [n1 >= 1] per half, one packed min (the compiler would compare and select)
+    asm("v_pk_min_i16 %0, %1, %2" : "=v"(ge) : "v"(as_u32(f0)), "s"(0x00010001u));
+    const uint32_t m1 = as_u32(__builtin_elementwise_max(n1, (s16x2){1, 1}));
+    base |= as_u32(f0) << (4 * i);                  // fields <= R + 1 <= 7: nibbles i and i + 4
+    const float w16_lo = __uint_as_float(p.w16_bits + (m1 << 23));
+    const float w16_hi = __uint_as_float(p.w16_bits + (__builtin_amdgcn_ubfe(m1, 16, 3) << 23));
+    // jj = j + 2^16 [n1 >= 1]: j of element e is half e & 1 of word e >> 1
+    const uint32_t jj_lo = __builtin_amdgcn_perm(ge, w[i >> 1], (i & 1) ? 0x0C040302u : 0x0C040100u);
+    const uint32_t jj_hi = __builtin_amdgcn_perm(ge, w[2 + (i >> 1)], (i & 1) ? 0x0C060302u : 0x0C060100u);
+    r.v[i] = __float_as_uint(fmaf((float)jj_lo, w16_lo, -__uint_as_float(pm << 16)));
+    r.v[i + 4] = __float_as_uint(fmaf((float)jj_hi, w16_hi, -__uint_as_float(pm & 0xFFFF0000u)));
+  }
+  const uint32_t up = (gather_signs(r) >> 3) & 0x11111111u;
+  const uint32_t fields = base + up;
+  const uint32_t nz = (fields | (fields >> 1) | (fields >> 2)) & 0x11111111u;
+  return fields | (sg & (nz << 3));
+}
+
 struct LuqArgs {
   const void* g;
   int64_t rows, cols, n;
@@ -483,17 +533,26 @@ __device__ __forceinline__ LuqParams luq_block_params(const LuqArgs& a) {
 
 // Codes of group g (elements 8g .. 8g+7): one word per sample plane, or with
 // SUM the 8 int8 sums of the two samples.
-template <bool NT, int NS, bool SUM, bool SCALED, bool HS>
+// The code word of 8 elements: the bf16-specialised encoder on the common
+// (unscaled, exact-maximum) bf16 path, luq_word otherwise.
+template <bool BF16, bool SCALED, bool HS>
+__device__ __forceinline__ uint32_t luq_code_word(const U8& v, uint64_t blk, uint32_t sample, const LuqArgs& a,
+                                                  const LuqParams& p) {
+  if constexpr (BF16 && !SCALED && !HS) return luq_word_bf16(v, blk, sample, a.counter, a.k0, a.k1, p);
+  return luq_word<SCALED, HS>(v, blk, sample, a.counter, a.k0, a.k1, p);
+}
+
+template <bool BF16, bool NT, int NS, bool SUM, bool SCALED, bool HS>
 __device__ __forceinline__ void luq_emit_group(const LuqArgs& a, const LuqParams& p, const U8& v, int64_t g) {
   if constexpr (SUM) {
     uint32_t lo, hi;
-    smp_sum_bytes(luq_word<SCALED, HS>(v, (uint64_t)g, 0, a.counter, a.k0, a.k1, p),
-                  luq_word<SCALED, HS>(v, (uint64_t)g, 1, a.counter, a.k0, a.k1, p), lo, hi);
+    smp_sum_bytes(luq_code_word<BF16, SCALED, HS>(v, (uint64_t)g, 0, a, p),
+                  luq_code_word<BF16, SCALED, HS>(v, (uint64_t)g, 1, a, p), lo, hi);
     store_word2<NT>(a.codes + g * 8, lo, hi);
   } else {
 #pragma unroll
     for (int s = 0; s < NS; ++s)
-      store_word<NT>(a.codes + s * a.plane + g * 4, luq_word<SCALED, HS>(v, (uint64_t)g, s, a.counter, a.k0, a.k1, p));
+      store_word<NT>(a.codes + s * a.plane + g * 4, luq_code_word<BF16, SCALED, HS>(v, (uint64_t)g, s, a, p));
   }
 }
 
@@ -517,20 +576,20 @@ __device__ __forceinline__ uint32_t luq_flat_body(const LuqArgs& a, const LuqPar
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
       if (HS) mx = max(mx, max_key8(v[u]));
-      luq_emit_group<NT, NS, SUM, SCALED, HS>(a, p, v[u], at(g + u * stride));
+      luq_emit_group<BF16, NT, NS, SUM, SCALED, HS>(a, p, v[u], at(g + u * stride));
     }
   }
   for (; g + stride < nfull; g += 2 * stride) {
     const U8 v0 = load8<BF16, NT>(a.g, at(g) * 8);
     const U8 v1 = load8<BF16, NT>(a.g, at(g + stride) * 8);
     if (HS) mx = max(mx, max(max_key8(v0), max_key8(v1)));
-    luq_emit_group<NT, NS, SUM, SCALED, HS>(a, p, v0, at(g));
-    luq_emit_group<NT, NS, SUM, SCALED, HS>(a, p, v1, at(g + stride));
+    luq_emit_group<BF16, NT, NS, SUM, SCALED, HS>(a, p, v0, at(g));
+    luq_emit_group<BF16, NT, NS, SUM, SCALED, HS>(a, p, v1, at(g + stride));
   }
   if (g < nfull) {
     const U8 v = load8<BF16, NT>(a.g, at(g) * 8);
     if (HS) mx = max(mx, max_key8(v));
-    luq_emit_group<NT, NS, SUM, SCALED, HS>(a, p, v, at(g));
+    luq_emit_group<BF16, NT, NS, SUM, SCALED, HS>(a, p, v, at(g));
   }
   if ((a.n & 7) && blockIdx.x == 0 && threadIdx.x == 0) {
     const U8 v = load8_tail<BF16>(a.g, nfull * 8, a.n);  // missing elements read +0
@@ -595,7 +654,7 @@ struct LuqEnc {
   const LuqParams* p;
   __device__ U8 load(int64_t e0) const { return load8<BF16, NT>(a->g, e0); }
   __device__ uint32_t word(const U8& v, uint64_t blk, int s) const {
-    return p->zero ? 0u : luq_word<SCALED, HS>(v, blk, s, a->counter, a->k0, a->k1, *p);
+    return p->zero ? 0u : luq_code_word<BF16, SCALED, HS>(v, blk, s, *a, *p);
   }
 };
 
