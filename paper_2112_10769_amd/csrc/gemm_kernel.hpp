@@ -423,6 +423,245 @@ __global__ __launch_bounds__(kGemmThreads, BK == 64 ? 3 : 1) void gemm_luq_int4_
   }
 }
 
+// ---- the 256 x 256 tile: eight waves, the B operand in registers ---------------
+//
+// 512 threads = 2 x 4 waves; a wave owns a 128 x 64 block of C (4 x 2 tiles of
+// the 32x32 MFMA), so two waves share each SIMD and the expansion, address and
+// LDS work of one overlaps the MFMAs of the other.  Only A passes through LDS,
+// expanded to int8 once per workgroup (the LUQ expansion is the costly one,
+// and LDS stores run at a quarter of the LDS read rate).  Each wave loads the
+// nibbles of its own 64 B rows straight into registers (the wave of the other
+// row half loads the same rows) and expands every fragment just before its
+// MFMAs, which is a shift and a mask per word.
+//
+// k order: a 128-deep stage is 64 nibble bytes of every row.  At k-step kk,
+// lane half h = lane/32 supplies the k of nibble bytes 32h + 8kk .. +7 of the
+// stage, for both operands, so a lane's B nibbles of a whole stage are one
+// contiguous 32-byte segment.  The products summed are the same, in another
+// order.  A sits in LDS as 8 slots of 16 expanded bytes per row, slot 2kk + h
+// holding those k.
+//
+// Pipeline (one barrier per stage): stage t is multiplied from LDS buffer t%2
+// with B registers set t%2, while the A codes of stage t+1 are expanded into
+// the other buffer; each A chunk and each B half-segment is reloaded (A with
+// stage t+3, B with stage t+2) as soon as its registers are consumed.
+constexpr int kW8Threads = 512;
+
+template <int AC, int NS, bool BSIGNED, bool FULLK>
+__global__ __launch_bounds__(kW8Threads, 1) void gemm_w8_kernel(GemmArgs a) {
+  constexpr int BM = 256, kBK = 128, kThr = kW8Threads;
+  constexpr int kPitch = kBK + 16;        // A row: 8 slots of 16 bytes, 16 bytes of pad
+  constexpr int STAGE = BM * kPitch;
+  constexpr int TM = 4, TN = 2;           // 32x32 tiles per wave
+  constexpr int ACH = BM * 4 / kThr;      // 16-byte A chunks per thread and stage
+  constexpr bool kI8 = AC == kAcSum2;
+  constexpr int NA = kI8 ? 2 : NS;
+  static_assert(ACH == 2, "one A half-chunk per k-step");
+  __shared__ __attribute__((aligned(16))) uint8_t lds[2 * STAGE];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave >> 2, wn = wave & 3, h = lane >> 5;
+  int tm, tn;
+  tile_coords(blockIdx.x, a.tiles_m, a.tiles_n, tm, tn);
+  const int64_t m0 = (int64_t)tm * BM, n0 = (int64_t)tn * 256;
+  const int64_t kbeg = (int64_t)blockIdx.y * a.k_chunk;
+  const int64_t kend = min(kbeg + a.k_chunk, a.K);
+  const int nkt = (int)((kend - kbeg + kBK - 1) / kBK);
+  const int64_t ld = a.K >> 1;              // bytes per B row (and per nibble A row)
+  const int64_t lda = kI8 ? a.K : ld;       // bytes per A row
+
+  __amdgpu_buffer_rsrc_t rsa[NS];
+#pragma unroll
+  for (int s = 0; s < NS; ++s)
+    rsa[s] = __builtin_amdgcn_make_buffer_rsrc((void*)(a.A + s * a.a_plane), (short)0,
+                                               (int)(a.M * lda), kBufferFlags);
+  const __amdgpu_buffer_rsrc_t rsb =
+      __builtin_amdgcn_make_buffer_rsrc((void*)a.B, (short)0, (int)(a.N * ld), kBufferFlags);
+  // A loader: chunk i of a thread is row c/4, 16 nibble bytes (32 k) at 16*(c%4)
+  int offa[ACH], kca[ACH], slota[ACH], rowa[ACH];
+#pragma unroll
+  for (int i = 0; i < ACH; ++i) {
+    const int c = tid + i * kThr, row = c >> 2, kc = c & 3;
+    kca[i] = kc * 32;
+    rowa[i] = row;
+    slota[i] = 4 * (kc & 1) + (kc >> 1);  // slot of the chunk's first half; the second is 2 further
+    offa[i] = kI8 ? (int)((m0 + row) * lda + kbeg + kc * 32) : (int)((m0 + row) * ld + (kbeg >> 1) + kc * 16);
+  }
+  // B: rows n0 + 64wn + 32j + lane%32, the 32-byte segment 32h of each stage
+  int offb[TN];
+#pragma unroll
+  for (int j = 0; j < TN; ++j) offb[j] = (int)((n0 + wn * 64 + j * 32 + (lane & 31)) * ld + (kbeg >> 1) + h * 32);
+
+  struct ARegs {
+    v4u a[NA][ACH];
+  };
+  struct BRegs {
+    v4u b[TN][2];
+  };
+  auto load_a = [&](ARegs& r, int t, int i) {
+    const int64_t k0 = kbeg + (int64_t)t * kBK;
+    const bool in = FULLK || (k0 + kca[i]) < kend;
+    if constexpr (kI8) {
+      const int off = in ? offa[i] + t * kBK : kOutOfRange;
+      r.a[0][i] = __builtin_amdgcn_raw_buffer_load_b128(rsa[0], off, 0, 0);
+      r.a[1][i] = __builtin_amdgcn_raw_buffer_load_b128(rsa[0], in ? off + 16 : kOutOfRange, 0, 0);
+    } else {
+      const int off = in ? offa[i] + t * (kBK / 2) : kOutOfRange;
+#pragma unroll
+      for (int s = 0; s < NS; ++s) r.a[s][i] = __builtin_amdgcn_raw_buffer_load_b128(rsa[s], off, 0, 0);
+    }
+  };
+  auto load_b = [&](BRegs& r, int t, int q) {
+    const bool in = FULLK || (kbeg + (int64_t)t * kBK + h * 64 + q * 32) < kend;
+#pragma unroll
+    for (int j = 0; j < TN; ++j)
+      r.b[j][q] = __builtin_amdgcn_raw_buffer_load_b128(rsb, in ? offb[j] + t * (kBK / 2) + q * 16 : kOutOfRange, 0, 0);
+  };
+  // half hf of A chunk i (its k 16hf .. 16hf+15) -> 16 bytes of LDS
+  auto expand_a = [&](const ARegs& r, int buf, int i, int hf) {
+    uint32_t w[4];
+    if constexpr (kI8) {
+      const v4u x = r.a[hf][i];
+      w[0] = __builtin_amdgcn_perm(x[1], x[0], 0x06040200u);  // k even
+      w[1] = __builtin_amdgcn_perm(x[1], x[0], 0x07050301u);  // k odd
+      w[2] = __builtin_amdgcn_perm(x[3], x[2], 0x06040200u);
+      w[3] = __builtin_amdgcn_perm(x[3], x[2], 0x07050301u);
+    } else if constexpr (AC != kAcLuq) {
+      expand_int4<AC == kAcInt4S>(r.a[0][i][2 * hf], w[0], w[1]);
+      expand_int4<AC == kAcInt4S>(r.a[0][i][2 * hf + 1], w[2], w[3]);
+    } else if constexpr (NS == 1) {
+      expand_luq(r.a[0][i][2 * hf], w[0], w[1]);
+      expand_luq(r.a[0][i][2 * hf + 1], w[2], w[3]);
+    } else {
+#pragma unroll
+      for (int d = 0; d < 2; ++d) {
+        uint32_t l0, h0, l1, h1;
+        expand_luq_excess64(r.a[0][i][2 * hf + d], l0, h0);
+        expand_luq_excess64(r.a[1][i][2 * hf + d], l1, h1);
+        w[2 * d] = (l0 + l1) ^ 0x80808080u;
+        w[2 * d + 1] = (h0 + h1) ^ 0x80808080u;
+      }
+    }
+    *reinterpret_cast<uint4*>(lds + buf * STAGE + rowa[i] * kPitch + ((slota[i] + 2 * hf) << 4)) =
+        make_uint4(w[0], w[1], w[2], w[3]);
+  };
+
+  v16i acc[TM][TN];
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int j = 0; j < TN; ++j) acc[i][j] = v16i{};
+
+  // A fragment i of k-step kk: row 128wm + 32i + lane%32, slot 2kk + h
+  const int aoff = (wm * 128 + (lane & 31)) * kPitch + (h << 4);
+  auto read_a = [&](int buf, int kk, v4i (&fa)[TM]) {
+    const uint8_t* as = lds + buf * STAGE + aoff + (kk << 5);
+#pragma unroll
+    for (int i = 0; i < TM; ++i) fa[i] = *reinterpret_cast<const v4i*>(as + i * 32 * kPitch);
+  };
+  // B fragment j of k-step kk: nibble dwords 2kk, 2kk+1 of the lane's segment
+  auto frag_b = [&](const BRegs& r, int kk, v4i (&fb)[TN]) {
+#pragma unroll
+    for (int j = 0; j < TN; ++j) {
+      uint32_t l0, h0, l1, h1;
+      expand_int4<BSIGNED>(r.b[j][kk >> 1][2 * (kk & 1)], l0, h0);
+      expand_int4<BSIGNED>(r.b[j][kk >> 1][2 * (kk & 1) + 1], l1, h1);
+      fb[j] = v4i{(int)l0, (int)h0, (int)l1, (int)h1};
+    }
+  };
+
+  auto step = [&](int cb, ARegs& ra, int ta, BRegs& rb, int tb) {
+#pragma unroll
+    for (int kk = 0; kk < 4; ++kk) {
+      v4i fa[TM], fb[TN];
+      read_a(cb, kk, fa);
+      frag_b(rb, kk, fb);
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_i32_32x32x32_i8(fb[j], fa[i], acc[i][j], 0, 0, 0);
+      if (kk & 1) load_b(rb, tb, kk >> 1);  // half kk/2 of the segment is consumed
+      expand_a(ra, cb ^ 1, kk >> 1, kk & 1);
+      if (kk & 1) load_a(ra, ta, kk >> 1);  // chunk kk/2 is expanded
+    }
+    __syncthreads();
+    // keep the next stage's work below the barrier: hoisted above it, the
+    // expansion of registers loaded in this stage would wait for those loads
+    __builtin_amdgcn_sched_barrier(0);
+  };
+
+  ARegs r0, r1;
+  BRegs b0, b1;
+#pragma unroll
+  for (int i = 0; i < ACH; ++i) load_a(r0, 0, i);
+  load_b(b0, 0, 0);
+  load_b(b0, 0, 1);
+#pragma unroll
+  for (int i = 0; i < ACH; ++i) load_a(r1, 1, i);
+  load_b(b1, 1, 0);
+  load_b(b1, 1, 1);
+#pragma unroll
+  for (int kk = 0; kk < 4; ++kk) expand_a(r0, 0, kk >> 1, kk & 1);
+  __syncthreads();
+#pragma unroll
+  for (int i = 0; i < ACH; ++i) load_a(r0, 2, i);
+  int t = 0;
+  for (; t + 2 <= nkt; t += 2) {
+    step(0, r1, t + 3, b0, t + 2);  // multiply t, expand t+1 (r1); reload r1 with t+3, b0 with t+2
+    step(1, r0, t + 4, b1, t + 3);  // multiply t+1, expand t+2 (r0); reload r0 with t+4, b1 with t+3
+  }
+  if (t < nkt) step(0, r1, t + 3, b0, t + 2);
+
+  // Epilogue through LDS, as in the four-wave kernel: each wave stages 32 rows
+  // of its 128 x 64 block at a time and stores whole 256-byte row segments.
+  constexpr int WN = 64;
+  constexpr int EP = WN + 4;
+  constexpr int LPR = WN / 4, RPI = 64 / LPR;
+  static_assert(8 * 32 * EP * 4 <= 2 * STAGE, "epilogue slabs fit in the stage buffers");
+  uint32_t* E = reinterpret_cast<uint32_t*>(lds) + wave * 32 * EP;
+  const bool part = a.partial != nullptr;
+  const float sc = part ? 0.0f : epilogue_scale<AC, NS, BSIGNED>(*a.alpha, *a.bscale);
+  uint32_t* out = part ? reinterpret_cast<uint32_t*>(a.partial + (int64_t)blockIdx.y * a.M * a.N)
+                       : reinterpret_cast<uint32_t*>(a.C);
+  const int64_t rbase = m0 + wm * 128, cbase = n0 + wn * WN;
+  const int srow = lane / LPR, scol = (lane % LPR) * 4;
+  __syncthreads();  // every wave is done with the stage buffers
+#pragma unroll
+  for (int i = 0; i < TM; ++i) {
+#pragma unroll
+    for (int j = 0; j < TN; ++j)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        v4u v;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int32_t x = acc[i][j][4 * q + r];
+          v[r] = part ? (uint32_t)x : __float_as_uint(__fmul_rn((float)x, sc));
+        }
+        *reinterpret_cast<v4u*>(E + (lane & 31) * EP + j * 32 + 8 * q + 4 * (lane >> 5)) = v;
+      }
+    __syncthreads();
+#pragma unroll
+    for (int rr = 0; rr < 32; rr += RPI) {
+      const int64_t row = rbase + i * 32 + rr + srow;
+      const int64_t col = cbase + scol;
+      if (row < a.M) {
+        const v4u v = *reinterpret_cast<const v4u*>(E + (rr + srow) * EP + scol);
+        uint32_t* dst = out + row * a.N + col;
+        if (a.vec && col + 3 < a.N) {
+          *reinterpret_cast<v4u*>(dst) = v;
+        } else {
+#pragma unroll
+          for (int r = 0; r < 4; ++r)
+            if (col + r < a.N) dst[r] = v[r];
+        }
+      }
+    }
+    __syncthreads();  // the slab is rewritten by the next i
+  }
+}
+
 // Sums the split-K chunk sums in int64 and applies the scales.  A block owns
 // 64 consecutive outputs; its four waves add every fourth chunk (coalesced
 // 256-byte reads), then combine through LDS in a fixed order.
@@ -529,8 +768,12 @@ static hipError_t gemm_launch_t(const GemmArgs& a0, const GemmPlan& p, hipStream
   const dim3 grid((unsigned)(p.tiles_m * p.tiles_n), (unsigned)p.splits);
   // 16-byte stores need 16-byte aligned rows
   a.vec = (a.N % 4) == 0 && (((uintptr_t)(a.partial ? (void*)a.partial : (void*)a.C)) & 15) == 0;
-  if (p.bm == 256)
-    launch_tile<256, 256, 128, AC, NS, BSIGNED>(a, grid, st);
+  if (p.bm == 256) {
+    if (a.K % kKAlign == 0)
+      hipLaunchKernelGGL((gemm_w8_kernel<AC, NS, BSIGNED, true>), grid, dim3(kW8Threads), 0, st, a);
+    else
+      hipLaunchKernelGGL((gemm_w8_kernel<AC, NS, BSIGNED, false>), grid, dim3(kW8Threads), 0, st, a);
+  }
   else if (p.bm == 128 && p.bk == 64)
     launch_tile<128, 128, 64, AC, NS, BSIGNED>(a, grid, st);
   else if (p.bm == 128)
