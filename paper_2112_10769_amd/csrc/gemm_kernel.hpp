@@ -62,15 +62,18 @@ __device__ __forceinline__ void expand_luq(uint32_t x, uint32_t& lo, uint32_t& h
   const uint32_t t_lo = 0x04020100u, t_hi = 0x40201008u;
   const uint32_t m_lo = __builtin_amdgcn_perm(t_hi, t_lo, x & 0x07070707u);
   const uint32_t m_hi = __builtin_amdgcn_perm(t_hi, t_lo, (x >> 4) & 0x07070707u);
-  // selector bytes 12 (sign clear) or 13 (sign set): v_perm_b32 turns them
-  // into 0x00 / 0xFF, a byte mask of the negative elements
-  const uint32_t q_lo = ((x >> 3) & 0x01010101u) | 0x0C0C0C0Cu;
-  const uint32_t q_hi = ((x >> 7) & 0x01010101u) | 0x0C0C0C0Cu;
-  const uint32_t k_lo = __builtin_amdgcn_perm(0u, 0u, q_lo), k_hi = __builtin_amdgcn_perm(0u, 0u, q_hi);
+  // byte masks of the negative elements: v_perm_b32 selectors 8..11 copy
+  // bit 7 of bytes 1 and 3 of either source into a whole byte, so with the
+  // sources (y << 8, y) selector bytes (10, 8, 11, 9) give byte i = bit 7 of
+  // byte i of y; y = x for the odd-k nibbles, x << 4 for the even-k ones
+  constexpr uint32_t kSignSel = 0x090B080Au;
+  const uint32_t y = x << 4;
+  const uint32_t k_lo = __builtin_amdgcn_perm(y << 8, y, kSignSel);
+  const uint32_t k_hi = __builtin_amdgcn_perm(x << 8, x, kSignSel);
   // negation = (m ^ 0xFF) + 1, which never carries out of a byte because
   // m >= 1 wherever the sign is set
-  lo = (m_lo ^ k_lo) + (q_lo & 0x01010101u);
-  hi = (m_hi ^ k_hi) + (q_hi & 0x01010101u);
+  lo = (m_lo ^ k_lo) + (k_lo & 0x01010101u);
+  hi = (m_hi ^ k_hi) + (k_hi & 0x01010101u);
 }
 
 // SMP operand (two LUQ planes, R <= 5 so every value is in [-32, 32]): each
@@ -573,6 +576,13 @@ __global__ __launch_bounds__(kW8Threads, 1) void gemm_w8_kernel(GemmArgs a) {
   auto step = [&](int cb, ARegs& ra, int ta, BRegs& rb, int tb) {
 #pragma unroll
     for (int kk = 0; kk < 4; ++kk) {
+      if (kk == 2) {
+        // the first B half-segment and A chunk are consumed: reload them now
+        // (the scheduler would otherwise sink the loads to the barrier)
+        load_b(rb, tb, 0);
+        load_a(ra, ta, 0);
+        __builtin_amdgcn_sched_barrier(0);
+      }
       v4i fa[TM], fb[TN];
       read_a(cb, kk, fa);
       frag_b(rb, kk, fb);
@@ -581,10 +591,10 @@ __global__ __launch_bounds__(kW8Threads, 1) void gemm_w8_kernel(GemmArgs a) {
 #pragma unroll
         for (int j = 0; j < TN; ++j)
           acc[i][j] = __builtin_amdgcn_mfma_i32_32x32x32_i8(fb[j], fa[i], acc[i][j], 0, 0, 0);
-      if (kk & 1) load_b(rb, tb, kk >> 1);  // half kk/2 of the segment is consumed
       expand_a(ra, cb ^ 1, kk >> 1, kk & 1);
-      if (kk & 1) load_a(ra, ta, kk >> 1);  // chunk kk/2 is expanded
     }
+    load_b(rb, tb, 1);
+    load_a(ra, ta, 1);
     __syncthreads();
     // keep the next stage's work below the barrier: hoisted above it, the
     // expansion of registers loaded in this stage would wait for those loads
