@@ -419,17 +419,25 @@ def time_graph(torch, g, reps):
 
 
 def time_stages(torch, stages, steps, warmup):
-    """Step time (whole hot path, one graph) and per-stage times (one graph each)."""
+    """Step time (the whole hot path replayed as one graph) and per-stage times
+    measured inside the step: right after the timed replays, the same steps
+    run once more with HIP events recorded on the stream between the stages,
+    so every stage is timed on the inputs its predecessors just wrote and at
+    the clock the step runs at (a kernel repeated on its own keeps its inputs
+    in the last-level cache and runs at a higher clock)."""
     step = capture(torch, [s.fn for s in stages])
     for _ in range(warmup):
         step.replay()
     step_s = time_graph(torch, step, steps)
-    per = {}
-    for s in stages:
-        # ten launches per graph, so one replay's submission cost is shared
-        g = capture(torch, [s.fn] * 10)
-        g.replay()
-        per[s.name] = time_graph(torch, g, max(4, steps // 2)) / 10
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(len(stages) + 1)] for _ in range(steps)]
+    torch.cuda.synchronize()
+    for e in ev:
+        e[0].record()
+        for i, s in enumerate(stages):
+            s.fn()
+            e[i + 1].record()
+    torch.cuda.synchronize()
+    per = {s.name: sum(e[i].elapsed_time(e[i + 1]) for e in ev) / 1e3 / steps for i, s in enumerate(stages)}
     return step_s, per
 
 
