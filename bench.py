@@ -431,6 +431,13 @@ def time_stages(torch, stages, steps, warmup):
     step_s = time_graph(torch, step, steps)
     ev = [[torch.cuda.Event(enable_timing=True) for _ in range(len(stages) + 1)] for _ in range(steps)]
     torch.cuda.synchronize()
+    # short steps: a spin kernel holds the GPU while the host enqueues every
+    # eager step, so the stages then run back to back (their kernels finish
+    # faster than the host could feed them one by one).  Long steps keep the
+    # GPU ahead of the host anyway and run right after the timed replays, in
+    # the same clock state.
+    if step_s < 3e-4:
+        torch.cuda._sleep(50_000_000)
     for e in ev:
         e[0].record()
         for i, s in enumerate(stages):
