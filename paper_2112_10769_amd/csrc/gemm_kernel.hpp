@@ -714,10 +714,10 @@ struct GemmPlan {
 static GemmPlan plan_gemm(int64_t M, int64_t N, int64_t K, int64_t max_exact_k) {
   GemmPlan p;
   auto tiles = [&](int bm, int bn) { return ((M + bm - 1) / bm) * ((N + bn - 1) / bn); };
-  // 256x256 tiles halve the expansion and LDS work per MAC but run one wave
-  // per SIMD; they pay off only for long reductions.  Short reductions (the
-  // conv dX with K = 64) are bound by the fp32 output and prefer the 128x128
-  // tile, which keeps two workgroups per CU.
+  // 256x256 tiles (the eight-wave kernel, one workgroup per CU) halve the
+  // expansion and LDS work per MAC; they pay off for long reductions.  Short
+  // reductions (the conv dX with K = 64) are bound by the fp32 output and
+  // prefer the 128x128 tile, which keeps two workgroups per CU.
   if (K >= 1024 && tiles(256, 256) >= 256) {
     p.bm = 256;
     p.bn = 256;
