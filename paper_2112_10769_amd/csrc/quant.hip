@@ -42,11 +42,15 @@ constexpr int kStatusWord = kMaxPartials + 1;
 constexpr uint32_t kStatusNonfinite = 8;  // LUQ_ERR_NONFINITE
 // Tensors above kCacheBytes (the 256 MB last-level cache) are streamed: the
 // max pass reads all but the last kKeepBytes of them non-temporally and the
-// encode pass, whose loads and code stores are then non-temporal too, walks
-// the tensor from its end, so that it starts on the part the max pass left
-// in the cache.
+// encode pass, whose loads (and LUQ code stores) are then non-temporal too,
+// walks the tensor from its end, so that it starts on the part the max pass
+// left in the cache.
 constexpr int64_t kCacheBytes = 256LL << 20;
 constexpr int64_t kKeepBytes = 192LL << 20;
+// INT4 tensors stream from a lower size: a tensor as large as the cache does not
+// stay in it beside the other data of a training step, and the INT4 encode is
+// bound by memory (the LUQ encode, bound by its ALU work, keeps kCacheBytes).
+constexpr int64_t kInt4StreamBytes = 160LL << 20;
 
 // Max-pass keys.  MODE 0: |x| (LUQ, signed INT4).  MODE 1: max(x, 0) with
 // non-finite values of either sign kept (unsigned INT4).
@@ -213,11 +217,11 @@ __device__ __forceinline__ void encode_tiles(const Enc& enc, int64_t rows, int64
               smp_sum_bytes(w[0], w[1], lo, hi);
               w[0] = lo;
               w[1] = hi;
-              if (codes) store_word2<Enc::kNT>(codes + T.e0[u], lo, hi);
+              if (codes) store_word2<Enc::kNTStore>(codes + T.e0[u], lo, hi);
             } else {
 #pragma unroll
               for (int s = 0; s < NS; ++s)
-                if (codes) store_word<Enc::kNT>(codes + s * plane + (T.e0[u] >> 1), w[s]);
+                if (codes) store_word<Enc::kNTStore>(codes + s * plane + (T.e0[u] >> 1), w[s]);
             }
           }
 #pragma unroll
@@ -267,11 +271,11 @@ __device__ __forceinline__ void encode_tiles(const Enc& enc, int64_t rows, int64
               smp_sum_bytes(w[0], w[1], lo, hi);
               w[0] = lo;
               w[1] = hi;
-              if (codes) store_word2<Enc::kNT>(codes + e0[u], lo, hi);
+              if (codes) store_word2<Enc::kNTStore>(codes + e0[u], lo, hi);
             } else {
 #pragma unroll
               for (int s = 0; s < NS; ++s)
-                if (codes) store_word<Enc::kNT>(codes + s * plane + (e0[u] >> 1), w[s]);
+                if (codes) store_word<Enc::kNTStore>(codes + s * plane + (e0[u] >> 1), w[s]);
             }
           }
 #pragma unroll
@@ -297,7 +301,7 @@ __device__ __forceinline__ void encode_tiles(const Enc& enc, int64_t rows, int64
           transpose4x4_bytes(ra, ca);   // rows 0..3
           transpose4x4_bytes(rb4, cb);  // rows 4..7
 #pragma unroll
-          for (int c = 0; c < 4; ++c) store_word2<Enc::kNT>(dst + (h * 4 + c) * rows, ca[c], cb[c]);
+          for (int c = 0; c < 4; ++c) store_word2<Enc::kNTStore>(dst + (h * 4 + c) * rows, ca[c], cb[c]);
         }
         continue;
       }
@@ -309,7 +313,7 @@ __device__ __forceinline__ void encode_tiles(const Enc& enc, int64_t rows, int64
         transpose8x8_nibbles(w8);
         uint8_t* dst = codes_t + s * plane + (cg * 8) * (rows >> 1) + (row0 >> 1);
 #pragma unroll
-        for (int c = 0; c < 8; ++c) store_word<Enc::kNT>(dst + c * (rows >> 1), w8[c]);
+        for (int c = 0; c < 8; ++c) store_word<Enc::kNTStore>(dst + c * (rows >> 1), w8[c]);
       }
     }
     __syncthreads();
@@ -650,6 +654,7 @@ struct LuqEnc {
   static constexpr bool kTrack = HS;
   static constexpr bool kPipeline = true;  // ALU-heavy words: overlap the next loads with them
   static constexpr bool kNT = NT;
+  static constexpr bool kNTStore = NT;
   const LuqArgs* a;
   const LuqParams* p;
   __device__ U8 load(int64_t e0) const { return load8<BF16, NT>(a->g, e0); }
@@ -792,7 +797,7 @@ __global__ __launch_bounds__(kThreads) void int4_encode_flat_kernel(Int4Args a) 
     const U8 v = full ? load8<BF16, NT>(a.x, g * 8) : load8_tail<BF16>(a.x, g * 8, a.n);
     const uint32_t word = p.zero ? 0u : int4_word(v, p);
     if (full)
-      store_word<NT>(a.codes + g * 4, word);
+      store_word<false>(a.codes + g * 4, word);
     else
       store_bytes(a.codes + g * 4, word, (int)((a.n - g * 8 + 1) >> 1));
   }
@@ -803,6 +808,9 @@ struct Int4Enc {
   static constexpr bool kTrack = false;
   static constexpr bool kPipeline = false;  // memory-bound: the plain trips measure faster
   static constexpr bool kNT = NT;
+  // the GEMM that follows reads the INT4 codes: keep them in the cache even
+  // when the tensor itself is streamed
+  static constexpr bool kNTStore = false;
   const Int4Args* a;
   const Int4Params* p;
   __device__ U8 load(int64_t e0) const { return load8<BF16, NT>(a->x, e0); }
@@ -942,8 +950,9 @@ static TileShape tile_shape(int64_t rows, int64_t cols, int max_lt) {
 // with non-temporal loads, except for their last kKeepBytes.
 
 template <bool BF16, int MODE>
-static void launch_max_pass(const void* x, int64_t n, int nblocks, uint32_t* partial, hipStream_t st) {
-  if (n * (BF16 ? 2 : 4) > kCacheBytes)
+static void launch_max_pass(const void* x, int64_t n, int nblocks, uint32_t* partial, hipStream_t st,
+                            int64_t stream_bytes = kCacheBytes) {
+  if (n * (BF16 ? 2 : 4) > stream_bytes)
     hipLaunchKernelGGL((max_partial_kernel<BF16, MODE, true>), dim3(nblocks), dim3(kThreads), 0, st, x, n,
                        partial);
   else
@@ -1139,12 +1148,12 @@ static hipError_t int4_launch_t(Int4Args a, hipStream_t st) {
   }
   if (a.clip <= 0.0f) {
     if (a.is_signed)
-      launch_max_pass<BF16, 0>(a.x, a.n, a.nparts, const_cast<uint32_t*>(a.partial), st);
+      launch_max_pass<BF16, 0>(a.x, a.n, a.nparts, const_cast<uint32_t*>(a.partial), st, kInt4StreamBytes);
     else
-      launch_max_pass<BF16, 1>(a.x, a.n, a.nparts, const_cast<uint32_t*>(a.partial), st);
+      launch_max_pass<BF16, 1>(a.x, a.n, a.nparts, const_cast<uint32_t*>(a.partial), st, kInt4StreamBytes);
     a.partial = encode_partials(a.partial, a.nparts, &a.nparts);
   }
-  const bool nt = stream_reads(a.n, BF16);
+  const bool nt = a.n * (BF16 ? 2 : 4) > kInt4StreamBytes;
   if (a.codes_t) {
     const TileShape t = tile_shape(a.rows, a.cols, kInt4TileLg);
     if (nt)
