@@ -456,7 +456,11 @@ __device__ __forceinline__ uint32_t as_u32(s16x2 x) { return __builtin_bit_cast(
 // paired (i, i+4), so a pair's base fields land in nibbles i and i+4 with one
 // shift-or, and the 16-bit bin index equals the 32-bit one:
 // ((a - a1) << 16) >> 23 = (a - a1) >> 7 for 16-bit a, a1 (|a - a1| < 2^15).
-// The rounding decision per element is luq_word's fused multiply-add.
+// The rounding decision per element is luq_word's fused multiply-add.  CAP
+// (an estimated maximum) clamps the base fields to the top one and drops the
+// round-up there, as luq_word does; the bin widths of elements above the top
+// level are then garbage, but their round-up bits are the dropped ones.
+template <bool CAP = false>
 __device__ __forceinline__ uint32_t luq_word_bf16(const U8& v, uint64_t blk, uint32_t sample, uint32_t counter,
                                                   uint32_t k0, uint32_t k1, const LuqParams& p) {
   const U4 y = philox4x32_10(U4{(uint32_t)blk, (uint32_t)(blk >> 32), sample, counter}, k0, k1);
@@ -466,6 +470,7 @@ __device__ __forceinline__ uint32_t luq_word_bf16(const U8& v, uint64_t blk, uin
 #pragma unroll
   for (int i = 0; i < 4; ++i) q[i] = (v.v[2 * i] >> 16) | (v.v[2 * i + 1] & 0xFFFF0000u);
   const s16x2 a1 = as_s16x2((p.a1_bits >> 16) * 0x10001u);
+  const s16x2 top = as_s16x2(p.top_field * 0x10001u);
   uint32_t base = 0, sg = 0;
   U8 r;
 #pragma unroll
@@ -475,7 +480,8 @@ __device__ __forceinline__ uint32_t luq_word_bf16(const U8& v, uint64_t blk, uin
     sg |= ((pr >> 12) & 0x00080008u) << (4 * i);    // signs of elements i, i+4 at bits 4i+3, 4i+19
     const uint32_t pm = pr & 0x7FFF7FFFu;
     const s16x2 n1 = (as_s16x2(pm) - a1) >> 7;
-    const s16x2 f0 = __builtin_elementwise_max(n1, (s16x2){0, 0});
+    s16x2 f0 = __builtin_elementwise_max(n1, (s16x2){0, 0});
+    if constexpr (CAP) f0 = __builtin_elementwise_min(f0, top);
     uint32_t ge;  // [n1 >= 1] per half, one packed min (the compiler would compare and select)
     asm("v_pk_min_i16 %0, %1, %2" : "=v"(ge) : "v"(as_u32(f0)), "s"(0x00010001u));
     const uint32_t m1 = as_u32(__builtin_elementwise_max(n1, (s16x2){1, 1}));
@@ -488,7 +494,11 @@ __device__ __forceinline__ uint32_t luq_word_bf16(const U8& v, uint64_t blk, uin
     r.v[i] = __float_as_uint(fmaf((float)jj_lo, w16_lo, -__uint_as_float(pm << 16)));
     r.v[i + 4] = __float_as_uint(fmaf((float)jj_hi, w16_hi, -__uint_as_float(pm & 0xFFFF0000u)));
   }
-  const uint32_t up = (gather_signs(r) >> 3) & 0x11111111u;
+  uint32_t up = (gather_signs(r) >> 3) & 0x11111111u;
+  if constexpr (CAP) {
+    const uint32_t t = base ^ (0x11111111u * p.top_field);
+    up &= (t | (t >> 1) | (t >> 2));  // bit 4e set unless field e is the top one
+  }
   const uint32_t fields = base + up;
   const uint32_t nz = (fields | (fields >> 1) | (fields >> 2)) & 0x11111111u;
   return fields | (sg & (nz << 3));
@@ -542,7 +552,7 @@ __device__ __forceinline__ LuqParams luq_block_params(const LuqArgs& a) {
 template <bool BF16, bool SCALED, bool HS>
 __device__ __forceinline__ uint32_t luq_code_word(const U8& v, uint64_t blk, uint32_t sample, const LuqArgs& a,
                                                   const LuqParams& p) {
-  if constexpr (BF16 && !SCALED && !HS) return luq_word_bf16(v, blk, sample, a.counter, a.k0, a.k1, p);
+  if constexpr (BF16 && !SCALED) return luq_word_bf16<HS>(v, blk, sample, a.counter, a.k0, a.k1, p);
   return luq_word<SCALED, HS>(v, blk, sample, a.counter, a.k0, a.k1, p);
 }
 

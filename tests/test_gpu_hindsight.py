@@ -2,7 +2,7 @@
 (luq_quantize_grad_hindsight) against the oracle: codes, alpha, the measured
 maximum and the updated estimate bit-exact, over ragged and tiled shapes,
 both dtypes, one and two SMP planes, estimates below, at and above the
-tensor's maximum, degenerate estimates and non-finite elements.
+tensor's maximum, degenerate estimates and non-finite elements (fp32 and bf16).
 """
 import numpy as np
 import pytest
@@ -70,6 +70,19 @@ def test_hindsight_tiles(L, shape, ns):
     _check(L, x, r, c, m_hat, R=5 if ns == 2 else 4, seed=r + c, counter=1, ns=ns, want_t=True, what="tile")
 
 
+@pytest.mark.parametrize("shape", [(264, 200), (1024, 392)])
+@pytest.mark.parametrize("ns", [1, 2])
+@pytest.mark.parametrize("frac", [0.3, 1.0])
+def test_hindsight_tiles_bf16(L, shape, ns, frac):
+    """bf16 tiles (the packed 16-bit encoder with the top field capped): an
+    estimate at 0.3 of the maximum clips every element above its top level."""
+    r, c = shape
+    x = synth.to_bf16_bits(synth.lognormal_grad((r, c), -10.0, 2.5, 0.3, [r, c, 7]))
+    m_hat = np.float32(np.abs(synth.bf16_bits_to_f32(x)).max() * frac)
+    _check(L, x, r, c, m_hat, R=5 if ns == 2 else 4, seed=r + c, counter=2, ns=ns, want_t=True,
+           what=f"bf16 tile x{frac}")
+
+
 @pytest.mark.parametrize("R", [4, 5, 6])
 def test_hindsight_R_and_eta(L, R):
     x = synth.grad_1d(70001, "f32", 0.1, seed=R)
@@ -91,6 +104,17 @@ def test_hindsight_nonfinite_elements(L):
     _check(L, y, 1, y.size, np.float32(np.abs(x).max()), what="inf elements")
     y[999] = np.nan
     _check(L, y, 1, y.size, np.float32(np.abs(x).max()), what="nan element")
+
+
+@pytest.mark.parametrize("R", [4, 6])
+def test_hindsight_nonfinite_elements_bf16(L, R):
+    """bf16 Inf, -Inf and NaN elements under an estimate: clipped to the top
+    code with their sign, like every element above the top level."""
+    x = synth.grad_1d(70000, "bf16", 0.2, seed=13)
+    m_hat = np.float32(np.abs(synth.bf16_bits_to_f32(x)).max() * 0.5)
+    y = x.copy()
+    y[123], y[4567], y[999], y[1001] = 0x7F80, 0xFF80, 0x7FC0, 0xFFC1  # +Inf, -Inf, NaN, -NaN
+    _check(L, y, 1, y.size, m_hat, R=R, what=f"bf16 non-finite R={R}")
 
 
 def test_hindsight_empty_and_sequence(L):
