@@ -448,9 +448,19 @@ __global__ __launch_bounds__(kGemmThreads, BK == 64 ? 3 : 1) void gemm_luq_int4_
 // with B registers set t%2, while the A codes of stage t+1 are expanded into
 // the other buffer; each A chunk and each B half-segment is reloaded (A with
 // stage t+3, B with stage t+2) as soon as its registers are consumed.
+//
+// PF sets how far ahead the MFMA operands are fetched, so that the LDS read
+// latency is covered by the previous k-step's MFMAs:
+//   0: each k-step's fragments are read and expanded just before its MFMAs;
+//   1: the A fragments of k-step kk+1 are read while kk is multiplied;
+//   2: as 1, and the B fragments of kk+1 are expanded during kk too;
+//   3: as 2 across the stage boundary as well (the next stage's first B
+//      fragments at the last k-step), with the B reload one k-step earlier.
+// Every mode sums the same products; the launcher picks the deepest mode that
+// fits the 256 registers of two waves per SIMD for the operand kinds.
 constexpr int kW8Threads = 512;
 
-template <int AC, int NS, bool BSIGNED, bool FULLK>
+template <int AC, int NS, bool BSIGNED, bool FULLK, int PF>
 __global__ __launch_bounds__(kW8Threads, 1) void gemm_w8_kernel(GemmArgs a) {
   constexpr int BM = 256, kBK = 128, kThr = kW8Threads;
   constexpr int kPitch = kBK + 16;        // A row: 8 slots of 16 bytes, 16 bytes of pad
@@ -573,24 +583,52 @@ __global__ __launch_bounds__(kW8Threads, 1) void gemm_w8_kernel(GemmArgs a) {
     }
   };
 
-  auto step = [&](int cb, ARegs& ra, int ta, BRegs& rb, int tb) {
+  // fragments fetched one k-step ahead (PF >= 1), carried across stages (PF 3)
+  v4i fa2[2][TM], fb2[2][TN];
+  auto mma = [&](const v4i (&fa)[TM], const v4i (&fb)[TN]) {
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+      for (int j = 0; j < TN; ++j)
+        acc[i][j] = __builtin_amdgcn_mfma_i32_32x32x32_i8(fb[j], fa[i], acc[i][j], 0, 0, 0);
+  };
+  // multiply stage t from buffer cb and B set rb while expanding the A codes
+  // of stage t+1 (ra) into the other buffer; rbn is the next stage's B set
+  auto step = [&](int cb, ARegs& ra, int ta, BRegs& rb, int tb, const BRegs& rbn) {
+    if constexpr (PF >= 1) read_a(cb, 0, fa2[0]);
+    if constexpr (PF == 2) frag_b(rb, 0, fb2[0]);
 #pragma unroll
     for (int kk = 0; kk < 4; ++kk) {
-      if (kk == 2) {
-        // the first B half-segment and A chunk are consumed: reload them now
-        // (the scheduler would otherwise sink the loads to the barrier)
+      // the first B half-segment and A chunk are consumed: reload them now
+      // (the scheduler would otherwise sink the loads to the barrier)
+      if (kk == (PF == 3 ? 1 : 2)) {
         load_b(rb, tb, 0);
+        if (PF != 3) load_a(ra, ta, 0);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+      if (PF == 3 && kk == 2) {
         load_a(ra, ta, 0);
         __builtin_amdgcn_sched_barrier(0);
       }
-      v4i fa[TM], fb[TN];
-      read_a(cb, kk, fa);
-      frag_b(rb, kk, fb);
-#pragma unroll
-      for (int i = 0; i < TM; ++i)
-#pragma unroll
-        for (int j = 0; j < TN; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_i32_32x32x32_i8(fb[j], fa[i], acc[i][j], 0, 0, 0);
+      if constexpr (PF == 0) {
+        v4i fa[TM], fb[TN];
+        read_a(cb, kk, fa);
+        frag_b(rb, kk, fb);
+        mma(fa, fb);
+      } else if constexpr (PF == 1) {
+        v4i fb[TN];
+        if (kk + 1 < 4) read_a(cb, kk + 1, fa2[(kk + 1) & 1]);
+        frag_b(rb, kk, fb);
+        mma(fa2[kk & 1], fb);
+      } else {
+        if (kk + 1 < 4) {
+          read_a(cb, kk + 1, fa2[(kk + 1) & 1]);
+          frag_b(rb, kk + 1, fb2[(kk + 1) & 1]);
+        } else if (PF == 3) {
+          frag_b(rbn, 0, fb2[0]);
+        }
+        mma(fa2[kk & 1], fb2[kk & 1]);
+      }
       expand_a(ra, cb ^ 1, kk >> 1, kk & 1);
     }
     load_b(rb, tb, 1);
@@ -613,15 +651,16 @@ __global__ __launch_bounds__(kW8Threads, 1) void gemm_w8_kernel(GemmArgs a) {
   load_b(b1, 1, 1);
 #pragma unroll
   for (int kk = 0; kk < 4; ++kk) expand_a(r0, 0, kk >> 1, kk & 1);
+  if constexpr (PF == 3) frag_b(b0, 0, fb2[0]);
   __syncthreads();
 #pragma unroll
   for (int i = 0; i < ACH; ++i) load_a(r0, 2, i);
   int t = 0;
   for (; t + 2 <= nkt; t += 2) {
-    step(0, r1, t + 3, b0, t + 2);  // multiply t, expand t+1 (r1); reload r1 with t+3, b0 with t+2
-    step(1, r0, t + 4, b1, t + 3);  // multiply t+1, expand t+2 (r0); reload r0 with t+4, b1 with t+3
+    step(0, r1, t + 3, b0, t + 2, b1);  // multiply t, expand t+1 (r1); reload r1 with t+3, b0 with t+2
+    step(1, r0, t + 4, b1, t + 3, b0);  // multiply t+1, expand t+2 (r0); reload r0 with t+4, b1 with t+3
   }
-  if (t < nkt) step(0, r1, t + 3, b0, t + 2);
+  if (t < nkt) step(0, r1, t + 3, b0, t + 2, b1);
 
   // Epilogue through LDS, as in the four-wave kernel: each wave stages 32 rows
   // of its 128 x 64 block at a time and stores whole 256-byte row segments.
@@ -779,10 +818,14 @@ static hipError_t gemm_launch_t(const GemmArgs& a0, const GemmPlan& p, hipStream
   // 16-byte stores need 16-byte aligned rows
   a.vec = (a.N % 4) == 0 && (((uintptr_t)(a.partial ? (void*)a.partial : (void*)a.C)) & 15) == 0;
   if (p.bm == 256) {
+    // prefetch depth by register budget (deeper modes spill where not taken)
+    constexpr bool kLuq1 = AC == kAcLuq && NS == 1;
+    constexpr int kPfFull = AC == kAcSum2 ? (BSIGNED ? 3 : 2) : kLuq1 ? 2 : 1;
+    constexpr int kPfPart = AC == kAcSum2 || kLuq1 ? 2 : AC == kAcLuq ? 0 : 1;
     if (a.K % kKAlign == 0)
-      hipLaunchKernelGGL((gemm_w8_kernel<AC, NS, BSIGNED, true>), grid, dim3(kW8Threads), 0, st, a);
+      hipLaunchKernelGGL((gemm_w8_kernel<AC, NS, BSIGNED, true, kPfFull>), grid, dim3(kW8Threads), 0, st, a);
     else
-      hipLaunchKernelGGL((gemm_w8_kernel<AC, NS, BSIGNED, false>), grid, dim3(kW8Threads), 0, st, a);
+      hipLaunchKernelGGL((gemm_w8_kernel<AC, NS, BSIGNED, false, kPfPart>), grid, dim3(kW8Threads), 0, st, a);
   }
   else if (p.bm == 128 && p.bk == 64)
     launch_tile<128, 128, 64, AC, NS, BSIGNED>(a, grid, st);
