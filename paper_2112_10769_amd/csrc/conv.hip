@@ -770,6 +770,352 @@ __global__ __launch_bounds__(kRedThreads) void conv_wgrad_reduce_kernel(const in
   }
 }
 
+// ---------------------------------------------------------------------------
+// Weight gradient, row form (W <= 64, C and Cout multiples of 32).  A
+// workgroup owns one 32 x 32 (o, c) block of all nine taps over a range of
+// image rows; each of its eight waves keeps the nine accumulator tiles of
+// that block for its own run of rows, so every operand code is expanded
+// once per workgroup and the expanded operands never pass through LDS.
+//
+// With r = b*H + y the flat image row and t = r*W + x, the tap (kh, kw) term
+// of pixel t reads the activation at flat row r + kh - 1, column x + kw - 1.
+// A row is multiplied as ceil(W / 32) k-steps of 32 columns (columns past W
+// carry zero gradient codes).  The raw codes of a chunk of rows (the
+// gradient rows, and the activation rows with one more on either side) are
+// staged in LDS by coalesced 16-byte loads, each channel's codes contiguous
+// as in memory.  In one k-step a lane takes 16 gradient codes of channel o
+// and, for each kernel row kh, the 16 activation codes of channel c at
+// columns x + kw - 1, cut by funnel shifts from one 4-dword window of that
+// activation row: an activation row is read and expanded once per wave and
+// serves the three kernel rows of three consecutive gradient rows.  Column
+// x + kw - 1 off the row (x = 0 with kw = 0, x = W - 1 with kw = 2) is
+// cleared; a kernel row off the image (y + kh - 1 outside [0, H)) skips its
+// three MFMAs.  Both operands use the GEMMs' expansions, which share one k
+// permutation, so the products summed are the same.  The eight waves add
+// their tiles through LDS; the workgroup writes the int32 sums of its block
+// for its row range, and conv_wgrad_reduce_kernel adds the ranges in int64
+// (with one range the scales are applied directly).
+// ---------------------------------------------------------------------------
+constexpr int kWrThreads = 512;
+constexpr int kWrWaves = kWrThreads / 64;
+constexpr int kWrLdsBytes = kWrWaves / 2 * 9 * 4 * 64 * 16;   // the tile sums; the staging reuses it
+// pixels one workgroup sums in int32: 2^18 - 64 (a row of slack) times at
+// most 64 * 120 per term stays below 2^31
+constexpr int64_t kWrMaxPixels = ((int64_t)1 << 18) - 64;
+
+// dwords staged per channel for n rows of width W: from the 16-byte block
+// holding the first code (up to 31 codes before it), through the last k-step
+// window (up to 64 + 16 codes past the rows' start of the last row), a
+// multiple of 4; the LDS pitch adds one dword so that channels fall in
+// different banks
+__host__ __device__ constexpr int wr_seg_dwords(int n, int W) { return ((n * W + 31 + 80) / 8 + 4 + 3) / 4 * 4; }
+
+struct ConvWrArgs {
+  const uint8_t* g;      // LUQ codes [Cout][T], ns planes
+  int64_t g_plane;
+  const uint8_t* a;      // INT4 codes [C][T]
+  const float* alpha;
+  const float* ascale;
+  float* dw;             // [Cout][9C]
+  int32_t* partial;      // [nr][Cout][9C] int32 sums of the row ranges, or null (nr == 1)
+  int T, H, W, C, Cout;
+  int rows;              // B * H
+  int nr;                // row ranges
+  int ch;                // rows per staged chunk
+  int oblk, cblk;        // 32-wide channel blocks
+  int vec;               // 16-byte stores of dW rows
+};
+
+template <int NS, bool ASIGNED>
+__global__ __launch_bounds__(kWrThreads, 1) void conv3x3_wgrad_rows_kernel(ConvWrArgs a) {
+  __shared__ __attribute__((aligned(16))) uint32_t lds[kWrLdsBytes / 4];
+  const int tid = threadIdx.x, lane = tid & 63;
+  // the wave index in a scalar register: the row bounds, offsets and branches
+  // derived from it are then wave-uniform scalar work
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int r32 = lane & 31, h = lane >> 5;
+  // blocks are dispatched round-robin over the XCDs: give each XCD runs of
+  // consecutive (range, block) indices, whose blocks share operand rows
+  const int total = a.nr * a.oblk * a.cblk;
+  int L = blockIdx.x;
+  if ((total & 7) == 0) L = (L & 7) * (total >> 3) + (L >> 3);
+  const int cbk = L % a.cblk, obk = (L / a.cblk) % a.oblk, range = L / (a.cblk * a.oblk);
+  const int rr0 = (int)((int64_t)range * a.rows / a.nr);
+  const int rr1 = (int)((int64_t)(range + 1) * a.rows / a.nr);
+  const int nk = (a.W + 31) >> 5;            // k-steps per row
+
+  __amdgpu_buffer_rsrc_t rsg[NS];
+#pragma unroll
+  for (int s = 0; s < NS; ++s)
+    rsg[s] = __builtin_amdgcn_make_buffer_rsrc((void*)(a.g + s * a.g_plane), (short)0,
+                                               (int)(((int64_t)a.Cout * a.T) >> 1), kBufferFlags);
+  const __amdgpu_buffer_rsrc_t rsa =
+      __builtin_amdgcn_make_buffer_rsrc((void*)a.a, (short)0, (int)(((int64_t)a.C * a.T) >> 1), kBufferFlags);
+
+  // gradient columns past W: per-lane masks of the 16 codes, per k-step
+  uint32_t mg[2][2];
+#pragma unroll
+  for (int k = 0; k < 2; ++k) {
+    const int v = a.W - 32 * k - 16 * h;    // valid codes of the lane's 16
+    mg[k][0] = v >= 8 ? ~0u : (v <= 0 ? 0u : (1u << (4 * v)) - 1u);
+    mg[k][1] = v >= 16 ? ~0u : (v <= 8 ? 0u : (1u << (4 * (v - 8))) - 1u);
+  }
+  // activation columns off the row: x = 0 with kw = 0 (k-step 0, lane half 0,
+  // code 0) and x = W - 1 with kw = 2
+  const uint32_t mleft = h == 0 ? ~0xFu : ~0u;
+  const int xe = a.W - 1, ke = xe >> 5, he = (xe >> 4) & 1, je = xe & 15;
+  const uint32_t mright0 = (h == he && je < 8) ? ~(0xFu << (4 * je)) : ~0u;
+  const uint32_t mright1 = (h == he && je >= 8) ? ~(0xFu << (4 * (je - 8))) : ~0u;
+
+  v16i acc[9];
+#pragma unroll
+  for (int t = 0; t < 9; ++t) acc[t] = v16i{};
+
+  struct Raw {
+    uint32_t g[NS][3];
+    uint32_t x[4];
+  };
+
+  for (int cr0 = rr0; cr0 < rr1; cr0 += a.ch) {
+    const int nrow = min(a.ch, rr1 - cr0);
+    // ---- stage the raw codes of the chunk: per channel, dwords from the
+    // 16-byte block holding the first code; T is a multiple of 32, so every
+    // channel's block starts at the same offset of its row range
+    const int segg = wr_seg_dwords(nrow, a.W), sega = wr_seg_dwords(nrow + 2, a.W);
+    const int pg = segg + 1, pa = sega + 1;
+    uint32_t* ldsg = lds;                    // [NS][32][pg]
+    uint32_t* ldsa = lds + NS * 32 * pg;     // [32][pa]
+    const int64_t g0 = ((int64_t)cr0 * a.W) >> 5 << 2;             // dword of row cr0's first code, 16-B block
+    const int64_t a0 = ((int64_t)(cr0 - 1) * a.W - 1) >> 5 << 2;   // column -1 of row cr0 - 1 (floor)
+    __syncthreads();  // the previous chunk is consumed
+    {
+      // 16-byte pieces: NS * 32 gradient segments of qg, then 32 activation
+      // segments of qa; eight loads of a thread in flight before its stores
+      const int qg = segg / 4, qa = sega / 4;
+      const int ng = NS * 32 * qg, ntot = ng + 32 * qa;
+      constexpr int kBatch = 8;
+      for (int u0 = tid; u0 < ntot; u0 += kBatch * kWrThreads) {
+        v4u v[kBatch];
+        int dst[kBatch];
+#pragma unroll
+        for (int b = 0; b < kBatch; ++b) {
+          const int u = u0 + b * kWrThreads;
+          dst[b] = -1;
+          if (u < ng) {
+            const int p = u / (32 * qg), rem = u - p * 32 * qg, k = rem / qg, j = rem - k * qg;
+            const int64_t dwi = (int64_t)(obk * 32 + k) * (a.T >> 3) + g0 + 4 * j;
+            v[b] = __builtin_amdgcn_raw_buffer_load_b128(rsg[p == 0 ? 0 : NS - 1], (int)(dwi << 2), 0, 0);
+            dst[b] = (p * 32 + k) * pg + 4 * j;
+          } else if (u < ntot) {
+            const int rem = u - ng, k = rem / qa, j = rem - k * qa;
+            const int64_t dwi = (int64_t)(cbk * 32 + k) * (a.T >> 3) + a0 + 4 * j;
+            v[b] = __builtin_amdgcn_raw_buffer_load_b128(rsa, dwi < 0 ? kOutOfRange : (int)(dwi << 2), 0, 0);
+            dst[b] = NS * 32 * pg + k * pa + 4 * j;
+          }
+        }
+#pragma unroll
+        for (int b = 0; b < kBatch; ++b)
+          if (dst[b] >= 0) {
+#pragma unroll
+            for (int e = 0; e < 4; ++e) lds[dst[b] + e] = v[b][e];
+          }
+      }
+    }
+    __syncthreads();
+
+    // ---- this wave's rows of the chunk, one pass per k-step: step i reads
+    // activation row r0 - 1 + i and, for i >= 2, multiplies gradient row
+    // r0 - 2 + i
+    const int r0 = cr0 + (wave * nrow) / kWrWaves, r1 = cr0 + ((wave + 1) * nrow) / kWrWaves;
+    const int n = r1 - r0, per = n + 2;
+    const uint32_t* lg = ldsg + r32 * pg + 2 * h;
+    const uint32_t* la = ldsa + r32 * pa + 2 * h;
+    const int ga = (int)a0, gg = (int)g0;
+    for (int kst = 0; kst < (n > 0 ? nk : 0); ++kst) {
+      // code offsets (within a channel) of the window start and of the
+      // gradient chunk at step 0; they advance by W per step
+      const int xa0 = (r0 - 1) * a.W + 32 * kst - 1;
+      const int xg0 = (r0 - 2) * a.W + 32 * kst;
+      int yy = r0 % a.H;  // image row of the next gradient row
+      auto load = [&](Raw& R, int i) {
+        if (i >= per) return;
+        const int qa = ((xa0 + i * a.W) >> 3) - ga;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) R.x[j] = la[qa + j];
+        if (i >= 2) {
+          const int qg = ((xg0 + i * a.W) >> 3) - gg;
+#pragma unroll
+          for (int p = 0; p < NS; ++p)
+#pragma unroll
+            for (int j = 0; j < 3; ++j) R.g[p][j] = lg[p * 32 * pg + qg + j];
+        }
+      };
+      // the three shifted activation fragments of a window
+      auto expand_x = [&](const Raw& R, v4i (&w)[3], int i) {
+        const int ob = (xa0 + i * a.W) & 7;
+#pragma unroll
+        for (int kw = 0; kw < 3; ++kw) {
+          const int sh = ob + kw;
+          uint32_t x0, x1;
+          if (sh < 8) {
+            x0 = __builtin_amdgcn_alignbit(R.x[1], R.x[0], 4 * sh);
+            x1 = __builtin_amdgcn_alignbit(R.x[2], R.x[1], 4 * sh);
+          } else {
+            x0 = __builtin_amdgcn_alignbit(R.x[2], R.x[1], 4 * (sh - 8));
+            x1 = __builtin_amdgcn_alignbit(R.x[3], R.x[2], 4 * (sh - 8));
+          }
+          if (kw == 0 && kst == 0) x0 &= mleft;
+          if (kw == 2 && kst == ke) {
+            x0 &= mright0;
+            x1 &= mright1;
+          }
+          uint32_t l0, h0, l1, h1;
+          expand_int4<ASIGNED>(x0, l0, h0);
+          expand_int4<ASIGNED>(x1, l1, h1);
+          w[kw] = v4i{(int)l0, (int)h0, (int)l1, (int)h1};
+        }
+      };
+      auto expand_g = [&](const Raw& R, int i) {
+        const int sg = 4 * ((xg0 + i * a.W) & 7);
+        const uint32_t m0 = kst ? mg[1][0] : mg[0][0], m1 = kst ? mg[1][1] : mg[0][1];
+        uint32_t w[4];
+        if constexpr (NS == 1) {
+          const uint32_t x0 = __builtin_amdgcn_alignbit(R.g[0][1], R.g[0][0], sg) & m0;
+          const uint32_t x1 = __builtin_amdgcn_alignbit(R.g[0][2], R.g[0][1], sg) & m1;
+          expand_luq(x0, w[0], w[1]);
+          expand_luq(x1, w[2], w[3]);
+        } else {
+#pragma unroll
+          for (int d = 0; d < 2; ++d) {
+            const uint32_t m = d ? m1 : m0;
+            const uint32_t p0 = __builtin_amdgcn_alignbit(R.g[0][d + 1], R.g[0][d], sg) & m;
+            const uint32_t p1 = __builtin_amdgcn_alignbit(R.g[1][d + 1], R.g[1][d], sg) & m;
+            uint32_t l0, h0, l1, h1;
+            expand_luq_excess64(p0, l0, h0);
+            expand_luq_excess64(p1, l1, h1);
+            w[2 * d] = (l0 + l1) ^ 0x80808080u;
+            w[2 * d + 1] = (h0 + h1) ^ 0x80808080u;
+          }
+        }
+        return v4i{(int)w[0], (int)w[1], (int)w[2], (int)w[3]};
+      };
+      // step i: expand the activation window into wj; for a gradient row
+      // (i >= 2) multiply it with the windows of rows r - 1 (w0), r (w1) and
+      // r + 1 (wj)
+      auto step = [&](int i, v4i (&wj)[3], const v4i (&w0)[3], const v4i (&w1)[3]) {
+        if (i >= per) return;
+        Raw R;
+        load(R, i);
+        expand_x(R, wj, i);
+        v4i fa = v4i{};
+        if (i >= 2) fa = expand_g(R, i);
+        if (i >= 2) {
+          const int y = yy;
+          yy = y + 1 == a.H ? 0 : y + 1;
+          if (y > 0) {
+#pragma unroll
+            for (int kw = 0; kw < 3; ++kw)
+              acc[kw] = __builtin_amdgcn_mfma_i32_32x32x32_i8(w0[kw], fa, acc[kw], 0, 0, 0);
+          }
+#pragma unroll
+          for (int kw = 0; kw < 3; ++kw)
+            acc[3 + kw] = __builtin_amdgcn_mfma_i32_32x32x32_i8(w1[kw], fa, acc[3 + kw], 0, 0, 0);
+          if (y < a.H - 1) {
+#pragma unroll
+            for (int kw = 0; kw < 3; ++kw)
+              acc[6 + kw] = __builtin_amdgcn_mfma_i32_32x32x32_i8(wj[kw], fa, acc[6 + kw], 0, 0, 0);
+          }
+        }
+      };
+
+      v4i win[3][3];
+      for (int i = 0; i < per; i += 3) {
+        step(i, win[0], win[1], win[2]);
+        step(i + 1, win[1], win[2], win[0]);
+        step(i + 2, win[2], win[0], win[1]);
+      }
+    }
+  }
+
+  // add the eight waves' tiles: 4 -> 2 -> 1 through LDS
+  v4i* red = reinterpret_cast<v4i*>(lds);   // [4][9][4][64]
+#pragma unroll
+  for (int half = kWrWaves / 2; half >= 1; half >>= 1) {
+    __syncthreads();  // the LDS is free (staging consumed, or the previous half read)
+    if (wave >= half && wave < 2 * half) {
+#pragma unroll
+      for (int t = 0; t < 9; ++t)
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+          red[(((wave - half) * 9 + t) * 4 + q) * 64 + lane] =
+              v4i{acc[t][4 * q], acc[t][4 * q + 1], acc[t][4 * q + 2], acc[t][4 * q + 3]};
+    }
+    __syncthreads();
+    if (wave < half) {
+#pragma unroll
+      for (int t = 0; t < 9; ++t)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const v4i v = red[((wave * 9 + t) * 4 + q) * 64 + lane];
+#pragma unroll
+          for (int k = 0; k < 4; ++k) acc[t][4 * q + k] += v[k];
+        }
+    }
+  }
+  if (wave != 0) return;
+  // lane: output channel o, input channels c0 + 8q + 4h .. +3 of each tap
+  const int o = obk * 32 + r32;
+  const bool part = a.partial != nullptr;
+  const float sc = part ? 0.0f : epilogue_scale<kAcLuq, NS, ASIGNED>(*a.alpha, *a.ascale);
+  const int64_t ncol = 9LL * a.C;
+  uint32_t* out = part ? reinterpret_cast<uint32_t*>(a.partial + (int64_t)range * a.Cout * ncol)
+                       : reinterpret_cast<uint32_t*>(a.dw);
+#pragma unroll
+  for (int t = 0; t < 9; ++t)
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      v4u v;
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        const int32_t x = acc[t][4 * q + k];
+        v[k] = part ? (uint32_t)x : __float_as_uint(__fmul_rn((float)x, sc));
+      }
+      uint32_t* dst = out + (int64_t)o * ncol + t * a.C + cbk * 32 + 8 * q + 4 * h;
+      if (a.vec) {
+        *reinterpret_cast<v4u*>(dst) = v;
+      } else {
+#pragma unroll
+        for (int k = 0; k < 4; ++k) dst[k] = v[k];
+      }
+    }
+}
+
+// rows per staged chunk: the gradient planes and the activation rows of a
+// chunk fit the kernel's LDS
+static int conv_wr_chunk_rows(int64_t W, int ns) {
+  int ch = 1;
+  while (4 * (ns * 32 * (wr_seg_dwords(ch + 1, (int)W) + 1) + 32 * (wr_seg_dwords(ch + 3, (int)W) + 1)) <=
+         kWrLdsBytes)
+    ++ch;
+  return ch;
+}
+
+// row ranges of the row form: about one workgroup per CU, and at most
+// kWrMaxPixels pixels per range (rows <= 0: an upper bound for any row count)
+static int64_t conv_wr_ranges(int64_t T, int64_t C, int64_t Cout, int64_t rows) {
+  const int64_t blocks = (C / 32) * (Cout / 32);
+  int64_t nr = 256 / blocks;
+  if (nr < 1) nr = 1;
+  const int64_t need = (T + kWrMaxPixels - 1) / kWrMaxPixels;
+  if (nr < need) nr = need;
+  if (rows > 0 && nr > rows) nr = rows;  // rows >= T / 64 >= need
+  return nr;
+}
+
+static bool conv_wr_eligible(int64_t W, int64_t C, int64_t Cout) {
+  return W >= 1 && W <= 64 && C % 32 == 0 && Cout % 32 == 0;
+}
+
 struct ConvWgPlan {
   int lg, nranges, nsplit;
 };
@@ -798,7 +1144,13 @@ static ConvWgPlan plan_conv_wgrad(int64_t T, int64_t C, int64_t Cout) {
 
 size_t conv3x3_wgrad_workspace_bytes(int64_t T, int64_t C, int64_t Cout) {
   const ConvWgPlan p = plan_conv_wgrad(T, C, Cout);
-  return p.nsplit > 1 ? (size_t)p.nsplit * (size_t)Cout * (size_t)(9 * C) * sizeof(int32_t) : 0;
+  int64_t parts = p.nsplit > 1 ? p.nsplit : 0;
+  // the row form (taken for W <= 64, which the workspace query does not see)
+  if (conv_wr_eligible(1, C, Cout)) {
+    const int64_t nr = conv_wr_ranges(T, C, Cout, 0);
+    if (nr > 1 && nr > parts) parts = nr;
+  }
+  return (size_t)parts * (size_t)Cout * (size_t)(9 * C) * sizeof(int32_t);
 }
 
 int64_t conv3x3_wgrad_blocks(int64_t T, int64_t C, int64_t Cout) {
@@ -814,6 +1166,16 @@ static void conv_wgrad_launch_t(const ConvWgArgs& a, unsigned blocks, hipStream_
     const int vec = (MN % 4) == 0;
     hipLaunchKernelGGL((conv_wgrad_reduce_kernel<NS, ASIGNED>), dim3((unsigned)((MN + 255) / 256)),
                        dim3(kRedThreads), 0, st, a.partial, a.nsplit, MN, vec, a.alpha, a.ascale, a.dw);
+  }
+}
+
+template <int NS, bool ASIGNED>
+static void conv_wr_launch_t(const ConvWrArgs& a, unsigned blocks, hipStream_t st) {
+  hipLaunchKernelGGL((conv3x3_wgrad_rows_kernel<NS, ASIGNED>), dim3(blocks), dim3(kWrThreads), 0, st, a);
+  if (a.partial) {
+    const int64_t MN = (int64_t)a.Cout * 9 * a.C;
+    hipLaunchKernelGGL((conv_wgrad_reduce_kernel<NS, ASIGNED>), dim3((unsigned)((MN + 255) / 256)),
+                       dim3(kRedThreads), 0, st, a.partial, a.nr, MN, 1, a.alpha, a.ascale, a.dw);
   }
 }
 
@@ -841,6 +1203,33 @@ hipError_t launch_conv3x3_wgrad(const uint8_t* g, int64_t g_plane, int ns, const
   a.nblk = 24 * ((p.nsplit + 7) / 8);
   a.ctiles = (int)((C + 63) / 64);
   a.vec = (C % 4) == 0 && (((uintptr_t)(a.partial ? (void*)a.partial : (void*)dw)) & 15) == 0;
+  if (conv_wr_eligible(W, C, Cout)) {
+    ConvWrArgs r;
+    r.g = g;
+    r.g_plane = g_plane;
+    r.a = act;
+    r.alpha = alpha;
+    r.ascale = ascale;
+    r.dw = dw;
+    r.T = (int)T;
+    r.H = (int)H;
+    r.W = (int)W;
+    r.C = (int)C;
+    r.Cout = (int)Cout;
+    r.rows = (int)(B * H);
+    r.nr = (int)conv_wr_ranges(T, C, Cout, B * H);
+    r.ch = conv_wr_chunk_rows(W, ns);
+    r.oblk = (int)(Cout / 32);
+    r.cblk = (int)(C / 32);
+    r.partial = r.nr > 1 ? static_cast<int32_t*>(ws) : nullptr;
+    r.vec = (((uintptr_t)(r.partial ? (void*)r.partial : (void*)dw)) & 15) == 0;
+    const unsigned blocks = (unsigned)((int64_t)r.nr * r.oblk * r.cblk);
+    if (ns == 1)
+      a_signed ? conv_wr_launch_t<1, true>(r, blocks, st) : conv_wr_launch_t<1, false>(r, blocks, st);
+    else
+      a_signed ? conv_wr_launch_t<2, true>(r, blocks, st) : conv_wr_launch_t<2, false>(r, blocks, st);
+    return hipGetLastError();
+  }
   const unsigned blocks = (unsigned)conv3x3_wgrad_blocks(T, C, Cout);
   if (ns == 1)
     a_signed ? conv_wgrad_launch_t<1, true>(a, blocks, st) : conv_wgrad_launch_t<1, false>(a, blocks, st);

@@ -195,6 +195,12 @@ def _wgrad_case(L, B, H, W, C, Cout, ns=1, asig=False, seed=0, R=4):
     (2, 3, 160, 8, 40),       # width above the 64-pixel window margin
     (16, 28, 28, 64, 64),     # several splits (split-K)
     (4, 256, 256, 8, 8),      # more pixel ranges than workgroups: some take two
+    # row form (W <= 64, channels in multiples of 32)
+    (2, 16, 7, 32, 32),       # odd width: every row starts at another nibble offset
+    (1, 64, 1, 32, 32),       # width 1: both column edges in one code
+    (8, 20, 36, 64, 64),      # row ranges of 2-3 rows that cross image borders
+    (2, 10, 64, 32, 96),      # width 64: two full k-steps, no padding columns
+    (3, 6, 48, 96, 32),       # the right edge column is the last code of a lane's 16
 ])
 @pytest.mark.parametrize("ns", [1, 2])
 def test_conv_wgrad_parity(L, B, H, W, C, Cout, ns):
@@ -209,15 +215,17 @@ def test_conv_wgrad_parity_wide_levels(L, B, H, W, C, Cout, R, ns):
 
 
 @pytest.mark.parametrize("R,ns", [(6, 1), (5, 2)])
-def test_conv_wgrad_largest_terms_many_pixels(L, R, ns):
+@pytest.mark.parametrize("B,H,W,C,Co", [(16, 256, 256, 384, 384), (32, 128, 64, 512, 512)])
+def test_conv_wgrad_largest_terms_many_pixels(L, R, ns, B, H, W, C, Co):
     """Every term at its largest magnitude, 64 * 120 in carrier units (a
     constant gradient puts every element on the top LUQ level, 2^6 in units
     of alpha for R = 6 and for the sum of two R = 5 samples; a constant
     activation gives the top unsigned INT4 code 15, carried as 8 * 15), over
     2^20 pixels and 6 x 6 channel tiles, so that few workgroups each sum
-    long pixel ranges.  The exact result has a closed form: tap (kh, kw)
-    gathers B (H - |kh - 1|) (W - |kw - 1|) products 2^6 * 15 in value units."""
-    B, H, W, C, Co = 16, 256, 256, 384, 384
+    long pixel ranges (the second shape takes the row form, whose 2^18 pixels
+    split into two row ranges of 2^17).  The exact result has a closed form:
+    tap (kh, kw) gathers B (H - |kh - 1|) (W - |kw - 1|) products 2^6 * 15
+    in value units."""
     T = B * H * W
     announce("conv3x3_wgrad largest terms", dict(T=T, C=C, Cout=Co, R=R, ns=ns))
     g = torch.full((T, Co), 1.0, dtype=torch.float32, device="cuda:0")
