@@ -274,6 +274,8 @@ def test_quantizer_workspace_holds_the_status_word():
     (1 << 22, 64, 64),
     (1 << 24, 256, 512),
     (1 << 29, 8, 8),
+    (1 << 29, 32, 32),           # row form: ranges forced by the int32 bound
+    (3 << 18, 512, 512),         # row form: one block set per range, several ranges
 ])
 def test_conv_wgrad_plan_keeps_int32_sums_exact(T, C, Cout):
     """The weight gradient's workgroups sum their pixel ranges in int32: for
@@ -282,7 +284,9 @@ def test_conv_wgrad_plan_keeps_int32_sums_exact(T, C, Cout):
     2^31 / 7680.  The split count comes from the workspace the plan asks for
     (one [Cout][9C] int32 slab per split); a workgroup then sums at most
     ceil(ranges / splits) ranges of 2 * lg <= 2560 pixels, i.e. fewer than
-    T / splits + 2 * 2560 pixels."""
+    T / splits + 2 * 2560 pixels.  The row form (W <= 64, channels in
+    multiples of 32) asks for one slab per row range and its ranges differ by
+    at most one row of <= 64 pixels, which the same bound covers."""
     ws = luq.workspace_size(luq.OP_CONV_WGRAD, T, C, Cout)
     slab = Cout * 9 * C * 4
     assert ws % slab == 0
