@@ -809,6 +809,10 @@ constexpr int64_t kWrMaxPixels = ((int64_t)1 << 18) - 64;
 // multiple of 4; the LDS pitch adds one dword so that channels fall in
 // different banks
 __host__ __device__ constexpr int wr_seg_dwords(int n, int W) { return ((n * W + 31 + 80) / 8 + 4 + 3) / 4 * 4; }
+// LDS pitch of a staged channel: at least seg dwords, 4 * (an odd number)
+__host__ __device__ constexpr int wr_pitch(int seg) { return (seg / 4) % 2 ? seg : seg + 4; }
+// s_waitcnt immediate (gfx9 encoding) of vmcnt(0) alone
+constexpr int kWaitVm0 = (0 & 15) | (7 << 4) | (15 << 8) | (0 << 14);
 
 struct ConvWrArgs {
   const uint8_t* g;      // LUQ codes [Cout][T], ns planes
@@ -880,46 +884,45 @@ __global__ __launch_bounds__(kWrThreads, 1) void conv3x3_wgrad_rows_kernel(ConvW
     const int nrow = min(a.ch, rr1 - cr0);
     // ---- stage the raw codes of the chunk: per channel, dwords from the
     // 16-byte block holding the first code; T is a multiple of 32, so every
-    // channel's block starts at the same offset of its row range
-    const int segg = wr_seg_dwords(nrow, a.W), sega = wr_seg_dwords(nrow + 2, a.W);
-    const int pg = segg + 1, pa = sega + 1;
-    uint32_t* ldsg = lds;                    // [NS][32][pg]
-    uint32_t* ldsa = lds + NS * 32 * pg;     // [32][pa]
+    // channel's block starts at the same offset of its row range.  Within an
+    // operand (a gradient plane, the activations) channels lie back to back
+    // at a pitch of 4 * (odd) dwords, so that the channels a k-step reads fall
+    // at most two to a bank; each operand starts on a 1 KB boundary.  Each
+    // wave instruction loads 64 consecutive 16-byte pieces of one operand
+    // straight into LDS.
+    const int pg = wr_pitch(wr_seg_dwords(nrow, a.W)), pa = wr_pitch(wr_seg_dwords(nrow + 2, a.W));
+    const int qg = pg / 4, qa = pa / 4;                 // pieces per channel
+    const int rg = (32 * qg + 63) / 64 * 64;            // pieces per gradient plane, whole wave loads
+    const int ra = (32 * qa + 63) / 64 * 64;
+    uint32_t* ldsg = lds;                               // plane p, channel k at 4 * (p * rg + k * qg)
+    uint32_t* ldsa = lds + 4 * NS * rg;                 // channel k at k * pa
     const int64_t g0 = ((int64_t)cr0 * a.W) >> 5 << 2;             // dword of row cr0's first code, 16-B block
     const int64_t a0 = ((int64_t)(cr0 - 1) * a.W - 1) >> 5 << 2;   // column -1 of row cr0 - 1 (floor)
     __syncthreads();  // the previous chunk is consumed
     {
-      // 16-byte pieces: NS * 32 gradient segments of qg, then 32 activation
-      // segments of qa; eight loads of a thread in flight before its stores
-      const int qg = segg / 4, qa = sega / 4;
-      const int ng = NS * 32 * qg, ntot = ng + 32 * qa;
-      constexpr int kBatch = 8;
-      for (int u0 = tid; u0 < ntot; u0 += kBatch * kWrThreads) {
-        v4u v[kBatch];
-        int dst[kBatch];
-#pragma unroll
-        for (int b = 0; b < kBatch; ++b) {
-          const int u = u0 + b * kWrThreads;
-          dst[b] = -1;
-          if (u < ng) {
-            const int p = u / (32 * qg), rem = u - p * 32 * qg, k = rem / qg, j = rem - k * qg;
-            const int64_t dwi = (int64_t)(obk * 32 + k) * (a.T >> 3) + g0 + 4 * j;
-            v[b] = __builtin_amdgcn_raw_buffer_load_b128(rsg[p == 0 ? 0 : NS - 1], (int)(dwi << 2), 0, 0);
-            dst[b] = (p * 32 + k) * pg + 4 * j;
-          } else if (u < ntot) {
-            const int rem = u - ng, k = rem / qa, j = rem - k * qa;
-            const int64_t dwi = (int64_t)(cbk * 32 + k) * (a.T >> 3) + a0 + 4 * j;
-            v[b] = __builtin_amdgcn_raw_buffer_load_b128(rsa, dwi < 0 ? kOutOfRange : (int)(dwi << 2), 0, 0);
-            dst[b] = NS * 32 * pg + k * pa + 4 * j;
-          }
+      const int ntot = NS * rg + ra;
+      for (int c0 = wave * 64; c0 < ntot; c0 += kWrThreads) {
+        uint32_t* dst = lds + 4 * c0;
+        if (c0 < NS * rg) {
+          const int pl = c0 >= rg ? 1 : 0;              // gradient plane (uniform)
+          const int u = c0 - pl * rg + lane;
+          const int k = u / qg, j = u - k * qg;
+          const int off = u < 32 * qg ? (int)((((int64_t)(obk * 32 + k) * (a.T >> 3)) + g0 + 4 * j) << 2)
+                                      : kOutOfRange;
+          // (a descriptor taken from the array inside the call drops the
+          // kernel's host stub: copy it first)
+          const __amdgpu_buffer_rsrc_t rsp = rsg[NS == 2 ? pl : 0];
+          __builtin_amdgcn_raw_ptr_buffer_load_lds(rsp, (__attribute__((address_space(3))) void*)dst, 16, off, 0, 0, 0);
+        } else {
+          const int u = c0 - NS * rg + lane;
+          const int k = u / qa, j = u - k * qa;
+          const int64_t dwi = (int64_t)(cbk * 32 + k) * (a.T >> 3) + a0 + 4 * j;
+          const int off = (u < 32 * qa && dwi >= 0) ? (int)(dwi << 2) : kOutOfRange;
+          __builtin_amdgcn_raw_ptr_buffer_load_lds(rsa, (__attribute__((address_space(3))) void*)dst, 16, off, 0, 0, 0);
         }
-#pragma unroll
-        for (int b = 0; b < kBatch; ++b)
-          if (dst[b] >= 0) {
-#pragma unroll
-            for (int e = 0; e < 4; ++e) lds[dst[b] + e] = v[b][e];
-          }
       }
+      // the loads into LDS are done before the barrier
+      __builtin_amdgcn_s_waitcnt(kWaitVm0);
     }
     __syncthreads();
 
@@ -930,6 +933,7 @@ __global__ __launch_bounds__(kWrThreads, 1) void conv3x3_wgrad_rows_kernel(ConvW
     const int n = r1 - r0, per = n + 2;
     const uint32_t* lg = ldsg + r32 * pg + 2 * h;
     const uint32_t* la = ldsa + r32 * pa + 2 * h;
+    const int gplane = 4 * rg;                          // dwords between gradient planes
     const int ga = (int)a0, gg = (int)g0;
     for (int kst = 0; kst < (n > 0 ? nk : 0); ++kst) {
       // code offsets (within a channel) of the window start and of the
@@ -939,15 +943,15 @@ __global__ __launch_bounds__(kWrThreads, 1) void conv3x3_wgrad_rows_kernel(ConvW
       int yy = r0 % a.H;  // image row of the next gradient row
       auto load = [&](Raw& R, int i) {
         if (i >= per) return;
-        const int qa = ((xa0 + i * a.W) >> 3) - ga;
+        const int wa = ((xa0 + i * a.W) >> 3) - ga;   // window's first dword in its channel
 #pragma unroll
-        for (int j = 0; j < 4; ++j) R.x[j] = la[qa + j];
+        for (int j = 0; j < 4; ++j) R.x[j] = la[wa + j];
         if (i >= 2) {
-          const int qg = ((xg0 + i * a.W) >> 3) - gg;
+          const int wg = ((xg0 + i * a.W) >> 3) - gg;
 #pragma unroll
           for (int p = 0; p < NS; ++p)
 #pragma unroll
-            for (int j = 0; j < 3; ++j) R.g[p][j] = lg[p * 32 * pg + qg + j];
+            for (int j = 0; j < 3; ++j) R.g[p][j] = lg[p * gplane + wg + j];
         }
       };
       // the three shifted activation fragments of a window
@@ -1093,10 +1097,14 @@ __global__ __launch_bounds__(kWrThreads, 1) void conv3x3_wgrad_rows_kernel(ConvW
 // rows per staged chunk: the gradient planes and the activation rows of a
 // chunk fit the kernel's LDS
 static int conv_wr_chunk_rows(int64_t W, int ns) {
+  // the staged pieces: each operand rounded up to whole wave loads of 64
+  auto bytes = [&](int n) {
+    const int rg = (32 * (wr_pitch(wr_seg_dwords(n, (int)W)) / 4) + 63) / 64 * 64;
+    const int ra = (32 * (wr_pitch(wr_seg_dwords(n + 2, (int)W)) / 4) + 63) / 64 * 64;
+    return 16 * (ns * rg + ra);
+  };
   int ch = 1;
-  while (4 * (ns * 32 * (wr_seg_dwords(ch + 1, (int)W) + 1) + 32 * (wr_seg_dwords(ch + 3, (int)W) + 1)) <=
-         kWrLdsBytes)
-    ++ch;
+  while (bytes(ch + 1) <= kWrLdsBytes) ++ch;
   return ch;
 }
 
