@@ -774,18 +774,19 @@ __global__ __launch_bounds__(kRedThreads) void conv_wgrad_reduce_kernel(const in
 // Weight gradient, row form (W <= 64, C and Cout multiples of 32).  A
 // workgroup owns one 32 x 32 (o, c) block of all nine taps over a range of
 // image rows; each of its eight waves keeps the nine accumulator tiles of
-// that block for its own run of rows, so every operand code is expanded
-// once per workgroup and the expanded operands never pass through LDS.
+// that block for its own run of rows, so an operand code is expanded once
+// per wave that reads it (the activation rows at the ends of a run by two
+// waves) and the expanded operands never pass through LDS.
 //
 // With r = b*H + y the flat image row and t = r*W + x, the tap (kh, kw) term
 // of pixel t reads the activation at flat row r + kh - 1, column x + kw - 1.
 // A row is multiplied as ceil(W / 32) k-steps of 32 columns (columns past W
 // carry zero gradient codes).  The raw codes of a chunk of rows (the
 // gradient rows, and the activation rows with one more on either side) are
-// staged in LDS by coalesced 16-byte loads, each channel's codes contiguous
-// as in memory.  In one k-step a lane takes 16 gradient codes of channel o
-// and, for each kernel row kh, the 16 activation codes of channel c at
-// columns x + kw - 1, cut by funnel shifts from one 4-dword window of that
+// staged in LDS by 16-byte loads that write LDS directly, each channel's
+// codes contiguous as in memory.  In one k-step a lane takes 16 gradient
+// codes of channel o and, for each kernel row kh, the 16 activation codes of
+// channel c at columns x + kw - 1, cut by funnel shifts from one 4-dword window of that
 // activation row: an activation row is read and expanded once per wave and
 // serves the three kernel rows of three consecutive gradient rows.  Column
 // x + kw - 1 off the row (x = 0 with kw = 0, x = W - 1 with kw = 2) is
