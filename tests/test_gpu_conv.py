@@ -201,6 +201,7 @@ def _wgrad_case(L, B, H, W, C, Cout, ns=1, asig=False, seed=0, R=4):
     (8, 20, 36, 64, 64),      # row ranges of 2-3 rows that cross image borders
     (2, 10, 64, 32, 96),      # width 64: two full k-steps, no padding columns
     (3, 6, 48, 96, 32),       # the right edge column is the last code of a lane's 16
+    (4, 70, 64, 256, 256),    # row ranges of 70 rows: two staged chunks (68 + 2, or 44 + 26 rows)
 ])
 @pytest.mark.parametrize("ns", [1, 2])
 def test_conv_wgrad_parity(L, B, H, W, C, Cout, ns):
