@@ -11,8 +11,10 @@
 // [Cout][3][3][C] in the transposed layout [9*C][Cout].  No lowered matrix
 // is formed: the output is T x C floats, not T x 9C.
 //
-// A tile is kBM consecutive pixels times 64 channels.  For each 64-deep chunk
-// of Cout a workgroup expands into LDS:
+// Tile form (any shape; images of at most 64 pixels with Cout 32 or 64 and C a
+// multiple of 32 take the row form further down): a tile is kBM consecutive
+// pixels times 64 channels.  For each 64-deep chunk of Cout a workgroup
+// expands into LDS:
 //   - the gradient codes of the tile's pixels and of the W + 1 pixels on
 //     either side (every tap of every pixel reads inside that halo, because a
 //     tap shifts the flat pixel index by (1 - kh) * W + (1 - kw)),
@@ -299,6 +301,219 @@ static void conv_launch_w(const ConvArgs& a, int wsigned, dim3 grid, hipStream_t
     hipLaunchKernelGGL((conv3x3_dgrad_kernel<MAXW, NS, false>), grid, dim3(kConvThreads), 0, st, a);
 }
 
+// ---------------------------------------------------------------------------
+// Activation gradient, row form (W <= 64, Cout 32 or 64, C a multiple of 32):
+// output image row (b, y) reads the gradient rows y - 1, y, y + 1 of its own
+// image and nothing else, so a workgroup walks a run of consecutive image
+// rows and keeps the expanded gradient codes of four rows in an LDS ring: the
+// three the current output row reads and the one being filled for the next.
+// Every code is expanded once per workgroup (the tile form expands the W + 1
+// pixels on either side of each tile again).  The weights of the workgroup's
+// channels (9 taps x Cout) are expanded once into registers, so LDS holds only
+// the ring (26 KB with its zero row) and up to four workgroups fit a CU.
+//
+// A wave owns 32 pixels of the row (one of its 32-pixel tiles) times 32
+// channels.  Per output row it reads one A fragment from the ring per (tap,
+// k-step) -- pixel x + 1 - kw of gradient row y + 1 - kh; a ring row carries a
+// zero pixel on either side of the image, and a kernel row off the image
+// reads an all-zero ring row -- and multiplies it with its weights.  The
+// output row goes from the accumulators straight to memory with ordinary
+// stores: each lane holds four consecutive channels of one pixel per register
+// quad, and a wave's four stores fill the 128 bytes of its channels of each
+// pixel.
+// ---------------------------------------------------------------------------
+constexpr int kDrThreads = 256;
+constexpr int kDrPitch = 80;                   // ring bytes per pixel (64 codes + 16 pad)
+constexpr int kDrSlot = 66 * kDrPitch;         // one ring row: pixels -1 .. 64
+constexpr int kDrSlots = 4;                    // ring rows, then one all-zero row
+constexpr int kDrAhead = 2;                    // gradient rows loaded ahead of their expansion
+
+struct ConvDrArgs {
+  const uint8_t* g;      // LUQ codes [T][Cout], ns planes
+  int64_t g_plane;
+  const uint8_t* w;      // INT4 codes [9*C][Cout]
+  const float* alpha;
+  const float* wscale;
+  float* dact;           // [T][C], 16-byte aligned
+  int rows, H, W, C;     // rows = B * H image rows
+  int npt;               // 32-pixel tiles per row: 1 or 2
+  int cblk;              // channels per workgroup, 32 * 4 / npt
+  int rq, rrem;          // rows per range: rq, and rq + 1 for the first rrem ranges
+};
+
+template <int NS, bool WSIGNED, int NK, int LA>
+__global__ __launch_bounds__(kDrThreads, 4) void conv3x3_dgrad_rows_kernel(ConvDrArgs a) {
+  __shared__ __attribute__((aligned(16))) uint8_t ring[(kDrSlots + 1) * kDrSlot];
+  constexpr int rowb = NK * 16;       // code bytes per pixel or weight row (Cout / 2)
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int pt = a.npt == 2 ? wave & 1 : 0;                 // pixel tile of the wave
+  const int cw = blockIdx.y * a.cblk + 32 * (a.npt == 2 ? wave >> 1 : wave);   // its first channel
+  const bool cact = cw < a.C;
+  // consecutive row ranges share gradient rows: give each XCD (blocks are
+  // dealt round-robin over the 8) a run of consecutive ranges
+  int L = blockIdx.x;
+  if ((gridDim.x & 7) == 0) L = (L & 7) * (gridDim.x >> 3) + (L >> 3);
+  // range L: rq rows, one more for the first rrem ranges
+  const int r0 = L * a.rq + min(L, a.rrem);
+  const int r1 = r0 + a.rq + (L < a.rrem ? 1 : 0);
+
+  __amdgpu_buffer_rsrc_t rsg[NS];
+#pragma unroll
+  for (int s = 0; s < NS; ++s)
+    rsg[s] = __builtin_amdgcn_make_buffer_rsrc((void*)(a.g + s * a.g_plane), (short)0, a.rows * a.W * rowb,
+                                               kBufferFlags);
+  const __amdgpu_buffer_rsrc_t rsw =
+      __builtin_amdgcn_make_buffer_rsrc((void*)a.w, (short)0, 9 * a.C * rowb, kBufferFlags);
+
+  // ---- the wave's weights as B fragments: lane l holds channel cw + l % 32
+  // and, for k-step kk, codes o = 32 kk + 16 (l / 32) .. + 15, expanded in the
+  // k order of the ring's rows (even-k nibbles of a raw word, then odd-k).
+  // Loaded here, expanded while the ring is cleared.
+  v4i fb[9][NK];
+  v2u32 wraw[9][NK];
+  {
+    const int c = cw + (lane & 31);
+#pragma unroll
+    for (int tap = 0; tap < 9; ++tap)
+#pragma unroll
+      for (int kk = 0; kk < NK; ++kk) {
+        const int off = cact ? (tap * a.C + c) * rowb + kk * 16 + (lane >> 5) * 8 : kOutOfRange;
+        wraw[tap][kk] = __builtin_amdgcn_raw_buffer_load_b64(rsw, off, 0, 0);
+      }
+  }
+
+  // ---- ring: row R sits in slot (R + 1) % 4 (R >= -1), pixel x at x + 1;
+  // pixel -1 and pixels W .. 64 of every slot, and all of slot 4, stay zero.
+  // A gradient row is W * NK pieces of 16 bytes (32 codes): thread tid loads
+  // and expands piece tid.  Every load and store of the row loop is issued
+  // unconditionally (out-of-range offsets where there is nothing to move), so
+  // that the compiler's waits for a row's codes count the stores issued after
+  // them exactly and never wait for those stores.
+  const int px = NK == 2 ? tid >> 1 : tid, hf = NK == 2 ? tid & 1 : 0;
+  const bool pact = tid < a.W * NK;
+  auto load_row = [&](int R, v4u (&v)[NS]) __attribute__((always_inline)) {
+    const bool in = pact && R >= 0 && R < a.rows && R <= r1;
+    const int off = in ? (R * a.W + px) * rowb + hf * 16 : kOutOfRange;
+#pragma unroll
+    for (int s = 0; s < NS; ++s) v[s] = __builtin_amdgcn_raw_buffer_load_b128(rsg[s], off, 0, 0);
+  };
+  auto put_row = [&](int R, const v4u (&v)[NS]) __attribute__((always_inline)) {
+    if (!pact) return;
+    uint32_t w[8];
+#pragma unroll
+    for (int d = 0; d < 4; ++d) {
+      if constexpr (NS == 1) {
+        expand_luq(v[0][d], w[2 * d], w[2 * d + 1]);
+      } else {
+        uint32_t l0, h0, l1, h1;
+        expand_luq_excess64(v[0][d], l0, h0);
+        expand_luq_excess64(v[1][d], l1, h1);
+        w[2 * d] = (l0 + l1) ^ 0x80808080u;
+        w[2 * d + 1] = (h0 + h1) ^ 0x80808080u;
+      }
+    }
+    uint4* dst = reinterpret_cast<uint4*>(ring + ((R + 1) & 3) * kDrSlot + (px + 1) * kDrPitch + hf * 32);
+    dst[0] = make_uint4(w[0], w[1], w[2], w[3]);
+    dst[1] = make_uint4(w[4], w[5], w[6], w[7]);
+  };
+
+  // rows R + 2 .. R + LA are loaded ahead, in register sets (row - r0) % LA
+  v4u ahead[LA][NS];
+  {
+    v4u v0[NS], v1[NS], v2[NS];
+    load_row(r0 - 1, v0);
+    load_row(r0, v1);
+    load_row(r0 + 1, v2);
+#pragma unroll
+    for (int k = 2; k <= LA; ++k) load_row(r0 + k, ahead[k % LA]);
+    // clear the ring while the loads are in flight
+    for (int i = tid; i < (kDrSlots + 1) * kDrSlot / 16; i += kDrThreads)
+      reinterpret_cast<uint4*>(ring)[i] = make_uint4(0, 0, 0, 0);
+#pragma unroll
+    for (int tap = 0; tap < 9; ++tap)
+#pragma unroll
+      for (int kk = 0; kk < NK; ++kk) {
+        uint32_t w0, w1, w2, w3;
+        expand_int4<WSIGNED>(wraw[tap][kk][0], w0, w1);
+        expand_int4<WSIGNED>(wraw[tap][kk][1], w2, w3);
+        fb[tap][kk] = v4i{(int)w0, (int)w1, (int)w2, (int)w3};
+      }
+    __syncthreads();
+    put_row(r0 - 1, v0);
+    put_row(r0, v1);
+    put_row(r0 + 1, v2);
+  }
+  __syncthreads();
+
+  const float sc = epilogue_scale<kAcLuq, NS, WSIGNED>(*a.alpha, *a.wscale);
+  const int x = 32 * pt + (lane & 31);
+  // the lane's A-fragment bytes at pixel x + 1 (kw = 0) of a ring row
+  const int abase = (x + 2) * kDrPitch + (lane >> 5) * 16;
+  // the lane's output bytes within an output row (four quads of channels)
+  const int obase = (cact && x < a.W) ? (x * a.C + cw + 4 * (lane >> 5)) * 4 : kOutOfRange;
+  const int orow = a.W * a.C;
+  int y = r0 % a.H;
+  // one output row; k = (R - r0) % LA selects the register sets
+  auto row = [&](int R, v4u (&put)[NS], v4u (&issue)[NS]) __attribute__((always_inline)) {
+    const bool live = R < r1;
+    load_row(R + LA + 1, issue);       // read by output row R + LA
+    v16i acc = v16i{};
+    if (live && cact) {
+#pragma unroll
+      for (int kh = 0; kh < 3; ++kh) {
+        // gradient row R + 1 - kh, or the zero row where it leaves the image
+        const bool off = (kh == 0 && y == a.H - 1) || (kh == 2 && y == 0);
+        const uint8_t* src = ring + (off ? kDrSlots : (R + 2 - kh) & 3) * kDrSlot + abase;
+        v4i fa[3][NK];
+#pragma unroll
+        for (int kw = 0; kw < 3; ++kw)
+#pragma unroll
+          for (int kk = 0; kk < NK; ++kk)
+            fa[kw][kk] = *reinterpret_cast<const v4i*>(src - kw * kDrPitch + kk * 32);
+#pragma unroll
+        for (int kw = 0; kw < 3; ++kw)
+#pragma unroll
+          for (int kk = 0; kk < NK; ++kk)
+            acc = __builtin_amdgcn_mfma_i32_32x32x32_i8(fb[kh * 3 + kw][kk], fa[kw][kk], acc, 0, 0, 0);
+      }
+    }
+    if (live && R + 2 <= r1) put_row(R + 2, put);   // read by output row R + 1
+    // the output row: each lane four quads of four consecutive channels
+    const __amdgpu_buffer_rsrc_t rso = __builtin_amdgcn_make_buffer_rsrc(
+        (void*)(a.dact + (int64_t)(live ? R : r0) * orow), (short)0, orow * 4, kBufferFlags);
+    const int o = live ? obase : kOutOfRange;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      v4u v;
+#pragma unroll
+      for (int k = 0; k < 4; ++k) v[k] = __float_as_uint(__fmul_rn((float)acc[4 * q + k], sc));
+      __builtin_amdgcn_raw_buffer_store_b128(v, rso, o + (o == kOutOfRange ? 0 : 32 * q), 0, 0);
+    }
+    y = y + 1 == a.H ? 0 : y + 1;
+    __syncthreads();
+  };
+  auto trip = [&](int R) __attribute__((always_inline)) {
+#pragma unroll
+    for (int k = 0; k < LA; ++k) row(R + k, ahead[(k + 2) % LA], ahead[(k + 1) % LA]);
+  };
+  // the first trip is peeled: the loop is then entered only from code that
+  // ends with a row's stores, as its back edge does, so the waits inside it
+  // are computed for the steady state
+  trip(r0);
+  for (int R = r0 + LA; R < r1; R += LA) trip(R);
+}
+
+static bool conv_dr_eligible(int64_t W, int64_t C, int64_t Cout, bool vec) {
+  return W <= 64 && (Cout == 32 || Cout == 64) && C % 32 == 0 && vec;
+}
+
+template <int NS, int NK>
+static void conv_dr_launch(const ConvDrArgs& d, int wsigned, dim3 grid, hipStream_t st) {
+  if (wsigned) hipLaunchKernelGGL((conv3x3_dgrad_rows_kernel<NS, true, NK, kDrAhead>), grid, dim3(kDrThreads), 0, st, d);
+  else hipLaunchKernelGGL((conv3x3_dgrad_rows_kernel<NS, false, NK, kDrAhead>), grid, dim3(kDrThreads), 0, st, d);
+}
+
 int conv3x3_max_width() { return 256; }
 
 hipError_t launch_conv3x3_dgrad(const uint8_t* g, int64_t g_plane, int ns, const float* alpha, const uint8_t* w,
@@ -318,6 +533,51 @@ hipError_t launch_conv3x3_dgrad(const uint8_t* g, int64_t g_plane, int ns, const
   a.Cout = (int)Cout;
   a.tiles_m = (a.T + kConvBM - 1) / kConvBM;
   a.vec = (C % 4) == 0 && (((uintptr_t)dact) & 15) == 0;
+  if (conv_dr_eligible(W, C, Cout, a.vec != 0)) {
+    ConvDrArgs d;
+    d.g = g;
+    d.g_plane = g_plane;
+    d.w = w;
+    d.alpha = alpha;
+    d.wscale = wscale;
+    d.dact = dact;
+    d.rows = (int)(B * H);
+    d.H = (int)H;
+    d.W = (int)W;
+    d.C = (int)C;
+    d.npt = W > 32 ? 2 : 1;
+    d.cblk = 32 * 4 / d.npt;
+    // row ranges: k = 1..4 workgroups per CU (four fit), the k that puts the
+    // fewest rows on the busiest CU (k workgroups of ceil(rows / ranges)
+    // rows), the larger k on a tie; a multiple of 8 ranges.  The ResNet layer
+    // (3584 rows) gets 512 ranges of 7 rows: 14.8 us against 16.3 with 1024
+    // ranges of 3 or 4 rows
+    const int cb = (int)((C + d.cblk - 1) / d.cblk);
+    int nr = 1;
+    int64_t best = -1;
+    for (int k = 1; k <= 4; ++k) {
+      int n = k * 256 / cb;
+      n = n < 8 ? 8 : n & ~7;
+      if (n > d.rows) n = d.rows;
+      const int64_t per_cu = ((int64_t)n * cb + 255) / 256;
+      const int64_t cost = per_cu * ((d.rows + n - 1) / n);
+      if (best < 0 || cost <= best) {
+        best = cost;
+        nr = n;
+      }
+    }
+    d.rq = d.rows / nr;
+    d.rrem = d.rows - d.rq * nr;
+    const dim3 grid((unsigned)nr, (unsigned)cb);
+    if (ns == 1) {
+      if (Cout == 64) conv_dr_launch<1, 2>(d, w_signed, grid, st);
+      else conv_dr_launch<1, 1>(d, w_signed, grid, st);
+    } else {
+      if (Cout == 64) conv_dr_launch<2, 2>(d, w_signed, grid, st);
+      else conv_dr_launch<2, 1>(d, w_signed, grid, st);
+    }
+    return hipGetLastError();
+  }
   // persistent workgroups: about two per CU (one for wide images), a multiple
   // of 8 wide, each taking tiles blockIdx.x, blockIdx.x + gridDim.x, ...
   const int ctiles = (int)((C + kConvBN - 1) / kConvBN);

@@ -12,7 +12,11 @@ counts that are not multiples of 64 (or of 4: scalar stores), Cout with a
 half-filled 64-deep chunk and several chunks, images narrower than a tile
 row and wider than 64 pixels (the wide-halo kernel), width and height 1, SMP
 planes, unsigned weights, and the full ResNet-50 layer (batch 64, 56 x 56,
-64 -> 64) on every pixel.
+64 -> 64) on every pixel.  The row form (image rows of at most 64 pixels,
+Cout 32 or 64, C a multiple of 32) gets its own shapes: one and two 32-pixel
+tiles per row (ragged or full), one or two k-steps per tap, idle waves and
+half-empty channel blocks, height and width 1, and row ranges of one row and
+of a few rows crossing image borders.
 """
 import numpy as np
 import pytest
@@ -88,13 +92,23 @@ def _conv_case(L, B, H, W, C, Cout, ns=1, wsig=True, seed=0, zero_grad=False, us
     (2, 45, 1, 16, 64),       # width 1
     (160, 32, 32, 8, 96),     # 640 tiles: workgroups walk two tiles, two Cout chunks each
     (8, 90, 100, 8, 96),      # wide-halo kernel with workgroups walking two tiles
+    # row form (W <= 64, Cout 32 or 64, C a multiple of 32)
+    (2, 9, 56, 64, 64),       # two pixel tiles per row, the second ragged
+    (3, 5, 64, 96, 32),       # width 64, one k-step per tap, a half-empty second channel block
+    (2, 7, 32, 128, 64),      # width 32: one pixel tile, four channel groups per workgroup
+    (1, 6, 20, 32, 32),       # one active wave of four
+    (3, 1, 40, 32, 64),       # height 1: both outer kernel rows off the image on every row
+    (2, 45, 1, 32, 64),       # width 1
+    (40, 3, 48, 64, 64),      # fewer rows than ranges: one row per workgroup
+    (64, 40, 8, 32, 32),      # 2560 rows: ranges of 2-3 rows that cross image borders
 ])
 @pytest.mark.parametrize("ns", [1, 2])
 def test_conv_dgrad_parity(L, B, H, W, C, Cout, ns):
     _conv_case(L, B, H, W, C, Cout, ns=ns, seed=B * 1000 + H * 100 + W + C + Cout)
 
 
-@pytest.mark.parametrize("B,H,W,C,Cout", [(2, 7, 9, 24, 64), (1, 6, 70, 8, 96)])
+@pytest.mark.parametrize("B,H,W,C,Cout", [(2, 7, 9, 24, 64), (1, 6, 70, 8, 96), (2, 9, 56, 64, 64),
+                                          (3, 4, 30, 64, 32)])
 def test_conv_dgrad_unsigned_weights(L, B, H, W, C, Cout):
     _conv_case(L, B, H, W, C, Cout, wsig=False, seed=17)
 
