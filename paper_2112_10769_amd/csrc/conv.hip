@@ -1302,50 +1302,38 @@ __global__ __launch_bounds__(kWrThreads, 1) void conv3x3_wgrad_rows_kernel(ConvW
     }
   }
 
-  // add the eight waves' tiles: 4 -> 2 -> 1 through LDS
-  v4i* red = reinterpret_cast<v4i*>(lds);   // [4][9][4][64]
-#pragma unroll
-  for (int half = kWrWaves / 2; half >= 1; half >>= 1) {
-    __syncthreads();  // the LDS is free (staging consumed, or the previous half read)
-    if (wave >= half && wave < 2 * half) {
-#pragma unroll
-      for (int t = 0; t < 9; ++t)
-#pragma unroll
-        for (int q = 0; q < 4; ++q)
-          red[(((wave - half) * 9 + t) * 4 + q) * 64 + lane] =
-              v4i{acc[t][4 * q], acc[t][4 * q + 1], acc[t][4 * q + 2], acc[t][4 * q + 3]};
-    }
-    __syncthreads();
-    if (wave < half) {
-#pragma unroll
-      for (int t = 0; t < 9; ++t)
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          const v4i v = red[((wave * 9 + t) * 4 + q) * 64 + lane];
-#pragma unroll
-          for (int k = 0; k < 4; ++k) acc[t][4 * q + k] += v[k];
-        }
-    }
-  }
-  if (wave != 0) return;
-  // lane: output channel o, input channels c0 + 8q + 4h .. +3 of each tap
-  const int o = obk * 32 + r32;
+  // add the eight waves' tiles through LDS in two rounds, each over half of
+  // the 36 (tap, quad) pairs (eight waves' halves fill the LDS): every wave
+  // writes its half, then every thread adds the eight values of its share of
+  // the round's outputs and stores them
+  v4i* red = reinterpret_cast<v4i*>(lds);   // [8][18][64]
+  constexpr int kHalfV4 = 18 * 64;          // one wave's half in 16-byte entries
   const bool part = a.partial != nullptr;
   const float sc = part ? 0.0f : epilogue_scale<kAcLuq, NS, ASIGNED>(*a.alpha, *a.ascale);
   const int64_t ncol = 9LL * a.C;
   uint32_t* out = part ? reinterpret_cast<uint32_t*>(a.partial + (int64_t)range * a.Cout * ncol)
                        : reinterpret_cast<uint32_t*>(a.dw);
 #pragma unroll
-  for (int t = 0; t < 9; ++t)
+  for (int r = 0; r < 2; ++r) {
+    __syncthreads();  // the staging is consumed, or the previous round read
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
+    for (int u = 0; u < 18; ++u) {
+      const int tq = 18 * r + u, t = tq >> 2, q = tq & 3;
+      red[(wave * 18 + u) * 64 + lane] = v4i{acc[t][4 * q], acc[t][4 * q + 1], acc[t][4 * q + 2], acc[t][4 * q + 3]};
+    }
+    __syncthreads();
+    // entry e = u * 64 + l: (tap, quad) pair 18r + u; output channel
+    // o = l % 32, input channels c0 + 8q + 4(l / 32) .. +3 of the tap
+    for (int e = tid; e < kHalfV4; e += kWrThreads) {
+      v4i s4 = red[e];
+#pragma unroll
+      for (int w = 1; w < kWrWaves; ++w) s4 += red[w * kHalfV4 + e];
+      const int tq = 18 * r + (e >> 6), t = tq >> 2, q = tq & 3, l = e & 63;
+      const int o = obk * 32 + (l & 31);
       v4u v;
 #pragma unroll
-      for (int k = 0; k < 4; ++k) {
-        const int32_t x = acc[t][4 * q + k];
-        v[k] = part ? (uint32_t)x : __float_as_uint(__fmul_rn((float)x, sc));
-      }
-      uint32_t* dst = out + (int64_t)o * ncol + t * a.C + cbk * 32 + 8 * q + 4 * h;
+      for (int k = 0; k < 4; ++k) v[k] = part ? (uint32_t)s4[k] : __float_as_uint(__fmul_rn((float)s4[k], sc));
+      uint32_t* dst = out + (int64_t)o * ncol + t * a.C + cbk * 32 + 8 * q + 4 * (l >> 5);
       if (a.vec) {
         *reinterpret_cast<v4u*>(dst) = v;
       } else {
@@ -1353,6 +1341,7 @@ __global__ __launch_bounds__(kWrThreads, 1) void conv3x3_wgrad_rows_kernel(ConvW
         for (int k = 0; k < 4; ++k) dst[k] = v[k];
       }
     }
+  }
 }
 
 // rows per staged chunk: the gradient planes and the activation rows of a

@@ -101,6 +101,8 @@ def _conv_case(L, B, H, W, C, Cout, ns=1, wsig=True, seed=0, zero_grad=False, us
     (2, 45, 1, 32, 64),       # width 1
     (40, 3, 48, 64, 64),      # fewer rows than ranges: one row per workgroup
     (64, 40, 8, 32, 32),      # 2560 rows: ranges of 2-3 rows that cross image borders
+    (256, 56, 8, 32, 32),     # 14336 rows in 1024 ranges: four workgroups per CU
+    (16, 30, 40, 96, 64),     # 480 rows, two channel blocks
 ])
 @pytest.mark.parametrize("ns", [1, 2])
 def test_conv_dgrad_parity(L, B, H, W, C, Cout, ns):
