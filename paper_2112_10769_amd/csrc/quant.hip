@@ -71,7 +71,7 @@ __device__ __forceinline__ uint32_t max_key8(const U8& v) {
 
 template <bool BF16, int MODE, bool NT>
 __global__ __launch_bounds__(kThreads) void max_partial_kernel(const void* __restrict__ x, int64_t n,
-                                                              uint32_t* __restrict__ partial) {
+                                                              uint32_t* __restrict__ partial, int64_t keep) {
   // groups of 8 elements per trip: eight 16-byte loads in flight per thread
   constexpr int G = BF16 ? 8 : 4;
   __shared__ uint32_t scratch[kThreads / kWave];
@@ -82,10 +82,10 @@ __global__ __launch_bounds__(kThreads) void max_partial_kernel(const void* __res
   for (int i = 0; i < G; ++i) m[i] = 0;
   int64_t g = (int64_t)blockIdx.x * kThreads + threadIdx.x;
   if constexpr (NT) {
-    // streamed tensor: all but its last kKeepBytes bypass the caches; that
+    // streamed tensor: all but its last keep bytes bypass the caches; that
     // tail, read last, is left in the last-level cache for the encode pass,
     // which starts there
-    const int64_t cut = ngroups - kKeepBytes / (BF16 ? 16 : 32);
+    const int64_t cut = ngroups - keep / (BF16 ? 16 : 32);
     for (; g + (G - 1) * stride < cut; g += G * stride) {
       U8 v[G];
 #pragma unroll
@@ -961,13 +961,13 @@ static TileShape tile_shape(int64_t rows, int64_t cols, int max_lt) {
 
 template <bool BF16, int MODE>
 static void launch_max_pass(const void* x, int64_t n, int nblocks, uint32_t* partial, hipStream_t st,
-                            int64_t stream_bytes = kCacheBytes) {
+                            int64_t stream_bytes = kCacheBytes, int64_t keep_bytes = kKeepBytes) {
   if (n * (BF16 ? 2 : 4) > stream_bytes)
     hipLaunchKernelGGL((max_partial_kernel<BF16, MODE, true>), dim3(nblocks), dim3(kThreads), 0, st, x, n,
-                       partial);
+                       partial, keep_bytes);
   else
     hipLaunchKernelGGL((max_partial_kernel<BF16, MODE, false>), dim3(nblocks), dim3(kThreads), 0, st, x, n,
-                       partial);
+                       partial, keep_bytes);
   if (nblocks > kDirectPartials)
     hipLaunchKernelGGL(fold_partials_kernel, dim3(1), dim3(1024), 0, st, partial, nblocks, partial + kMaxPartials);
 }
@@ -1012,7 +1012,16 @@ static int luq_encode_launch(const LuqArgs& a, int ns, hipStream_t st) {
 template <bool BF16>
 static hipError_t luq_launch_t(LuqArgs a, int ns, int nmax, hipStream_t st) {
   uint32_t* ws = const_cast<uint32_t*>(a.partial);
-  launch_max_pass<BF16, 0>(a.g, a.n, nmax, ws, st);
+  // a bf16 gradient too large to stay cached beside a training step's other
+  // data, but not streamed (kInt4StreamBytes .. kCacheBytes): the max pass
+  // reads all of it non-temporally.  Read through the cache, it would evict
+  // (and wait for the write-back of) the output the previous kernel left
+  // there; the encode, bound by its ALU work, reads it again from memory.
+  const int64_t bytes = a.n * (BF16 ? 2 : 4);
+  if (BF16 && bytes > kInt4StreamBytes && bytes <= kCacheBytes)
+    launch_max_pass<BF16, 0>(a.g, a.n, nmax, ws, st, 0, 0);
+  else
+    launch_max_pass<BF16, 0>(a.g, a.n, nmax, ws, st);
   a.partial = encode_partials(ws, nmax, &a.nparts);
   if (stream_reads(a.n, BF16))
     luq_encode_launch<BF16, true, false>(a, ns, st);
