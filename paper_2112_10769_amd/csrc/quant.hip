@@ -50,6 +50,9 @@ constexpr int64_t kKeepBytes = 192LL << 20;
 // INT4 tensors stream from a lower size: a tensor as large as the cache does not
 // stay in it beside the other data of a training step, and the INT4 encode is
 // bound by memory (the LUQ encode, bound by its ALU work, keeps kCacheBytes).
+// Their max pass keeps no tail cached: read through the cache, that tail
+// evicted (and waited for the write-back of) what the step's earlier kernels
+// left there.
 constexpr int64_t kInt4StreamBytes = 160LL << 20;
 
 // Max-pass keys.  MODE 0: |x| (LUQ, signed INT4).  MODE 1: max(x, 0) with
@@ -1167,9 +1170,9 @@ static hipError_t int4_launch_t(Int4Args a, hipStream_t st) {
   }
   if (a.clip <= 0.0f) {
     if (a.is_signed)
-      launch_max_pass<BF16, 0>(a.x, a.n, a.nparts, const_cast<uint32_t*>(a.partial), st, kInt4StreamBytes);
+      launch_max_pass<BF16, 0>(a.x, a.n, a.nparts, const_cast<uint32_t*>(a.partial), st, kInt4StreamBytes, 0);
     else
-      launch_max_pass<BF16, 1>(a.x, a.n, a.nparts, const_cast<uint32_t*>(a.partial), st, kInt4StreamBytes);
+      launch_max_pass<BF16, 1>(a.x, a.n, a.nparts, const_cast<uint32_t*>(a.partial), st, kInt4StreamBytes, 0);
     a.partial = encode_partials(a.partial, a.nparts, &a.nparts);
   }
   const bool nt = a.n * (BF16 ? 2 : 4) > kInt4StreamBytes;
